@@ -1,0 +1,396 @@
+"""Plain, slow, fp64 CPU oracle for Tangram's ragged paged attention path.
+
+TEST INFRASTRUCTURE ONLY.  Only tests/, __graft_entry__.smoke() and the
+cpu_baseline leg of bench.py may import or call this module.  It shares no
+code with the HIP/C++ library (paper_2606_06302_amd) and never imports it.
+
+Every function restates the method from the paper (Tangram, arXiv 2606.06302)
+in the paper's order and notation:
+
+  * retained_lengths  - Budget Reservation, Eq. 4: head (l, h) of a request with
+                        context N keeps ceil(B_{l,h} * N) entries.
+  * cluster_heads     - Budget-Aware Clustering, Section 4.2.2: sort the heads of
+                        each layer by budget, cut into groups of H_p.
+  * group_lengths     - Ragged Paging, Section 4.2.1: each group's page table is
+                        sized by its longest member.
+  * reserve           - Precise Page Allocation, Section 4.1: all pages are
+                        reserved once, at admission, from the free list.
+  * split_map         - Algorithm 1 (AOT Workload Partitioning).
+  * partition_plan    - Algorithm 1's proportional rule applied to one batch's
+                        integer retained lengths, then greedy longest-first
+                        assignment of the split chunks to persistent workgroups.
+  * decode_attention  - softmax attention of one query token per request over
+                        each KV head's retained rows (Eq. 1 with standard
+                        scaled-dot-product attention; grouped-query heads share
+                        a KV head, Section 2.1).
+  * merge_partials    - log-sum-exp merge of split-KV partial results
+                        (KV-dimension parallelism, Section 2.2.3).
+  * prefill_attention - chunked prefill (Section 2.2.1): a chunk attends to the
+                        compressed history of its head and, causally, to itself.
+
+Readings of points the paper leaves open (each also listed in the design doc):
+  - ceil(B*N) is the IEEE fp64 product followed by ceil, with no epsilon.
+  - Equal budgets keep ascending head order in the sort (a stable sort).
+  - Algorithm 1's round() is round-half-up, floor(x + 0.5), for x >= 0.
+  - Pages come off the front of the caller's free list in (request, layer,
+    group, page) order; a request that does not fit consumes nothing.
+  - A page stores [K|V][slot][token row][head_dim]; slot = a head's position in
+    its group.
+  - The work unit of the executed partition is (request, KV head); its split
+    count follows Algorithm 1's proportional rule on the batch's lengths.
+  - Softmax scale 1/sqrt(d) unless given.
+  - A prefill chunk sees all of its head's compressed history and, causally
+    and inclusively, its own (uncompressed) keys.
+"""
+from __future__ import annotations
+
+import heapq
+import math
+
+import numpy as np
+
+MODE_AOT, MODE_NAIVE, MODE_UNIFORM = 0, 1, 2
+GROUP_CLUSTERED, GROUP_ADJACENT = 0, 1
+
+
+class OracleError(ValueError):
+    pass
+
+
+class OutOfPages(OracleError):
+    pass
+
+
+def _check_ratio(r: float):
+    if not (r > 0.0 and r <= 1.0):          # also rejects NaN
+        raise OracleError(f"budget ratio {r!r} outside (0, 1]")
+
+
+# ----------------------------------------------------------------- Eq. 4
+
+def retained_lengths(ratio, ctx_len):
+    """Eq. 4: every (request b, layer l, KV head h) keeps ceil(r_{b,l,h} * N_b).
+
+    ratio: [B][L][H] float64 in (0, 1]; ctx_len: [B] ints >= 1.
+    Returns int64 [B][L][H].
+    """
+    ratio = np.asarray(ratio, dtype=np.float64)
+    Bn, L, H = ratio.shape
+    out = np.zeros((Bn, L, H), dtype=np.int64)
+    for b in range(Bn):
+        n = int(ctx_len[b])
+        if n < 1:
+            raise OracleError("context length must be >= 1")
+        for l in range(L):
+            for h in range(H):
+                r = float(ratio[b, l, h])
+                _check_ratio(r)
+                out[b, l, h] = math.ceil(r * n)      # one fp64 multiply, then ceil
+    return out
+
+
+# ------------------------------------------------- Section 4.2.2 clustering
+
+def cluster_heads(budget, heads_per_group, grouping=GROUP_CLUSTERED):
+    """Budget-Aware Clustering: pi_l sorts layer l's heads by ascending budget.
+
+    Group i of layer l holds pi_l(j) for j in [i*H_p, (i+1)*H_p).  Returns
+    (perm, group_of, slot_of), each int64 [L][H]; slot_of is a head's position
+    within its group.  grouping=GROUP_ADJACENT keeps pi_l = identity (the
+    paper's "adjacent" alternative in Algorithm 1's comment).
+    """
+    budget = np.asarray(budget, dtype=np.float64)
+    L, H = budget.shape
+    if heads_per_group < 1 or H % heads_per_group != 0:
+        raise OracleError("H must be a multiple of H_p")
+    perm = np.zeros((L, H), dtype=np.int64)
+    group_of = np.zeros((L, H), dtype=np.int64)
+    slot_of = np.zeros((L, H), dtype=np.int64)
+    for l in range(L):
+        for h in range(H):
+            _check_ratio(float(budget[l, h]))
+        if grouping == GROUP_CLUSTERED:
+            order = sorted(range(H), key=lambda h: (float(budget[l, h]), h))
+        elif grouping == GROUP_ADJACENT:
+            order = list(range(H))
+        else:
+            raise OracleError("unknown grouping")
+        for j, h in enumerate(order):
+            perm[l, j] = h
+            group_of[l, h] = j // heads_per_group
+            slot_of[l, h] = j % heads_per_group
+    return perm, group_of, slot_of
+
+
+# ------------------------------------------------- Section 4.2.1 ragged paging
+
+def group_lengths(kv_len, group_of, num_groups):
+    """A group's page table holds its longest member: GL = max_{h in g} kv_len."""
+    Bn, L, H = kv_len.shape
+    gl = np.zeros((Bn, L, num_groups), dtype=np.int64)
+    for b in range(Bn):
+        for l in range(L):
+            for h in range(H):
+                g = int(group_of[l, h])
+                gl[b, l, g] = max(gl[b, l, g], int(kv_len[b, l, h]))
+    return gl
+
+
+def reserve(ratio, ctx_len, group_of, num_groups, page_size, free_pages):
+    """Precise Page Allocation (Section 4.1) into per-group page tables.
+
+    Pages are taken from the front of free_pages in (b, l, g, page) order.  The
+    per-(b, l, g) tables are concatenated (the Vectorized Block Table, Section
+    4.2.3): table (b, l, g) is pages[offsets[(b*L+l)*G+g] : offsets[...+1]].
+    Raises OutOfPages, consuming nothing, when the list is too short.
+    """
+    kv_len = retained_lengths(ratio, ctx_len)
+    gl = group_lengths(kv_len, group_of, num_groups)
+    Bn, L, G = gl.shape
+    offsets = np.zeros(Bn * L * G + 1, dtype=np.int64)
+    k = 0
+    for b in range(Bn):
+        for l in range(L):
+            for g in range(G):
+                offsets[(b * L + l) * G + g] = k
+                k += -(-int(gl[b, l, g]) // page_size)     # ceil(GL / P) pages
+    offsets[-1] = k
+    free_pages = np.asarray(free_pages)
+    if k > len(free_pages):
+        raise OutOfPages(f"need {k} pages, {len(free_pages)} free")
+    pages = free_pages[:k].astype(np.int64).copy()
+    return dict(kv_len=kv_len, group_len=gl, offsets=offsets, pages=pages, pages_needed=k)
+
+
+def token_location(b, l, h, i, *, num_layers, num_groups, page_size, offsets, pages, group_of, slot_of):
+    """Physical (page id, slot, row) of retained entry i of head (b, l, h)."""
+    g = int(group_of[l, h])
+    table = int(offsets[(b * num_layers + l) * num_groups + g])
+    return int(pages[table + i // page_size]), int(slot_of[l, h]), i % page_size
+
+
+def gather_head(pool, b, l, h, t0, t1, *, geom, offsets, pages, group_of, slot_of):
+    """Retained K, V rows t0..t1-1 of head (b, l, h), upcast to fp64.
+
+    pool: [pool_pages][2][H_p][P][d] (any float dtype, numpy).
+    """
+    d = geom.head_dim
+    K = np.zeros((t1 - t0, d), dtype=np.float64)
+    V = np.zeros((t1 - t0, d), dtype=np.float64)
+    for i in range(t0, t1):
+        p, s, r = token_location(b, l, h, i, num_layers=geom.num_layers, num_groups=geom.num_groups,
+                                 page_size=geom.page_size, offsets=offsets, pages=pages,
+                                 group_of=group_of, slot_of=slot_of)
+        K[i - t0] = pool[p, 0, s, r].astype(np.float64)
+        V[i - t0] = pool[p, 1, s, r].astype(np.float64)
+    return K, V
+
+
+# ------------------------------------------------------------ Algorithm 1
+
+def split_map(budget, perm, heads_per_group, n_cta):
+    """Algorithm 1: S_{l,i} = max(1, round(Phi_{l,i} / tau_l)), tau_l = Omega_l / N_CTA."""
+    budget = np.asarray(budget, dtype=np.float64)
+    L, H = budget.shape
+    G = H // heads_per_group
+    S = np.ones((L, G), dtype=np.int64)
+    for l in range(L):
+        omega = 0.0
+        for h in range(H):
+            omega += float(budget[l, h])
+        if omega == 0.0:
+            continue
+        tau = omega / n_cta
+        for i in range(G):
+            phi = 0.0
+            for j in range(i * heads_per_group, (i + 1) * heads_per_group):
+                phi += float(budget[l, int(perm[l, j])])
+            S[l, i] = max(1, math.floor(phi / tau + 0.5))
+    return S
+
+
+# ------------------------------------------- executed partition for one layer
+
+def partition_plan(kv_len, offsets, group_of, slot_of, layer, *, num_layers, num_groups, page_size,
+                   mode=MODE_AOT, n_bins=1, split_target=1):
+    """Balanced split-KV partition of one layer of one batch.
+
+    Work unit u = (request b, KV head h), in order b, h.  In AOT mode unit u is
+    split into s_u = min(ceil(L_u/P), max(1, round_half_up(L_u * T / W)))
+    chunks (T = split_target, W = sum of the layer's lengths): Algorithm 1's
+    "CTAs proportional to budget share" rule on exact integer lengths.  Chunk c
+    covers pages [c*n//s, (c+1)*n//s) of the unit's n = ceil(L_u/P) pages.
+    Chunks are then placed longest-first, each on the currently least-loaded of
+    n_bins bins (ties: lowest bin).  NAIVE: one chunk per unit, one bin per
+    unit.  UNIFORM: every unit gets the same split count ceil(n_bins/units),
+    one bin per chunk.
+
+    Returns dict(items=[(pt_base, b, h, slot, t0, t1, out_idx)], bin_offsets,
+    unit_splits [B][H], unit_partial_base [B][H], num_partials, bin_load).
+    """
+    Bn, L, H = kv_len.shape
+    P = page_size
+    lens = [[int(kv_len[b, layer, h]) for h in range(H)] for b in range(Bn)]
+    W = sum(sum(r) for r in lens)
+    n_units = Bn * H
+    splits = np.zeros((Bn, H), dtype=np.int64)
+    for b in range(Bn):
+        for h in range(H):
+            n = -(-lens[b][h] // P)
+            if mode == MODE_AOT:
+                s = max(1, (2 * lens[b][h] * split_target + W) // (2 * W))
+            elif mode == MODE_NAIVE:
+                s = 1
+            elif mode == MODE_UNIFORM:
+                s = max(1, -(-n_bins // n_units))
+            else:
+                raise OracleError("unknown mode")
+            splits[b, h] = min(n, s)
+    base = np.full((Bn, H), -1, dtype=np.int64)
+    nparts = 0
+    for b in range(Bn):
+        for h in range(H):
+            if splits[b, h] > 1:
+                base[b, h] = nparts
+                nparts += int(splits[b, h])
+    chunks = []          # (t0, t1, b, h, c, item tuple)
+    for b in range(Bn):
+        for h in range(H):
+            n = -(-lens[b][h] // P)
+            s = int(splits[b, h])
+            g = int(group_of[layer, h])
+            pt_base = int(offsets[(b * num_layers + layer) * num_groups + g])
+            for c in range(s):
+                p0, p1 = c * n // s, (c + 1) * n // s
+                t0, t1 = p0 * P, min(p1 * P, lens[b][h])
+                out_idx = -1 if s == 1 else int(base[b, h]) + c
+                chunks.append((t0, t1, b, h, c, (pt_base, b, h, int(slot_of[layer, h]), t0, t1, out_idx)))
+    if mode == MODE_AOT:
+        order = sorted(chunks, key=lambda x: (-(x[1] - x[0]), x[2], x[3], x[4]))
+        heap = [(0, k) for k in range(n_bins)]
+        bins = [[] for _ in range(n_bins)]
+        for ch in order:
+            load, k = heapq.heappop(heap)
+            bins[k].append(ch[5])
+            heapq.heappush(heap, (load + (ch[1] - ch[0]), k))
+    else:
+        # NAIVE: one chunk per unit; UNIFORM: fixed split count.  Either way
+        # every chunk is its own bin, in (b, h, c) order.
+        bins = [[ch[5]] for ch in chunks]
+    items, bin_offsets, bin_load = [], [0], []
+    for blist in bins:
+        items.extend(blist)
+        bin_offsets.append(len(items))
+        bin_load.append(sum(it[5] - it[4] for it in blist))
+    return dict(items=items, bin_offsets=np.array(bin_offsets, dtype=np.int64),
+                unit_splits=splits, unit_partial_base=base, num_partials=nparts,
+                bin_load=np.array(bin_load, dtype=np.int64))
+
+
+# ------------------------------------------------------------- attention
+
+def attend(q_rows, K, V, scale):
+    """Softmax attention of query rows [m][d] over keys K [n][d], values V [n][d].
+
+    Returns (O [m][d], lse [m]) in fp64; lse is the natural-log normaliser of
+    the scaled logits.
+    """
+    z = (np.asarray(q_rows, dtype=np.float64) @ K.T) * scale          # [m][n]
+    m = z.max(axis=1, keepdims=True)
+    w = np.exp(z - m)
+    s = w.sum(axis=1, keepdims=True)
+    O = (w @ V) / s
+    lse = (m + np.log(s))[:, 0]
+    return O, lse
+
+
+def decode_attention(q, pool, layer, *, geom, batch, kv_len, offsets, pages, group_of, slot_of,
+                     sm_scale=0.0, heads=None):
+    """One decode step of layer `layer`: q [B][Hq][d] -> (O [B][Hq][d], lse [B][Hq]).
+
+    Query head qh reads KV head qh // gqa over its retained kv_len[b, layer, h]
+    rows.  `heads` optionally restricts the computation to a list of (b, kv_head)
+    pairs (the rest of O stays zero).
+    """
+    d, gqa = geom.head_dim, geom.gqa
+    scale = sm_scale if sm_scale != 0.0 else 1.0 / math.sqrt(d)
+    O = np.zeros((batch, geom.num_q_heads, d), dtype=np.float64)
+    lse = np.zeros((batch, geom.num_q_heads), dtype=np.float64)
+    todo = heads if heads is not None else [(b, h) for b in range(batch) for h in range(geom.num_kv_heads)]
+    for b, h in todo:
+        n = int(kv_len[b, layer, h])
+        K, V = gather_head(pool, b, layer, h, 0, n, geom=geom, offsets=offsets, pages=pages,
+                           group_of=group_of, slot_of=slot_of)
+        qs = slice(h * gqa, (h + 1) * gqa)
+        O[b, qs], lse[b, qs] = attend(q[b, qs], K, V, scale)
+    return O, lse
+
+
+def merge_partials(outs, lses):
+    """Log-sum-exp merge: lse* = log sum_i e^{lse_i}; O = sum_i e^{lse_i - lse*} o_i."""
+    lses = np.asarray(lses, dtype=np.float64)
+    outs = np.asarray(outs, dtype=np.float64)
+    m = lses.max(axis=0)
+    tot = m + np.log(np.exp(lses - m).sum(axis=0))
+    w = np.exp(lses - tot)
+    return (w[..., None] * outs).sum(axis=0), tot
+
+
+def decode_by_plan(q, pool, layer, plan, *, geom, batch, offsets, pages, group_of, slot_of, sm_scale=0.0):
+    """Evaluate decode attention chunk by chunk along a partition plan, then merge.
+
+    Split-KV with a log-sum-exp merge is algebraically exact, so this must
+    reproduce decode_attention up to fp64 rounding.
+    """
+    d, gqa = geom.head_dim, geom.gqa
+    scale = sm_scale if sm_scale != 0.0 else 1.0 / math.sqrt(d)
+    parts = {}
+    for (pt_base, b, h, slot, t0, t1, out_idx) in plan["items"]:
+        K, V = gather_head(pool, b, layer, h, t0, t1, geom=geom, offsets=offsets, pages=pages,
+                           group_of=group_of, slot_of=slot_of)
+        qs = slice(h * gqa, (h + 1) * gqa)
+        parts.setdefault((b, h), []).append((t0,) + attend(q[b, qs], K, V, scale))
+    O = np.zeros((batch, geom.num_q_heads, d))
+    lse = np.zeros((batch, geom.num_q_heads))
+    for (b, h), lst in parts.items():
+        lst.sort(key=lambda x: x[0])
+        qs = slice(h * gqa, (h + 1) * gqa)
+        O[b, qs], lse[b, qs] = merge_partials([x[1] for x in lst], [x[2] for x in lst])
+    return O, lse
+
+
+def prefill_attention(q, k_new, v_new, pool, layer, *, geom, kv_len, offsets, pages, group_of, slot_of,
+                      sm_scale=0.0, rows=None):
+    """Chunked-prefill attention.
+
+    q [B][C][Hq][d]; k_new, v_new [B][C][H][d].  Row i of chunk b for query
+    head qh (KV head h = qh // gqa) attends to the kv_len[b, layer, h] retained
+    history rows of h followed by chunk keys 0..i.  Returns O [B][C][Hq][d].
+    `rows` optionally restricts to a list of (b, qh) pairs.
+    """
+    Bn, C, Hq, d = q.shape
+    gqa = geom.gqa
+    scale = sm_scale if sm_scale != 0.0 else 1.0 / math.sqrt(d)
+    O = np.zeros((Bn, C, Hq, d), dtype=np.float64)
+    todo = rows if rows is not None else [(b, qh) for b in range(Bn) for qh in range(Hq)]
+    cache = {}
+    for b, qh in todo:
+        h = qh // gqa
+        if (b, h) not in cache:
+            n = int(kv_len[b, layer, h])
+            Kh, Vh = gather_head(pool, b, layer, h, 0, n, geom=geom, offsets=offsets, pages=pages,
+                                 group_of=group_of, slot_of=slot_of)
+            Kc = np.asarray(k_new[b, :, h], dtype=np.float64)
+            Vc = np.asarray(v_new[b, :, h], dtype=np.float64)
+            cache = {(b, h): (np.concatenate([Kh, Kc]), np.concatenate([Vh, Vc]), n)}
+        Kall, Vall, n = cache[(b, h)]
+        Q = np.asarray(q[b, :, qh], dtype=np.float64)                   # [C][d]
+        z = (Q @ Kall.T) * scale                                         # [C][n + C]
+        visible = np.ones_like(z, dtype=bool)
+        for i in range(C):
+            visible[i, n + i + 1:] = False                               # causal within the chunk
+        z = np.where(visible, z, -np.inf)
+        m = z.max(axis=1, keepdims=True)
+        w = np.exp(z - m)
+        O[b, :, qh] = (w @ Vall) / w.sum(axis=1, keepdims=True)
+    return O
