@@ -1,0 +1,216 @@
+#!/usr/bin/env python3
+"""Benchmark: one decode step of ragged paged attention over a compressed KV cache.
+
+Default workload: the Qwen2.5-32B-shaped multi-turn decode step (64 layers run
+back to back, batch 64, 64 query / 8 KV heads, head_dim 128, bf16, lognormal
+contexts with median 16384, 20 % of (layer, head) pairs retaining 60-100 % and
+the rest 3-15 %, page size 16, groups of 2 heads).  A step is the 64 per-layer
+tg_decode calls (split-KV attention + log-sum-exp merge) with every input
+already resident in HBM; host planning is done before the timed region and
+reported separately as plan_build_us.
+
+Prints ONE JSON line.  `value` is KV GB/s: the algorithmic retained-KV bytes
+of a step (sum over requests, layers and KV heads of kv_len * 2 * d * 2 bytes)
+divided by the measured step time.
+
+    python bench.py [--steps K] [--warmup W] [--config 3] [--mode aot|naive|uniform]
+    python bench.py --copy-probe BYTES     # plain copy kernel, for counter calibration
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+HBM_PEAK_GBS = 8000.0
+METRIC = "ragged paged decode attn: KV GB/s, % of HBM peak, µs/decode step"
+DECODE_SRC = os.path.join(ROOT, "paper_2606_06302_amd", "csrc", "tg_decode.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_traffic.json")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_sha():
+    h = hashlib.sha256()
+    for p in (DECODE_SRC, os.path.join(ROOT, "paper_2606_06302_amd", "csrc", "tg_device.h")):
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def copy_probe(nbytes):
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": nbytes}))
+
+
+def measured_traffic(workload, mode):
+    """HBM bytes per decode launch from committed rocprofv3 counter runs, if they
+    were taken on the current decode source; else None."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if rec.get("source_sha") != source_sha() or rec.get("workload") != workload or rec.get("mode") != mode:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(session, seconds, seed=7):
+    """The fp64 oracle on a bounded sample of the same workload, timed on the host."""
+    sys.path.insert(0, ROOT)
+    from threadpoolctl import threadpool_limits
+
+    import oracle
+    import torch
+    wl, t = session.wl, session.t
+    g = wl.geom
+    rng = np.random.default_rng(seed)
+    order = [(int(b), int(l)) for b, l in zip(rng.integers(0, wl.batch, 10**4), rng.choice(session.layers, 10**4))]
+    done_bytes, spent, pairs, max_abs = 0, 0.0, 0, 0.0
+    P, G, L = g.page_size, g.num_groups, g.num_layers
+    with threadpool_limits(limits=1):
+        for b, l in order:
+            if spent >= seconds:
+                break
+            heads = [(b, h) for h in range(g.num_kv_heads)]
+            # copy this request's pages of layer l back to the host (not timed)
+            need = []
+            for _, h in heads:
+                base = int(t.pt_offsets[(b * L + l) * G + t.group_of[l, h]])
+                need.append(t.pt_pages[base: base + (int(t.kv_len[b, l, h]) + P - 1) // P])
+            idx = np.unique(np.concatenate(need)).astype(np.int64)
+            sub = session.pool[torch.from_numpy(idx).cuda()].float().cpu().numpy().astype(np.float64)
+            remap = np.full(t.pool_pages, -1, dtype=np.int64)
+            remap[idx] = np.arange(len(idx))
+            q = session.q[l].float().cpu().numpy().astype(np.float64)
+            t0 = time.perf_counter()
+            O, _ = oracle.decode_attention(q, sub, l, geom=g, batch=wl.batch, kv_len=t.kv_len, offsets=t.pt_offsets,
+                                           pages=remap[t.pt_pages], group_of=t.group_of, slot_of=t.slot_of,
+                                           heads=heads)
+            spent += time.perf_counter() - t0
+            done_bytes += int(t.kv_len[b, l].sum()) * 2 * g.head_dim * (2 if wl.dtype == "bf16" else 4)
+            pairs += 1
+            got = session.out[l, b].float().cpu().numpy().astype(np.float64)
+            max_abs = max(max_abs, float(np.abs(got - O[b]).max()))
+    return {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{pairs} (request, layer) pairs x all {g.num_kv_heads} KV heads of the same workload, "
+                      f"{done_bytes / 1e9:.3f} GB of retained KV, {spent:.1f} s, BLAS pinned to 1 thread",
+            "gpu_vs_oracle_max_abs": max_abs}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--mode", default="aot", choices=["aot", "naive", "uniform"])
+    ap.add_argument("--n-bins", type=int, default=0)
+    ap.add_argument("--split-target", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.copy_probe:
+        copy_probe(args.copy_probe)
+        return
+
+    import torch
+    sys.path.insert(0, ROOT)
+    from paper_2606_06302_amd import tangram as tg
+    from paper_2606_06302_amd.runner import DecodeSession
+    from workloads import config
+
+    mode = {"aot": tg.TG_PLAN_AOT, "naive": tg.TG_PLAN_NAIVE, "uniform": tg.TG_PLAN_UNIFORM}[args.mode]
+    wl = config(args.config)
+    log(f"[bench] workload {wl.name}: building tables, plans and a "
+        f"{'device-filled' if args.config != 1 else 'host-filled'} pool")
+    t0 = time.perf_counter()
+    s = DecodeSession(wl, mode=mode, n_bins=args.n_bins or None, split_target=args.split_target or None,
+                      fill="host" if args.config == 1 else "device")
+    torch.cuda.synchronize()
+    log(f"[bench] setup {time.perf_counter() - t0:.1f} s: pool {s.t.pool_pages} pages "
+        f"({s.pool.numel() * s.pool.element_size() / 1e9:.1f} GB), n_bins {s.n_bins}, "
+        f"split_target {s.split_target}, plan build {s.plan_build_us / 1e3:.2f} ms")
+    g = wl.geom
+    kv_bytes_step = s.t.kv_bytes()
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            s.run_step(stream)
+        stream.synchronize()
+        log(f"[bench] warmup {args.warmup} steps done")
+        # whole-step timing
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(args.steps):
+            s.run_step(stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_per_step = e0.elapsed_time(e1) / args.steps
+        log(f"[bench] timed {args.steps} steps: {ms_per_step:.3f} ms/step")
+        # per-launch timing of the decode call (roofline), events on the launch stream
+        nrep = max(1, min(args.steps, 5))
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in s.layers]
+        lay_ms = np.zeros(len(s.layers))
+        for _ in range(nrep):
+            for i, l in enumerate(s.layers):
+                evs[i][0].record(stream)
+                s.run_layer(l, stream)
+                evs[i][1].record(stream)
+            torch.cuda.synchronize()
+            lay_ms += np.array([a.elapsed_time(b) for a, b in evs])
+        lay_ms /= nrep
+    launch_bytes = np.array([s.t.kv_bytes(l) for l in s.layers], dtype=np.float64)
+    achieved = float(launch_bytes.sum() / (lay_ms.sum() * 1e-3) / 1e9)
+    imb = [s.bin_load_stats(l) for l in s.layers]
+    planned_imbalance = float(np.mean([mx / mean for mx, mean in imb]))
+    value = kv_bytes_step / (ms_per_step * 1e-3) / 1e9
+    traffic = measured_traffic(wl.name, args.mode)
+    res = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": wl.dtype, "data": "synthetic",
+        "config": {"workload": wl.name, "layers": g.num_layers, "batch": wl.batch, "q_heads": g.num_q_heads,
+                   "kv_heads": g.num_kv_heads, "head_dim": g.head_dim, "page_size": g.page_size,
+                   "heads_per_group": g.heads_per_group, "plan": args.mode, "n_bins": s.n_bins,
+                   "split_target": s.split_target, "kv_bytes_per_step": kv_bytes_step,
+                   "parallelism": "single GPU"},
+        "us_per_step": round(ms_per_step * 1e3, 1),
+        "hbm_frac": round(value / HBM_PEAK_GBS, 4),
+        "plan_build_us": round(s.plan_build_us, 1),
+        "load_imbalance_planned": round(planned_imbalance, 4),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic,
+                     "kernel": "tg_decode (split-KV decode + merge) per layer",
+                     "avg_launch_us": round(float(lay_ms.mean()) * 1e3, 2),
+                     "algorithmic_bytes_per_launch": round(float(launch_bytes.mean()))},
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        log(f"[bench] cpu_baseline: oracle on a bounded sample (~{args.cpu_seconds:.0f} s)")
+        res["cpu_baseline"] = cpu_baseline(s, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,278 @@
+/*
+ * tangram.h - C ABI of libtangram.so: ragged paged attention over a
+ * non-uniformly compressed KV cache on AMD Instinct MI355X (gfx950).
+ *
+ * The calls follow the problem statement of Tangram (arXiv 2606.06302):
+ *   1. per-head budgets fix every head's retained length, and all pages are
+ *      reserved once, at admission, in per-group page tables
+ *      (Section 4.1 "Budget Reservation", Eq. 4; Section 4.2 "Ragged Paging");
+ *   2. heads are clustered by budget into groups of H_p (Section 4.2.2);
+ *   3. an ahead-of-time split map / balanced split-KV partition decides how
+ *      many workgroups each piece of work gets (Section 4.3, Algorithm 1);
+ *   4. ragged paged split-KV decode attention plus a log-sum-exp merge, and a
+ *      ragged chunked-prefill attention (Section 2.2, chunked prefill and
+ *      KV-dimension parallelism).
+ *
+ * Conventions
+ *   - Every function returns int32_t: TG_OK (0) or a negative TG_ERR_* code.
+ *     tg_last_error() returns a thread-local message describing the most
+ *     recent failure on the calling thread.
+ *   - The caller owns all memory.  Host calls write only into caller arrays.
+ *     Device calls take raw device pointers and a hipStream_t passed as
+ *     void*; they enqueue asynchronously, never synchronise, never allocate,
+ *     and take any scratch memory from a caller workspace whose size the
+ *     matching tg_*_workspace_bytes call reports.
+ *   - Arguments are validated on the host before anything is written or
+ *     enqueued.  On error nothing is written past what the error's
+ *     description says, and no page is consumed.
+ *   - Host integer calls are pure, deterministic and thread-safe.  The only
+ *     library state is a per-device cache of compute-unit counts.
+ *   - Physical page layout (Section 4.2.1: a page holds H_p x 2 x P x d
+ *     elements for the H_p heads of one group in one layer):
+ *         element (page p, kv in {0 = K, 1 = V}, slot s, row t, dim e) at
+ *         offset (((p*2 + kv)*H_p + s)*P + t)*d + e   (elements of `dtype`).
+ *     Retained entry i of head (b, l, h) lives in page
+ *     pt_pages[pt_offsets[(b*L + l)*G + group_of[l][h]] + i / P],
+ *     slot slot_of[l][h], row i % P.
+ */
+#ifndef TANGRAM_H
+#define TANGRAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ------------------------------------------------------------ status codes */
+enum {
+  TG_OK = 0,
+  TG_ERR_INVALID_ARG = -1,     /* malformed argument (bad ratio, shape, id ...) */
+  TG_ERR_OUT_OF_PAGES = -2,    /* free list shorter than the reservation needs */
+  TG_ERR_BUFFER_TOO_SMALL = -3,/* caller output / workspace buffer too small */
+  TG_ERR_UNSUPPORTED = -4,     /* valid but not implemented (head_dim, page size) */
+  TG_ERR_HIP = -5              /* a HIP runtime call or kernel launch failed */
+};
+
+/* storage / arithmetic types of Q, K, V and outputs */
+enum { TG_F32 = 0, TG_BF16 = 1 };
+/* head grouping for tg_cluster_heads */
+enum { TG_GROUP_CLUSTERED = 0, TG_GROUP_ADJACENT = 1 };
+/* partition modes for tg_build_plan */
+enum { TG_PLAN_AOT = 0, TG_PLAN_NAIVE = 1, TG_PLAN_UNIFORM = 2 };
+
+/* Model / cache geometry.  H = num_kv_heads (compression is per KV head,
+ * Section 2.1), G = H / heads_per_group groups per layer (must divide),
+ * gqa = num_q_heads / num_kv_heads query heads per KV head (must divide);
+ * query head qh reads KV head qh / gqa. */
+typedef struct {
+  int32_t num_layers;      /* L  >= 1 */
+  int32_t num_kv_heads;    /* H  >= 1 */
+  int32_t num_q_heads;     /* Hq >= H, multiple of H */
+  int32_t head_dim;        /* d */
+  int32_t page_size;       /* P tokens per page, >= 1 */
+  int32_t heads_per_group; /* H_p, divides H */
+} tg_geometry;
+
+const char* tg_status_string(int32_t code);   /* static string, never NULL */
+const char* tg_last_error(void);              /* thread-local, never NULL */
+int32_t     tg_version(void);                 /* (major << 16) | minor */
+
+/* --------------------------------------------- 1a. Budget-Aware Clustering
+ * Section 4.2.2.  For each layer l, pi_l is the permutation of the H heads by
+ * ascending budget (equal budgets keep ascending head index); group i holds
+ * pi_l(j) for j in [i*H_p, (i+1)*H_p).  grouping = TG_GROUP_ADJACENT uses
+ * pi_l = identity (the "adjacent" grouping that Algorithm 1 also admits).
+ *   budget   [L][H] float64, each in (0, 1]         (host, read)
+ *   perm     [L][H] int32 out: perm[l][j] = pi_l(j) (host, written)
+ *   group_of [L][H] int32 out: group of head h       (host, written)
+ *   slot_of  [L][H] int32 out: position of h in its group, 0..H_p-1
+ * Errors: TG_ERR_INVALID_ARG for a NULL pointer, bad geometry, H % H_p != 0,
+ * a budget outside (0, 1] or NaN, or an unknown grouping (nothing written). */
+int32_t tg_cluster_heads(const tg_geometry* geom, const double* budget, int32_t grouping,
+                         int32_t* perm, int32_t* group_of, int32_t* slot_of);
+
+/* ----------------------------- 1b. Budget Reservation + ragged page tables
+ * Eq. 4 and Section 4.1 ("Precise Page Allocation"), Section 4.2.1 and 4.2.3.
+ *   kv_len[b][l][h]    = ceil(r[b][l][h] * ctx_len[b])   (one fp64 multiply,
+ *                        then ceil; r = ratio, or budget broadcast if ratio is NULL)
+ *   group_len[b][l][g] = max over heads h of group g of kv_len[b][l][h]
+ *   table (b, l, g) holds ceil(group_len/P) pages; tables are concatenated in
+ *   (b, l, g) order into one CSR array (the Vectorized Block Table):
+ *   table (b, l, g) = pt_pages[pt_offsets[(b*L+l)*G+g] .. pt_offsets[...+1]).
+ *   Pages are taken from the front of free_pages in that order, so
+ *   pt_pages[k] == free_pages[k] for every k < pages_needed.
+ * Arguments (all host memory):
+ *   batch >= 1; ctx_len [B] int32 >= 1;
+ *   ratio [B][L][H] float64 in (0, 1], or NULL to use budget for every request;
+ *   budget [L][H] float64 in (0, 1] (read only when ratio is NULL);
+ *   group_of [L][H] int32 from tg_cluster_heads;
+ *   free_pages [num_free] int32; every id that gets consumed must be in
+ *   [0, pool_pages) and distinct;
+ *   kv_len [B][L][H] int32 out, group_len [B][L][G] int32 out,
+ *   pt_offsets [B*L*G+1] int64 out;
+ *   pt_pages [pt_capacity] int32 out, or NULL for a size query;
+ *   pages_needed int64 out (always written on TG_OK, and on
+ *   TG_ERR_OUT_OF_PAGES / TG_ERR_BUFFER_TOO_SMALL).
+ * Returns TG_OK; TG_ERR_OUT_OF_PAGES if num_free < pages_needed (real
+ * reservations only: a size query never examines the free list);
+ * TG_ERR_BUFFER_TOO_SMALL if pt_pages != NULL and pt_capacity < pages_needed;
+ * TG_ERR_INVALID_ARG for bad ratios / lengths / group ids, or consumed page
+ * ids that repeat or fall outside the pool.  With pt_pages == NULL the call
+ * writes kv_len, group_len, pt_offsets and pages_needed and consumes nothing.
+ * On any error pt_pages is left untouched. */
+int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_len,
+                   const double* ratio, const double* budget, const int32_t* group_of,
+                   const int32_t* free_pages, int64_t num_free, int64_t pool_pages,
+                   int32_t* kv_len, int32_t* group_len, int64_t* pt_offsets,
+                   int32_t* pt_pages, int64_t pt_capacity, int64_t* pages_needed);
+
+/* ------------------------------------------- 2a. AOT Workload Split Map
+ * Algorithm 1, arithmetic in fp64 in the paper's order:
+ *   Omega_l = sum_h B[l][h] (h ascending); tau_l = Omega_l / n_cta;
+ *   Phi_{l,i} = sum over j in [i*H_p, (i+1)*H_p) of B[l][perm[l][j]];
+ *   S[l][i] = max(1, floor(Phi_{l,i} / tau_l + 0.5))   (round half up).
+ *   budget [L][H] float64 in (0,1]; perm [L][H] from tg_cluster_heads;
+ *   n_cta >= 1; S [L][G] int32 out.  All host memory.
+ * Errors: TG_ERR_INVALID_ARG (nothing written). */
+int32_t tg_split_map(const tg_geometry* geom, const double* budget, const int32_t* perm,
+                     int32_t n_cta, int32_t* S);
+
+/* N_CTA of Section 4.3: the number of decode workgroups the device runs
+ * concurrently (HIP occupancy of the decode kernel for this geometry/dtype x
+ * compute-unit count of `device`).  n_cta out (host).  Errors:
+ * TG_ERR_UNSUPPORTED for shapes the decode kernel does not implement,
+ * TG_ERR_HIP if the device query fails. */
+int32_t tg_decode_max_ctas(const tg_geometry* geom, int32_t dtype, int32_t device, int32_t* n_cta);
+
+/* ------------------------------- 2b. balanced split-KV partition of a layer
+ * Algorithm 1's rule "workgroups proportional to budget share, at least one"
+ * applied to this batch's integer retained lengths, with work unit
+ * u = (request b, KV head h), units in order b, h.  All arithmetic is int64.
+ *   W = sum_u kv_len[b][layer][h];  n_u = ceil(kv_len/P) pages;
+ *   AOT:     s_u = min(n_u, max(1, floor((2*kv_len*split_target + W) / (2*W))))
+ *   NAIVE:   s_u = 1, and one bin per unit (n_bins ignored: B*H bins)
+ *   UNIFORM: s_u = min(n_u, max(1, ceil(n_bins / (B*H)))), one bin per chunk
+ *   chunk c < s_u of unit u covers pages [c*n_u/s_u, (c+1)*n_u/s_u) and tokens
+ *   [p0*P, min(p1*P, kv_len)).  out_idx = -1 when s_u == 1, else
+ *   unit_partial_base[u] + c (partials numbered over units in order).
+ *   AOT bins: chunks sorted by (length desc, b, h, c), each placed on the bin
+ *   with the least token load so far (ties: lowest bin), kept in placement
+ *   order within a bin.  Items are emitted bin by bin; bin k owns
+ *   items[bin_offsets[k] .. bin_offsets[k+1]).
+ * Arguments (host): kv_len [B][L][H] and pt_offsets [B*L*G+1] from tg_reserve;
+ *   group_of, slot_of [L][H]; 0 <= layer < L; n_bins >= 1 (AOT, UNIFORM);
+ *   split_target >= 1 (AOT); items [item_capacity] out, or NULL for a size
+ *   query (num_items, num_partials and the bin count are still written);
+ *   bin_offsets [bins+1] out, where bins = n_bins (AOT), B*H (NAIVE) or the
+ *   number of chunks (UNIFORM) - its capacity is bin_capacity entries;
+ *   unit_splits [B][H] out; unit_partial_base [B][H] out (-1 when unsplit);
+ *   num_items, num_bins, num_partials out.
+ * Errors: TG_ERR_INVALID_ARG; TG_ERR_BUFFER_TOO_SMALL when item_capacity <
+ * num_items or bin_capacity < bins + 1 (counts still written). */
+typedef struct {
+  int64_t pt_base;   /* pt_offsets[(b*L+layer)*G + group_of[layer][h]] */
+  int32_t b;         /* request */
+  int32_t kv_head;   /* h */
+  int32_t slot;      /* slot_of[layer][h] */
+  int32_t tok_begin; /* first retained entry, a multiple of P */
+  int32_t tok_end;   /* one past the last entry, <= kv_len */
+  int32_t out_idx;   /* -1: write the final output; else partial index */
+} tg_work_item;      /* 32 bytes */
+
+int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, const int32_t* kv_len,
+                      const int64_t* pt_offsets, const int32_t* group_of, const int32_t* slot_of,
+                      int32_t mode, int32_t n_bins, int32_t split_target,
+                      tg_work_item* items, int32_t item_capacity,
+                      int32_t* bin_offsets, int32_t bin_capacity,
+                      int32_t* unit_splits, int32_t* unit_partial_base,
+                      int32_t* num_items, int32_t* num_bins, int32_t* num_partials);
+
+/* ------------------------------------ 3. ragged paged decode attention
+ * One decode step of one layer (Section 2.2.3 split-KV decoding over the
+ * ragged cache of Section 4.2): for every request b and query head qh with
+ * KV head h = qh / gqa,
+ *   O[b][qh] = softmax(K_h q * sm_scale) V_h   over the retained rows of h,
+ * executed as the work items of a tg_build_plan partition.  Workgroup k
+ * runs the items of bin k; items with out_idx >= 0 write fp32 partial
+ * (o, lse) to the workspace and a merge pass combines the splits of each
+ * unit with a log-sum-exp merge.
+ * All pointers below are DEVICE pointers:
+ *   q        [B][Hq][d] dtype
+ *   kv_pool  [pool_pages][2][H_p][P][d] dtype (layout in the file header)
+ *   pt_pages CSR page ids (device copy of tg_reserve's output)
+ *   items [num_items], bin_offsets [n_bins+1], unit_splits [B][H],
+ *   unit_partial_base [B][H]: device copies of tg_build_plan's output
+ *   out      [B][Hq][d] dtype, written for every (b, qh)
+ *   lse      [B][Hq] float32 natural-log normaliser, or NULL
+ *   workspace >= tg_decode_workspace_bytes(geom, batch, num_partials) bytes
+ *   sm_scale: 0 means 1/sqrt(d).
+ * Supported: dtype TG_F32 or TG_BF16, head_dim 64 or 128, page_size 16,
+ * gqa 1..16 (else TG_ERR_UNSUPPORTED).  hip_stream is a hipStream_t (NULL =
+ * default stream).  Returns TG_ERR_HIP if a launch fails. */
+typedef struct {
+  tg_geometry geom;
+  int32_t batch;
+  int32_t dtype;
+  const void* q;
+  const void* kv_pool;
+  const int32_t* pt_pages;
+  const tg_work_item* items;
+  const int32_t* bin_offsets;
+  int32_t n_bins;
+  int32_t num_items;
+  const int32_t* unit_splits;
+  const int32_t* unit_partial_base;
+  int32_t num_partials;
+  void* out;
+  float* lse;
+  float sm_scale;
+  void* workspace;
+  size_t workspace_bytes;
+} tg_decode_args;
+
+size_t  tg_decode_workspace_bytes(const tg_geometry* geom, int32_t batch, int32_t num_partials);
+int32_t tg_decode(const tg_decode_args* args, void* hip_stream);
+
+/* ------------------------------- 4. ragged chunked-prefill attention (MFMA)
+ * Chunked prefill (Section 2.2.1) over the compressed history (Section 4.1):
+ * row i of request b's chunk, query head qh, KV head h = qh / gqa, attends to
+ * the kv_len[b][layer][h] retained history rows of h (all visible) followed by
+ * chunk keys 0..i (causal, inclusive).  No position encoding is applied
+ * (q and k are taken as already rotated).
+ * DEVICE pointers:
+ *   q     [B][C][Hq][d] bf16      k_new, v_new [B][C][H][d] bf16
+ *   kv_pool, pt_pages, pt_offsets [B*L*G+1] int64, kv_len [B][L][H] int32,
+ *   group_of, slot_of [L][H] int32   (device copies of the host tables)
+ *   out   [B][C][Hq][d] bf16
+ * Supported: dtype TG_BF16, head_dim 128, page_size 16, gqa 1..16,
+ * chunk_len >= 1.  The kernel needs no workspace (workspace may be NULL). */
+typedef struct {
+  tg_geometry geom;
+  int32_t batch;
+  int32_t chunk_len;
+  int32_t layer;
+  int32_t dtype;
+  const void* q;
+  const void* k_new;
+  const void* v_new;
+  const void* kv_pool;
+  const int32_t* pt_pages;
+  const int64_t* pt_offsets;
+  const int32_t* kv_len;
+  const int32_t* group_of;
+  const int32_t* slot_of;
+  void* out;
+  float sm_scale;
+  void* workspace;
+  size_t workspace_bytes;
+} tg_prefill_args;
+
+size_t  tg_prefill_workspace_bytes(const tg_prefill_args* args);
+int32_t tg_prefill(const tg_prefill_args* args, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TANGRAM_H */

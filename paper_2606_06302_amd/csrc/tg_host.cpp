@@ -1,0 +1,314 @@
+// Host integer half of libtangram.so: Budget-Aware Clustering, Budget
+// Reservation into ragged per-group page tables, Algorithm 1's split map and
+// the balanced split-KV partition plan.  Everything here is deterministic
+// integer (or exactly specified fp64) work on caller-owned host arrays.
+//
+// Must be compiled with -ffp-contract=off: the retained length is the IEEE
+// fp64 product ceil(r * N) and Algorithm 1's quotients are plain fp64 ops.
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <functional>
+#include <queue>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "tg_internal.h"
+
+namespace tg {
+
+static thread_local char g_last_error[512] = "";
+
+int32_t fail(int32_t code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int32_t check_geometry(const tg_geometry* g) {
+  if (!g) return fail(TG_ERR_INVALID_ARG, "geometry is NULL");
+  if (g->num_layers < 1 || g->num_kv_heads < 1 || g->num_q_heads < 1 || g->head_dim < 1 ||
+      g->page_size < 1 || g->heads_per_group < 1)
+    return fail(TG_ERR_INVALID_ARG, "geometry fields must be >= 1");
+  if (g->num_kv_heads % g->heads_per_group != 0)
+    return fail(TG_ERR_INVALID_ARG, "num_kv_heads (%d) is not a multiple of heads_per_group (%d)",
+                g->num_kv_heads, g->heads_per_group);
+  if (g->num_q_heads % g->num_kv_heads != 0)
+    return fail(TG_ERR_INVALID_ARG, "num_q_heads (%d) is not a multiple of num_kv_heads (%d)",
+                g->num_q_heads, g->num_kv_heads);
+  return TG_OK;
+}
+
+static bool ratio_ok(double r) { return r > 0.0 && r <= 1.0; }  // false for NaN
+
+}  // namespace tg
+
+using tg::ceil_div;
+using tg::fail;
+
+extern "C" {
+
+const char* tg_status_string(int32_t code) {
+  switch (code) {
+    case TG_OK: return "ok";
+    case TG_ERR_INVALID_ARG: return "invalid argument";
+    case TG_ERR_OUT_OF_PAGES: return "out of pages";
+    case TG_ERR_BUFFER_TOO_SMALL: return "buffer too small";
+    case TG_ERR_UNSUPPORTED: return "unsupported";
+    case TG_ERR_HIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+const char* tg_last_error(void) { return tg::g_last_error; }
+
+int32_t tg_version(void) { return (1 << 16) | 0; }
+
+// Section 4.2.2: sort each layer's heads by ascending budget (stable, so
+// equal budgets keep ascending head index) and cut into groups of H_p.
+int32_t tg_cluster_heads(const tg_geometry* geom, const double* budget, int32_t grouping,
+                         int32_t* perm, int32_t* group_of, int32_t* slot_of) {
+  if (int32_t rc = tg::check_geometry(geom)) return rc;
+  if (!budget || !perm || !group_of || !slot_of) return fail(TG_ERR_INVALID_ARG, "NULL array");
+  if (grouping != TG_GROUP_CLUSTERED && grouping != TG_GROUP_ADJACENT)
+    return fail(TG_ERR_INVALID_ARG, "unknown grouping %d", grouping);
+  const int L = geom->num_layers, H = geom->num_kv_heads, Hp = geom->heads_per_group;
+  for (int64_t i = 0; i < (int64_t)L * H; ++i)
+    if (!tg::ratio_ok(budget[i])) return fail(TG_ERR_INVALID_ARG, "budget[%lld] outside (0,1]", (long long)i);
+  std::vector<int32_t> order(H);
+  for (int l = 0; l < L; ++l) {
+    const double* bl = budget + (int64_t)l * H;
+    for (int h = 0; h < H; ++h) order[h] = h;
+    if (grouping == TG_GROUP_CLUSTERED)
+      std::stable_sort(order.begin(), order.end(), [bl](int32_t a, int32_t b) { return bl[a] < bl[b]; });
+    for (int j = 0; j < H; ++j) {
+      const int h = order[j];
+      perm[(int64_t)l * H + j] = h;
+      group_of[(int64_t)l * H + h] = j / Hp;
+      slot_of[(int64_t)l * H + h] = j % Hp;
+    }
+  }
+  return TG_OK;
+}
+
+// Eq. 4 + Section 4.1 (Precise Page Allocation) + Section 4.2.1/4.2.3.
+int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_len, const double* ratio,
+                   const double* budget, const int32_t* group_of, const int32_t* free_pages, int64_t num_free,
+                   int64_t pool_pages, int32_t* kv_len, int32_t* group_len, int64_t* pt_offsets,
+                   int32_t* pt_pages, int64_t pt_capacity, int64_t* pages_needed) {
+  if (int32_t rc = tg::check_geometry(geom)) return rc;
+  if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
+  if (!ctx_len || !group_of || !kv_len || !group_len || !pt_offsets || !pages_needed)
+    return fail(TG_ERR_INVALID_ARG, "NULL array");
+  if (!ratio && !budget) return fail(TG_ERR_INVALID_ARG, "ratio and budget are both NULL");
+  if (num_free < 0 || pool_pages < 0) return fail(TG_ERR_INVALID_ARG, "negative pool size");
+  if (num_free > 0 && !free_pages) return fail(TG_ERR_INVALID_ARG, "free_pages is NULL");
+  const int L = geom->num_layers, H = geom->num_kv_heads, G = H / geom->heads_per_group;
+  const int64_t P = geom->page_size;
+  for (int64_t i = 0; i < (int64_t)L * H; ++i)
+    if (group_of[i] < 0 || group_of[i] >= G) return fail(TG_ERR_INVALID_ARG, "group_of[%lld] out of range", (long long)i);
+  for (int b = 0; b < batch; ++b)
+    if (ctx_len[b] < 1) return fail(TG_ERR_INVALID_ARG, "ctx_len[%d] < 1", b);
+  // retained lengths first (validating every ratio before anything is written)
+  for (int b = 0; b < batch; ++b)
+    for (int64_t i = 0; i < (int64_t)L * H; ++i) {
+      const double r = ratio ? ratio[(int64_t)b * L * H + i] : budget[i];
+      if (!tg::ratio_ok(r)) return fail(TG_ERR_INVALID_ARG, "ratio of request %d entry %lld outside (0,1]", b, (long long)i);
+    }
+  for (int b = 0; b < batch; ++b) {
+    const double n = (double)ctx_len[b];
+    for (int64_t i = 0; i < (int64_t)L * H; ++i) {
+      const double r = ratio ? ratio[(int64_t)b * L * H + i] : budget[i];
+      kv_len[(int64_t)b * L * H + i] = (int32_t)std::ceil(r * n);
+    }
+  }
+  // group lengths and the CSR offsets of every (b, l, g) table
+  int64_t k = 0;
+  for (int b = 0; b < batch; ++b)
+    for (int l = 0; l < L; ++l) {
+      int32_t* gl = group_len + ((int64_t)b * L + l) * G;
+      for (int g = 0; g < G; ++g) gl[g] = 0;
+      const int32_t* kl = kv_len + ((int64_t)b * L + l) * H;
+      const int32_t* gof = group_of + (int64_t)l * H;
+      for (int h = 0; h < H; ++h) gl[gof[h]] = std::max(gl[gof[h]], kl[h]);
+      for (int g = 0; g < G; ++g) {
+        pt_offsets[((int64_t)b * L + l) * G + g] = k;
+        k += ceil_div(gl[g], P);
+      }
+    }
+  pt_offsets[(int64_t)batch * L * G] = k;
+  *pages_needed = k;
+  if (!pt_pages) return TG_OK;  // size query: nothing consumed, free list not examined
+  if (k > num_free) return fail(TG_ERR_OUT_OF_PAGES, "reservation needs %lld pages, %lld free", (long long)k, (long long)num_free);
+  if (pt_capacity < k) return fail(TG_ERR_BUFFER_TOO_SMALL, "pt_pages holds %lld, need %lld", (long long)pt_capacity, (long long)k);
+  // the consumed ids must be distinct pages of the pool
+  std::vector<uint8_t> seen((size_t)pool_pages, 0);
+  for (int64_t i = 0; i < k; ++i) {
+    const int32_t p = free_pages[i];
+    if (p < 0 || p >= pool_pages) return fail(TG_ERR_INVALID_ARG, "free_pages[%lld] = %d outside the pool", (long long)i, p);
+    if (seen[p]) return fail(TG_ERR_INVALID_ARG, "page id %d appears twice in the free list", p);
+    seen[p] = 1;
+  }
+  std::memcpy(pt_pages, free_pages, (size_t)k * sizeof(int32_t));
+  return TG_OK;
+}
+
+// Algorithm 1, fp64, in the paper's order of operations.
+int32_t tg_split_map(const tg_geometry* geom, const double* budget, const int32_t* perm, int32_t n_cta, int32_t* S) {
+  if (int32_t rc = tg::check_geometry(geom)) return rc;
+  if (!budget || !perm || !S) return fail(TG_ERR_INVALID_ARG, "NULL array");
+  if (n_cta < 1) return fail(TG_ERR_INVALID_ARG, "n_cta must be >= 1");
+  const int L = geom->num_layers, H = geom->num_kv_heads, Hp = geom->heads_per_group, G = H / Hp;
+  for (int64_t i = 0; i < (int64_t)L * H; ++i) {
+    if (!tg::ratio_ok(budget[i])) return fail(TG_ERR_INVALID_ARG, "budget[%lld] outside (0,1]", (long long)i);
+    if (perm[i] < 0 || perm[i] >= H) return fail(TG_ERR_INVALID_ARG, "perm[%lld] out of range", (long long)i);
+  }
+  for (int l = 0; l < L; ++l) {
+    std::vector<uint8_t> hit(H, 0);
+    for (int j = 0; j < H; ++j) {
+      if (hit[perm[(int64_t)l * H + j]]) return fail(TG_ERR_INVALID_ARG, "perm of layer %d is not a permutation", l);
+      hit[perm[(int64_t)l * H + j]] = 1;
+    }
+  }
+  for (int l = 0; l < L; ++l) {
+    const double* bl = budget + (int64_t)l * H;
+    int32_t* Sl = S + (int64_t)l * G;
+    double omega = 0.0;
+    for (int h = 0; h < H; ++h) omega += bl[h];
+    for (int i = 0; i < G; ++i) Sl[i] = 1;
+    if (omega == 0.0) continue;
+    const double tau = omega / (double)n_cta;
+    for (int i = 0; i < G; ++i) {
+      double phi = 0.0;
+      for (int j = i * Hp; j < (i + 1) * Hp; ++j) phi += bl[perm[(int64_t)l * H + j]];
+      const double s = std::floor(phi / tau + 0.5);
+      Sl[i] = s < 1.0 ? 1 : (int32_t)s;
+    }
+  }
+  return TG_OK;
+}
+
+// Balanced split-KV partition of one layer (Algorithm 1's rule on the batch).
+int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, const int32_t* kv_len,
+                      const int64_t* pt_offsets, const int32_t* group_of, const int32_t* slot_of, int32_t mode,
+                      int32_t n_bins, int32_t split_target, tg_work_item* items, int32_t item_capacity,
+                      int32_t* bin_offsets, int32_t bin_capacity, int32_t* unit_splits, int32_t* unit_partial_base,
+                      int32_t* num_items, int32_t* num_bins, int32_t* num_partials) {
+  if (int32_t rc = tg::check_geometry(geom)) return rc;
+  if (!kv_len || !pt_offsets || !group_of || !slot_of || !unit_splits || !unit_partial_base || !num_items ||
+      !num_bins || !num_partials)
+    return fail(TG_ERR_INVALID_ARG, "NULL array");
+  const int L = geom->num_layers, H = geom->num_kv_heads, Hp = geom->heads_per_group, G = H / Hp;
+  const int64_t P = geom->page_size;
+  if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
+  if (layer < 0 || layer >= L) return fail(TG_ERR_INVALID_ARG, "layer %d out of range", layer);
+  if (mode != TG_PLAN_AOT && mode != TG_PLAN_NAIVE && mode != TG_PLAN_UNIFORM)
+    return fail(TG_ERR_INVALID_ARG, "unknown plan mode %d", mode);
+  if (mode != TG_PLAN_NAIVE && n_bins < 1) return fail(TG_ERR_INVALID_ARG, "n_bins must be >= 1");
+  if (mode == TG_PLAN_AOT && split_target < 1) return fail(TG_ERR_INVALID_ARG, "split_target must be >= 1");
+  const int64_t n_units = (int64_t)batch * H;
+  // lengths of this layer, checked against the capacity of their table
+  std::vector<int64_t> len(n_units), base(n_units);
+  int64_t W = 0;
+  for (int b = 0; b < batch; ++b)
+    for (int h = 0; h < H; ++h) {
+      const int64_t u = (int64_t)b * H + h;
+      const int g = group_of[(int64_t)layer * H + h];
+      const int s = slot_of[(int64_t)layer * H + h];
+      if (g < 0 || g >= G || s < 0 || s >= Hp) return fail(TG_ERR_INVALID_ARG, "group_of/slot_of out of range");
+      const int64_t t = ((int64_t)b * L + layer) * G + g;
+      const int64_t cap = (pt_offsets[t + 1] - pt_offsets[t]) * P;
+      len[u] = kv_len[((int64_t)b * L + layer) * H + h];
+      if (len[u] < 1 || len[u] > cap)
+        return fail(TG_ERR_INVALID_ARG, "kv_len of request %d head %d (%lld) outside [1, table capacity %lld]", b, h,
+                    (long long)len[u], (long long)cap);
+      base[u] = pt_offsets[t];
+      W += len[u];
+    }
+  // split counts
+  std::vector<int64_t> splits(n_units);
+  int64_t total = 0, nparts = 0;
+  for (int64_t u = 0; u < n_units; ++u) {
+    const int64_t n = ceil_div(len[u], P);
+    int64_t s;
+    if (mode == TG_PLAN_AOT)
+      s = std::max<int64_t>(1, (2 * len[u] * (int64_t)split_target + W) / (2 * W));
+    else if (mode == TG_PLAN_NAIVE)
+      s = 1;
+    else
+      s = std::max<int64_t>(1, ceil_div(n_bins, n_units));
+    s = std::min(s, n);
+    splits[u] = s;
+    total += s;
+    unit_splits[u] = (int32_t)s;
+    unit_partial_base[u] = s > 1 ? (int32_t)nparts : -1;
+    if (s > 1) nparts += s;
+  }
+  const int64_t bins = mode == TG_PLAN_AOT ? n_bins : (mode == TG_PLAN_NAIVE ? n_units : total);
+  if (total > INT32_MAX || nparts > INT32_MAX) return fail(TG_ERR_INVALID_ARG, "plan too large");
+  *num_items = (int32_t)total;
+  *num_bins = (int32_t)bins;
+  *num_partials = (int32_t)nparts;
+  if (!items) return TG_OK;  // size query
+  if (!bin_offsets) return fail(TG_ERR_INVALID_ARG, "bin_offsets is NULL");
+  if (item_capacity < total) return fail(TG_ERR_BUFFER_TOO_SMALL, "items holds %d, need %lld", item_capacity, (long long)total);
+  if (bin_capacity < bins + 1) return fail(TG_ERR_BUFFER_TOO_SMALL, "bin_offsets holds %d, need %lld", bin_capacity, (long long)(bins + 1));
+
+  // chunks in (b, h, c) order
+  std::vector<tg_work_item> chunks;
+  chunks.reserve((size_t)total);
+  for (int b = 0; b < batch; ++b)
+    for (int h = 0; h < H; ++h) {
+      const int64_t u = (int64_t)b * H + h, n = ceil_div(len[u], P), s = splits[u];
+      for (int64_t c = 0; c < s; ++c) {
+        const int64_t p0 = c * n / s, p1 = (c + 1) * n / s;
+        tg_work_item it;
+        it.pt_base = base[u];
+        it.b = b;
+        it.kv_head = h;
+        it.slot = slot_of[(int64_t)layer * H + h];
+        it.tok_begin = (int32_t)(p0 * P);
+        it.tok_end = (int32_t)std::min(p1 * P, len[u]);
+        it.out_idx = s == 1 ? -1 : (int32_t)(unit_partial_base[u] + c);
+        chunks.push_back(it);
+      }
+    }
+  if (mode != TG_PLAN_AOT) {
+    // every chunk is its own bin, in (b, h, c) order
+    for (int64_t i = 0; i < total; ++i) {
+      items[i] = chunks[i];
+      bin_offsets[i] = (int32_t)i;
+    }
+    bin_offsets[total] = (int32_t)total;
+    return TG_OK;
+  }
+  // longest first; ties by (b, h, c), i.e. by position in `chunks`
+  std::vector<int32_t> order((size_t)total);
+  for (int64_t i = 0; i < total; ++i) order[i] = (int32_t)i;
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) {
+    return (chunks[a].tok_end - chunks[a].tok_begin) > (chunks[b].tok_end - chunks[b].tok_begin);
+  });
+  // greedy: least-loaded bin, ties to the lowest bin index
+  using Slot = std::pair<int64_t, int32_t>;
+  std::priority_queue<Slot, std::vector<Slot>, std::greater<Slot>> heap;
+  for (int32_t k = 0; k < n_bins; ++k) heap.push({0, k});
+  std::vector<int32_t> bin_of((size_t)total), count((size_t)n_bins, 0);
+  for (int64_t i = 0; i < total; ++i) {
+    Slot s = heap.top();
+    heap.pop();
+    const tg_work_item& c = chunks[order[i]];
+    bin_of[i] = s.second;
+    count[s.second] += 1;
+    heap.push({s.first + (c.tok_end - c.tok_begin), s.second});
+  }
+  bin_offsets[0] = 0;
+  for (int32_t k = 0; k < n_bins; ++k) bin_offsets[k + 1] = bin_offsets[k] + count[k];
+  std::vector<int32_t> fill(bin_offsets, bin_offsets + n_bins);
+  for (int64_t i = 0; i < total; ++i) items[fill[bin_of[i]]++] = chunks[order[i]];
+  return TG_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,117 @@
+"""Sets up one synthetic decode / prefill workload on the GPU and runs it through the C ABI.
+
+Plumbing only: the host tables come from libtangram's tg_cluster_heads /
+tg_reserve / tg_build_plan, device memory comes from torch, and every step of
+the attention runs in libtangram's HIP kernels.
+"""
+from __future__ import annotations
+
+import time
+
+import numpy as np
+import torch
+
+from . import tangram as tg
+from .device import bind_decode, to_device, upload_plan
+
+TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
+TG_DTYPE = {"f32": tg.TG_F32, "bf16": tg.TG_BF16}
+
+
+class Tables:
+    """Clustering + reservation of one workload (host arrays and device copies)."""
+
+    def __init__(self, wl, free_pages=None, pool_pages=None, grouping=tg.TG_GROUP_CLUSTERED, device="cuda"):
+        from workloads import free_list, pool_pages_for   # seeded inputs only
+        g = wl.geom
+        self.wl = wl
+        self.perm, self.group_of, self.slot_of = tg.tg_cluster_heads(g, wl.budget, grouping)
+        if free_pages is None:
+            need = tg.tg_reserve(g, wl.ctx_len, wl.ratio, None, self.group_of, np.zeros(0, np.int32), 0,
+                                 size_query=True)["pages_needed"]
+            pool_pages = pool_pages_for(need)
+            free_pages = free_list(wl, pool_pages)
+        self.pool_pages = int(pool_pages)
+        self.free_pages = np.asarray(free_pages, dtype=np.int32)
+        t0 = time.perf_counter()
+        res = tg.tg_reserve(g, wl.ctx_len, wl.ratio, None, self.group_of, self.free_pages, self.pool_pages)
+        self.reserve_us = (time.perf_counter() - t0) * 1e6
+        self.kv_len = res["kv_len"]
+        self.group_len = res["group_len"]
+        self.pt_offsets = res["pt_offsets"]
+        self.pt_pages = res["pt_pages"]
+        self.pages_needed = res["pages_needed"]
+        self.device = device
+        self.d_pt_pages = to_device(self.pt_pages if len(self.pt_pages) else np.zeros(1, np.int32), device)
+
+    def kv_bytes(self, layer=None) -> int:
+        """Algorithmic bytes of retained K and V (what the method must read)."""
+        g = self.wl.geom
+        esz = 4 if self.wl.dtype == "f32" else 2
+        kv = self.kv_len if layer is None else self.kv_len[:, layer]
+        return int(kv.sum()) * 2 * g.head_dim * esz
+
+
+class DecodeSession:
+    """Pool, queries, outputs and per-layer plans of one decode workload."""
+
+    def __init__(self, wl, tables: Tables = None, mode=tg.TG_PLAN_AOT, n_bins=None, split_target=None,
+                 fill="device", pool=None, q=None, want_lse=True, device="cuda", layers=None):
+        from workloads import S_POOL, S_Q, device_normal_, host_pool, host_q_decode, page_elems
+        g = wl.geom
+        self.wl, self.device = wl, device
+        self.t = tables if tables is not None else Tables(wl, device=device)
+        self.dtype = TORCH_DTYPE[wl.dtype]
+        self.tg_dtype = TG_DTYPE[wl.dtype]
+        if n_bins is None:
+            n_bins = tg.tg_decode_max_ctas(g, self.tg_dtype, torch.device(device).index or 0)
+        if split_target is None:
+            split_target = 4 * n_bins
+        self.mode, self.n_bins, self.split_target = mode, n_bins, split_target
+        L, B = g.num_layers, wl.batch
+        self.layers = list(range(L)) if layers is None else list(layers)
+        # plans (timed: this is the host planning cost the paper's Table 1 measures for a runtime planner)
+        t0 = time.perf_counter()
+        self.plans = {l: tg.tg_build_plan(g, B, l, self.t.kv_len, self.t.pt_offsets, self.t.group_of,
+                                          self.t.slot_of, mode, n_bins, split_target) for l in self.layers}
+        self.plan_build_us = (time.perf_counter() - t0) * 1e6
+        self.dplans = {l: upload_plan(g, B, p, device) for l, p in self.plans.items()}
+        # pool
+        if pool is not None:
+            self.pool = pool
+        elif fill == "host":
+            host = host_pool(wl, self.t.pool_pages)
+            self.pool = torch.from_numpy(host).to(self.dtype).to(device)
+        else:
+            self.pool = torch.empty(self.t.pool_pages * page_elems(g), dtype=self.dtype, device=device)
+            device_normal_(self.pool, wl, S_POOL, wl.kv_scale)
+        self.pool = self.pool.view(self.t.pool_pages, 2, g.heads_per_group, g.page_size, g.head_dim)
+        if q is not None:
+            self.q = q
+        elif fill == "host":
+            self.q = torch.from_numpy(host_q_decode(wl)).to(self.dtype).to(device)
+        else:
+            self.q = torch.empty(L, B, g.num_q_heads, g.head_dim, dtype=self.dtype, device=device)
+            device_normal_(self.q, wl, S_Q, wl.q_scale)
+        self.out = torch.zeros(L, B, g.num_q_heads, g.head_dim, dtype=self.dtype, device=device)
+        self.lse = torch.zeros(L, B, g.num_q_heads, dtype=torch.float32, device=device) if want_lse else None
+        for l in self.layers:
+            bind_decode(self.dplans[l], g, B, self.tg_dtype, self.q[l], self.pool, self.t.d_pt_pages, self.out[l],
+                        None if self.lse is None else self.lse[l])
+
+    def run_layer(self, l, stream=None):
+        tg.tg_decode(self.dplans[l].args, stream)
+
+    def run_step(self, stream=None):
+        for l in self.layers:
+            tg.tg_decode(self.dplans[l].args, stream)
+
+    def bin_load_stats(self, l):
+        """Planned token load per bin: (max, mean)."""
+        p = self.plans[l]
+        items = p["items"]
+        lens = (items["tok_end"] - items["tok_begin"]).astype(np.int64)
+        bo = p["bin_offsets"]
+        loads = np.zeros(len(bo) - 1, dtype=np.int64)
+        np.add.at(loads, np.repeat(np.arange(len(bo) - 1), np.diff(bo)), lens)
+        return float(loads.max()), float(loads.mean())

@@ -1,0 +1,189 @@
+"""Ragged paged decode attention on the GPU (through the C ABI) vs the fp64 oracle.
+
+Small cases compare every output element; the full-size workloads compare
+seeded samples of (request, KV head) pairs whose pages are copied back and run
+through the oracle one by one.  Unused pool rows are NaN in the small cases so
+any read outside a head's retained entries shows up as a non-finite output.
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_helpers import compare_layer, poisoned_host_pool, sample_pairs, say
+from workloads import Geometry, config, custom
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2606_06302_amd import tangram as tg
+    from paper_2606_06302_amd.runner import DecodeSession, Tables
+
+
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _small_session(wl, mode=0, n_bins=None, split_target=None, free_seed=None, poison=True):
+    tables = Tables(wl)
+    if free_seed is not None:
+        rng = np.random.default_rng(free_seed)
+        tables = Tables(wl, free_pages=rng.permutation(tables.pool_pages).astype(np.int32),
+                        pool_pages=tables.pool_pages)
+    pool = None
+    if poison:
+        pool = torch.from_numpy(poisoned_host_pool(wl, tables)).to({"f32": torch.float32,
+                                                                    "bf16": torch.bfloat16}[wl.dtype]).cuda()
+    s = DecodeSession(wl, tables=tables, mode=mode, n_bins=n_bins, split_target=split_target, fill="host",
+                      pool=pool)
+    s.run_step()
+    torch.cuda.synchronize()
+    return s
+
+
+@pytest.mark.parametrize("mode,n_bins,st", [(0, 8, 16), (0, 1, 1), (0, 512, 2048), (0, 3, 40), (1, None, None),
+                                            (2, 64, None)])
+def test_config1_tiny_fp32_all_plans(mode, n_bins, st):
+    _gpu()
+    wl = config(1)
+    say(f"config1 mode={mode} n_bins={n_bins} split_target={st}")
+    s = _small_session(wl, mode=mode, n_bins=n_bins or 8, split_target=st or 1)
+    compare_layer(s, 0, what=f"config1 mode {mode}")
+
+
+@pytest.mark.parametrize("dtype,d,gqa,Hp,H", [("bf16", 128, 4, 2, 8), ("bf16", 128, 8, 2, 8), ("bf16", 128, 1, 1, 4),
+                                              ("bf16", 128, 3, 2, 4), ("bf16", 64, 5, 4, 4), ("bf16", 128, 16, 2, 2),
+                                              ("f32", 128, 2, 2, 4), ("f32", 64, 7, 1, 2), ("bf16", 64, 2, 8, 8)])
+def test_shapes_vs_oracle(dtype, d, gqa, Hp, H):
+    _gpu()
+    g = Geometry(2, H, H * gqa, d, 16, Hp)
+    wl = custom(100 + d + gqa * 3 + Hp, g, 3, dtype, (40, 700), kv_scale=0.5)
+    say(f"shape dtype={dtype} d={d} gqa={gqa} Hp={Hp} H={H} ctx={wl.ctx_len.tolist()}")
+    s = _small_session(wl, n_bins=37, split_target=50)
+    for l in range(2):
+        compare_layer(s, l, what=f"{dtype} d{d} gqa{gqa} layer {l}")
+
+
+def test_config2_shape_scaled_plan_modes_agree():
+    _gpu()
+    g = Geometry(1, 8, 32, 128, 16, 2)
+    wl = custom(2002, g, 6, "bf16", 2048, kv_scale=0.5)
+    outs = []
+    for mode, nb, stg in [(0, 512, 2048), (0, 7, 9), (1, 1, 1), (2, 100, 1)]:
+        say(f"config2-scaled mode={mode} n_bins={nb}")
+        s = _small_session(wl, mode=mode, n_bins=nb, split_target=stg)
+        compare_layer(s, 0, what=f"mode {mode}")
+        outs.append(s.out.float().cpu())
+    for o in outs[1:]:
+        assert torch.allclose(o, outs[0], atol=2e-2, rtol=0)
+
+
+def test_single_retained_token_returns_value_exactly():
+    _gpu()
+    g = Geometry(1, 4, 8, 128, 16, 2)
+    wl = custom(77, g, 3, "bf16", (100, 900), budget=np.full((1, 4), 1e-6), jitter=0.0)
+    s = _small_session(wl, n_bins=5, split_target=5)
+    t = s.t
+    assert np.all(t.kv_len == 1)
+    out = s.out[0].cpu()
+    for b in range(wl.batch):
+        for h in range(4):
+            page = int(t.pt_pages[t.pt_offsets[b * 2 + t.group_of[0, h]]])
+            v = s.pool[page, 1, int(t.slot_of[0, h]), 0].cpu()
+            for j in range(2):
+                assert torch.equal(out[b, h * 2 + j], v), (b, h, j)
+
+
+def test_page_placement_invariance_is_bitwise():
+    _gpu()
+    g = Geometry(1, 8, 32, 128, 16, 2)
+    wl = custom(303, g, 4, "bf16", (500, 3000), kv_scale=0.5)
+    t1 = Tables(wl)
+    # same logical contents at a different physical placement
+    rng = np.random.default_rng(5)
+    free2 = rng.permutation(t1.pool_pages).astype(np.int32)
+    t2 = Tables(wl, free_pages=free2, pool_pages=t1.pool_pages)
+    pool1 = torch.from_numpy(poisoned_host_pool(wl, t1)).to(torch.bfloat16).cuda()
+    pool2 = torch.full_like(pool1, float("nan"))
+    pool2[torch.from_numpy(t2.pt_pages.astype(np.int64)).cuda()] = pool1[torch.from_numpy(t1.pt_pages.astype(np.int64)).cuda()]
+    s1 = DecodeSession(wl, tables=t1, n_bins=40, split_target=90, fill="host", pool=pool1)
+    s2 = DecodeSession(wl, tables=t2, n_bins=40, split_target=90, fill="host", pool=pool2)
+    s1.run_step()
+    s2.run_step()
+    torch.cuda.synchronize()
+    assert torch.equal(s1.out, s2.out)
+    compare_layer(s1, 0, what="placement")
+
+
+def test_empty_bins_and_single_bin():
+    _gpu()
+    g = Geometry(1, 2, 4, 128, 16, 1)
+    wl = custom(9, g, 1, "bf16", 300)
+    for nb, stg in [(1, 1), (300, 1), (300, 1000)]:
+        say(f"bins={nb} split_target={stg}")
+        s = _small_session(wl, n_bins=nb, split_target=stg)
+        compare_layer(s, 0, what=f"bins {nb}")
+
+
+def test_negative_controls_fail():
+    """Corrupting the page table or a length must break parity (the check is not vacuous)."""
+    _gpu()
+    g = Geometry(1, 8, 32, 128, 16, 2)
+    wl = custom(404, g, 4, "bf16", 4096, kv_scale=0.5, budget=np.full((1, 8), 0.5), jitter=0.0)
+    s = _small_session(wl, n_bins=64, split_target=64, poison=False)
+    compare_layer(s, 0, what="baseline")
+    # point request 0's first page at the last request's last page (a page of
+    # another table; swapping pages inside one table would only permute tokens)
+    good = s.t.d_pt_pages.clone()
+    bad = good.clone()
+    bad[[0, -1]] = good[[-1, 0]]
+    s.t.d_pt_pages.copy_(bad)
+    s.run_step()
+    torch.cuda.synchronize()
+    with pytest.raises(AssertionError):
+        compare_layer(s, 0, pairs=[(0, h) for h in range(8)], check_lse=False, what="swapped pages")
+    s.t.d_pt_pages.copy_(good)
+    # drop the last page of one head: plan from a shortened length
+    kv = s.t.kv_len.copy()
+    kv[1, 0, 3] -= 16
+    plan = tg.tg_build_plan(g, 4, 0, kv, s.t.pt_offsets, s.t.group_of, s.t.slot_of, 0, 64, 64)
+    from paper_2606_06302_amd.device import bind_decode, upload_plan
+    dp = upload_plan(g, 4, plan, "cuda")
+    bind_decode(dp, g, 4, tg.TG_BF16, s.q[0], s.pool, s.t.d_pt_pages, s.out[0], s.lse[0])
+    tg.tg_decode(dp.args)
+    torch.cuda.synchronize()
+    with pytest.raises(AssertionError):
+        compare_layer(s, 0, pairs=[(1, 3)], check_lse=False, what="short head")
+
+
+@pytest.mark.parametrize("cfg", [2, 4])
+def test_full_size_config_sampled(cfg):
+    _gpu()
+    wl = config(cfg)
+    say(f"config {cfg} full size: B={wl.batch} ctx range {wl.ctx_len.min()}..{wl.ctx_len.max()}")
+    for mode in (0, 1):
+        s = DecodeSession(wl, mode=mode)
+        s.run_step()
+        torch.cuda.synchronize()
+        pairs = sample_pairs(wl, 24, seed=cfg)
+        if cfg == 4:   # always include the longest unit
+            b = int(np.argmax(wl.ctx_len))
+            h = int(np.argmax(s.t.kv_len[b, 0]))
+            pairs = sorted(set(pairs) | {(b, h)})
+        compare_layer(s, 0, pairs=pairs, what=f"config {cfg} mode {mode}")
+        del s
+        torch.cuda.empty_cache()
+
+
+def test_full_size_config3_sampled():
+    _gpu()
+    wl = config(3)
+    say(f"config 3 full size: 64 layers, B=64")
+    s = DecodeSession(wl)
+    s.run_step()
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(33)
+    for layer in sorted(rng.choice(64, size=4, replace=False).tolist()):
+        compare_layer(s, layer, pairs=sample_pairs(wl, 10, seed=layer), what=f"config 3 layer {layer}")
+    del s
+    torch.cuda.empty_cache()
