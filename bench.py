@@ -123,6 +123,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0)
+    ap.add_argument("--free-order", default="shuffled", choices=["shuffled", "sequential"],
+                    help="order of the free page list (shuffled = seeded permutation of the pool)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path (asked for --gpus {args.gpus}).",
@@ -143,8 +145,13 @@ def main():
     log(f"[bench] workload {wl.name}: building tables, plans and a "
         f"{'device-filled' if args.config != 1 else 'host-filled'} pool")
     t0 = time.perf_counter()
-    s = DecodeSession(wl, mode=mode, n_bins=args.n_bins or None, split_target=args.split_target or None,
-                      fill="host" if args.config == 1 else "device")
+    tables = None
+    if args.free_order == "sequential":
+        from paper_2606_06302_amd.runner import Tables
+        t0_ = Tables(wl)
+        tables = Tables(wl, free_pages=np.arange(t0_.pool_pages, dtype=np.int32), pool_pages=t0_.pool_pages)
+    s = DecodeSession(wl, tables=tables, mode=mode, n_bins=args.n_bins or None,
+                      split_target=args.split_target or None, fill="host" if args.config == 1 else "device")
     torch.cuda.synchronize()
     log(f"[bench] setup {time.perf_counter() - t0:.1f} s: pool {s.t.pool_pages} pages "
         f"({s.pool.numel() * s.pool.element_size() / 1e9:.1f} GB), n_bins {s.n_bins}, "
@@ -193,6 +200,7 @@ def main():
                    "kv_heads": g.num_kv_heads, "head_dim": g.head_dim, "page_size": g.page_size,
                    "heads_per_group": g.heads_per_group, "plan": args.mode, "n_bins": s.n_bins,
                    "split_target": s.split_target, "kv_bytes_per_step": kv_bytes_step,
+                   "free_order": args.free_order,
                    "parallelism": "single GPU"},
         "us_per_step": round(ms_per_step * 1e3, 1),
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),

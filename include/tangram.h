@@ -194,9 +194,10 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
  * ragged cache of Section 4.2): for every request b and query head qh with
  * KV head h = qh / gqa,
  *   O[b][qh] = softmax(K_h q * sm_scale) V_h   over the retained rows of h,
- * executed as the work items of a tg_build_plan partition.  Workgroup k
- * runs the items of bin k; items with out_idx >= 0 write fp32 partial
- * (o, lse) to the workspace and a merge pass combines the splits of each
+ * executed as the work items of a tg_build_plan partition: workgroup k of
+ * the decode launch runs the items of bin k; an item with out_idx >= 0
+ * writes an fp32 partial (o, lse) to the workspace, and a second launch on the
+ * same stream (only when num_partials > 0) merges the partials of every split
  * unit with a log-sum-exp merge.
  * All pointers below are DEVICE pointers:
  *   q        [B][Hq][d] dtype
@@ -207,6 +208,8 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
  *   out      [B][Hq][d] dtype, written for every (b, qh)
  *   lse      [B][Hq] float32 natural-log normaliser, or NULL
  *   workspace >= tg_decode_workspace_bytes(geom, batch, num_partials) bytes
+ *            (fp32 partials; no initialisation needed).  Calls that share a
+ *            workspace must not overlap in time.
  *   sm_scale: 0 means 1/sqrt(d).
  * Supported: dtype TG_F32 or TG_BF16, head_dim 64 or 128, page_size 16,
  * gqa 1..16 (else TG_ERR_UNSUPPORTED).  hip_stream is a hipStream_t (NULL =

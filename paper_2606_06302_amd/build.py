@@ -29,6 +29,8 @@ HIP_FLAGS = [
     # no packed-fp32 instructions anywhere in the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-ffp-contract=fast", "-munsafe-fp-atomics",
+    # LDS staging buffers are reinterpreted between 16-, 32- and 128-bit views
+    "-fno-strict-aliasing",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-ffp-contract=off", "-Wall", "-Wextra",
