@@ -330,9 +330,9 @@ __device__ __forceinline__ Stage<SP> fetch_step(const DecodeParams& p, const u4*
     const u4* kb = base + slot * 256 + lane;
     const u4* vb = base + (p.heads_per_group + slot) * 256 + lane;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      s.k[q * 4 + j] = kb[j * 64];
-      s.v[q * 4 + j] = vb[j * 64];
+    for (int j = 0; j < 4; ++j) {   // streamed once: non-temporal
+      s.k[q * 4 + j] = __builtin_nontemporal_load(kb + j * 64);
+      s.v[q * 4 + j] = __builtin_nontemporal_load(vb + j * 64);
     }
   }
   return s;
@@ -561,9 +561,10 @@ __global__ void __launch_bounds__(kBlock) tg_decode_fast_kernel(DecodeParams p, 
 constexpr int kFastStep = 2;   // pages per wave step in the fast path
 
 // Log-sum-exp merge of the split partials of every unit (b, h) with more than
-// one split: lse* = log sum_i e^{lse_i}, O = sum_i e^{lse_i - lse*} o_i.  One
-// workgroup per unit; a single pass with a running max, so the partial loads
-// of consecutive splits are independent.
+// one split: lse* = log sum_i e^{lse_i}, O = sum_i e^{lse_i - lse*} o_i.
+// Grid (units, ceil(gqa*D / 256)): each thread owns one output element and
+// makes a single pass with a running max, so the loads of consecutive splits
+// are independent and issue back to back.
 template <typename T, int D>
 __global__ void __launch_bounds__(kBlock) tg_merge_kernel(const int32_t* __restrict__ unit_splits,
                                                          const int32_t* __restrict__ unit_base,
@@ -572,28 +573,27 @@ __global__ void __launch_bounds__(kBlock) tg_merge_kernel(const int32_t* __restr
                                                          int32_t num_kv_heads, int32_t gqa) {
   const int u = blockIdx.x;
   const int s = unit_splits[u];
-  if (s <= 1) return;
+  const int o = blockIdx.y * kBlock + threadIdx.x;
+  if (s <= 1 || o >= gqa * D) return;
   const int base = unit_base[u];
   const int b = u / num_kv_heads, h = u % num_kv_heads;
   const int64_t row0 = (int64_t)b * num_kv_heads * gqa + (int64_t)h * gqa;
-  for (int o = threadIdx.x; o < gqa * D; o += kBlock) {
-    const int g = o / D, e = o % D;
-    const float* pl = part_lse + (int64_t)base * gqa + g;
-    const float* po = part_o + ((int64_t)base * gqa + g) * D + e;
-    float m = -INFINITY, L = 0.f, A = 0.f;
+  const int g = o / D, e = o % D;
+  const float* pl = part_lse + (int64_t)base * gqa + g;
+  const float* po = part_o + ((int64_t)base * gqa + g) * D + e;
+  float m = -INFINITY, L = 0.f, A = 0.f;
 #pragma unroll 8
-    for (int i = 0; i < s; ++i) {
-      const float li = pl[(int64_t)i * gqa];
-      const float oi = po[(int64_t)i * gqa * D];
-      const float mn = fmaxf(m, li);
-      const float a = __expf(m - mn), w = __expf(li - mn);
-      L = fmaf(L, a, w);
-      A = fmaf(A, a, w * oi);
-      m = mn;
-    }
-    store_out<T>(static_cast<T*>(out) + (row0 + g) * D + e, A / L);
-    if (lse && e == 0) lse[row0 + g] = m + logf(L);
+  for (int i = 0; i < s; ++i) {
+    const float li = pl[(int64_t)i * gqa];
+    const float oi = po[(int64_t)i * gqa * D];
+    const float mn = fmaxf(m, li);
+    const float a = __expf(m - mn), w = __expf(li - mn);
+    L = fmaf(L, a, w);
+    A = fmaf(A, a, w * oi);
+    m = mn;
   }
+  store_out<T>(static_cast<T*>(out) + (row0 + g) * D + e, A / L);
+  if (lse && e == 0) lse[row0 + g] = m + logf(L);
 }
 
 using MergeFn = void (*)(const int32_t*, const int32_t*, const float*, const float*, void*, float*, int32_t,
@@ -721,7 +721,8 @@ int32_t tg_decode(const tg_decode_args* a, void* hip_stream) {
   if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
   if (a->num_partials > 0) {
     MergeFn mf = pick_merge(a->dtype, g.head_dim);
-    hipLaunchKernelGGL(mf, dim3(a->batch * g.num_kv_heads), dim3(kBlock), 0, st, a->unit_splits,
+    hipLaunchKernelGGL(mf, dim3(a->batch * g.num_kv_heads, (gqa * g.head_dim + kBlock - 1) / kBlock), dim3(kBlock), 0,
+                       st, a->unit_splits,
                        a->unit_partial_base, p.part_o, p.part_lse, a->out, a->lse, g.num_kv_heads, gqa);
     e = hipGetLastError();
     if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "merge launch failed: %s", hipGetErrorString(e));
