@@ -111,6 +111,48 @@ def cpu_baseline(session, seconds, seed=7):
             "gpu_vs_oracle_max_abs": max_abs}
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def bench_prefill(args):
+    """Ragged chunked prefill (bf16 MFMA), one layer: TFLOP/s of the algorithmic work."""
+    import torch
+    from paper_2606_06302_amd.runner import PrefillSession
+    from workloads import config
+    wl = config(5)
+    log(f"[bench] workload {wl.name}: tables, pool, chunk inputs")
+    s = PrefillSession(wl)
+    torch.cuda.synchronize()
+    flops = s.flops()
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            s.run(stream)
+        stream.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            s.run(stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    tflops = flops / (ms * 1e-3) / 1e12
+    g = wl.geom
+    res = {
+        "metric": "ragged chunked prefill attn: TFLOP/s (bf16 MFMA)", "value": round(tflops, 2), "unit": "TFLOP/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.batch, "chunk_len": wl.chunk_len, "q_heads": g.num_q_heads,
+                   "kv_heads": g.num_kv_heads, "head_dim": g.head_dim, "history_ctx": int(wl.ctx_len[0]),
+                   "flops_per_step": flops, "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": "tg_prefill_kernel",
+                     "avg_launch_us": round(ms * 1e3, 2), "algorithmic_flops_per_launch": flops},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -140,6 +182,8 @@ def main():
     from paper_2606_06302_amd.runner import DecodeSession
     from workloads import config
 
+    if args.config == 5:
+        return bench_prefill(args)
     mode = {"aot": tg.TG_PLAN_AOT, "naive": tg.TG_PLAN_NAIVE, "uniform": tg.TG_PLAN_UNIFORM}[args.mode]
     wl = config(args.config)
     log(f"[bench] workload {wl.name}: building tables, plans and a "

@@ -115,3 +115,53 @@ class DecodeSession:
         loads = np.zeros(len(bo) - 1, dtype=np.int64)
         np.add.at(loads, np.repeat(np.arange(len(bo) - 1), np.diff(bo)), lens)
         return float(loads.max()), float(loads.mean())
+
+
+class PrefillSession:
+    """Pool, chunk inputs and output of one chunked-prefill workload (one layer)."""
+
+    def __init__(self, wl, tables: Tables = None, layer=0, fill="device", pool=None, device="cuda"):
+        from workloads import S_K, S_POOL, S_Q, S_V, device_normal_, host_pool, host_prefill_inputs, page_elems
+        g = wl.geom
+        assert wl.chunk_len >= 1, "prefill workloads need a chunk length"
+        self.wl, self.layer, self.device = wl, layer, device
+        self.t = tables if tables is not None else Tables(wl, device=device)
+        self.dtype = TORCH_DTYPE[wl.dtype]
+        B, C = wl.batch, wl.chunk_len
+        if pool is not None:
+            self.pool = pool
+        elif fill == "host":
+            self.pool = torch.from_numpy(host_pool(wl, self.t.pool_pages)).to(self.dtype).to(device)
+        else:
+            self.pool = torch.empty(self.t.pool_pages * page_elems(g), dtype=self.dtype, device=device)
+            device_normal_(self.pool, wl, S_POOL, wl.kv_scale)
+        self.pool = self.pool.view(self.t.pool_pages, 2, g.heads_per_group, g.page_size, g.head_dim)
+        if fill == "host":
+            q, k, v = host_prefill_inputs(wl)
+            self.q, self.k_new, self.v_new = (torch.from_numpy(x).to(self.dtype).to(device) for x in (q, k, v))
+        else:
+            self.q = torch.empty(B, C, g.num_q_heads, g.head_dim, dtype=self.dtype, device=device)
+            self.k_new = torch.empty(B, C, g.num_kv_heads, g.head_dim, dtype=self.dtype, device=device)
+            self.v_new = torch.empty_like(self.k_new)
+            device_normal_(self.q, wl, S_Q, wl.q_scale)
+            device_normal_(self.k_new, wl, S_K, wl.kv_scale)
+            device_normal_(self.v_new, wl, S_V, wl.kv_scale)
+        self.out = torch.zeros(B, C, g.num_q_heads, g.head_dim, dtype=self.dtype, device=device)
+        self.d_offsets = to_device(self.t.pt_offsets, device)
+        self.d_kv_len = to_device(self.t.kv_len, device)
+        self.d_group_of = to_device(self.t.group_of, device)
+        self.d_slot_of = to_device(self.t.slot_of, device)
+        self.args = tg.make_prefill_args(g, B, C, layer, TG_DTYPE[wl.dtype], self.q, self.k_new, self.v_new,
+                                         self.pool, self.t.d_pt_pages, self.d_offsets, self.d_kv_len,
+                                         self.d_group_of, self.d_slot_of, self.out)
+
+    def run(self, stream=None):
+        tg.tg_prefill(self.args, stream)
+
+    def flops(self) -> int:
+        """Algorithmic flops: 4*d per (query row, visible key) for q.k and p.v."""
+        g, wl = self.wl.geom, self.wl
+        C = wl.chunk_len
+        hist = self.t.kv_len[:, self.layer, :].astype(np.int64)          # [B][H]
+        per_row_keys = hist.sum() * C + wl.batch * g.num_kv_heads * C * (C + 1) // 2
+        return int(4 * g.head_dim * g.gqa * per_row_keys)

@@ -1,0 +1,92 @@
+"""Ragged chunked-prefill attention (bf16 MFMA kernel, through the C ABI) vs the fp64 oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import check_close, poisoned_host_pool, say
+from workloads import Geometry, config, custom
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2606_06302_amd.runner import PrefillSession, Tables
+
+
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _oracle(ps, rows):
+    """fp64 oracle for the given (b, q_head) rows, from pages copied back."""
+    wl, t = ps.wl, ps.t
+    g = wl.geom
+    L, G, P = g.num_layers, g.num_groups, g.page_size
+    need = []
+    for b, qh in rows:
+        h = qh // g.gqa
+        base = int(t.pt_offsets[(b * L + ps.layer) * G + t.group_of[ps.layer, h]])
+        need.append(t.pt_pages[base: base + (int(t.kv_len[b, ps.layer, h]) + P - 1) // P])
+    idx = np.unique(np.concatenate(need)).astype(np.int64)
+    sub = ps.pool[torch.from_numpy(idx).cuda()].float().cpu().numpy().astype(np.float64)
+    remap = np.full(t.pool_pages, -1, dtype=np.int64)
+    remap[idx] = np.arange(len(idx))
+    f = lambda x: x.float().cpu().numpy().astype(np.float64)
+    return oracle.prefill_attention(f(ps.q), f(ps.k_new), f(ps.v_new), sub, ps.layer, geom=g, kv_len=t.kv_len,
+                                    offsets=t.pt_offsets, pages=remap[t.pt_pages], group_of=t.group_of,
+                                    slot_of=t.slot_of, rows=rows)
+
+
+def _compare(ps, rows, what):
+    ref = _oracle(ps, rows)
+    got = ps.out.float().cpu().numpy().astype(np.float64)
+    bi = [r[0] for r in rows]
+    qi = [r[1] for r in rows]
+    g = np.stack([got[b, :, q] for b, q in zip(bi, qi)])
+    r = np.stack([ref[b, :, q] for b, q in zip(bi, qi)])
+    return check_close(g.reshape(-1, g.shape[-1]), r.reshape(-1, r.shape[-1]), "bf16", what)
+
+
+@pytest.mark.parametrize("gqa,C,Hp,ctx", [(4, 40, 2, 300), (1, 33, 1, 100), (3, 70, 2, (20, 600)), (8, 128, 4, 1000),
+                                          (16, 9, 2, 50), (2, 1, 1, 64), (5, 200, 1, (1, 2000))])
+def test_prefill_small_vs_oracle(gqa, C, Hp, ctx):
+    _gpu()
+    H = 4 if Hp != 1 else 2
+    g = Geometry(1, H, H * gqa, 128, 16, Hp)
+    wl = custom(500 + gqa * 7 + C, g, 3, "bf16", ctx, chunk_len=C)
+    say(f"prefill gqa={gqa} C={C} Hp={Hp} ctx={wl.ctx_len.tolist()}")
+    tables = Tables(wl)
+    pool = torch.from_numpy(poisoned_host_pool(wl, tables)).to(torch.bfloat16).cuda()
+    ps = PrefillSession(wl, tables=tables, fill="host", pool=pool)
+    ps.run()
+    torch.cuda.synchronize()
+    rows = [(b, q) for b in range(wl.batch) for q in range(g.num_q_heads)]
+    _compare(ps, rows, f"gqa {gqa} C {C}")
+
+
+def test_prefill_chunk_of_one_matches_decode_path():
+    """C = 1: the prefill kernel and the decode kernel see the same keys when the
+    decode cache holds the chunk's key; both must match the oracle."""
+    _gpu()
+    g = Geometry(1, 8, 32, 128, 16, 2)
+    wl = custom(612, g, 4, "bf16", (100, 900), chunk_len=1)
+    tables = Tables(wl)
+    ps = PrefillSession(wl, tables=tables, fill="host")
+    ps.run()
+    torch.cuda.synchronize()
+    _compare(ps, [(b, q) for b in range(4) for q in range(32)], "C=1")
+
+
+def test_prefill_config5_full_size_sampled():
+    _gpu()
+    wl = config(5)
+    say(f"config 5 full size: B={wl.batch} C={wl.chunk_len}")
+    ps = PrefillSession(wl)
+    ps.run()
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(55)
+    rows = [(int(rng.integers(0, wl.batch)), int(rng.integers(0, wl.geom.num_q_heads))) for _ in range(6)]
+    b = int(np.argmax(ps.t.kv_len[:, 0, :].max(axis=1)))
+    rows.append((b, int(np.argmax(ps.t.kv_len[b, 0])) * wl.geom.gqa))      # the longest history
+    _compare(ps, sorted(set(rows)), "config 5")
