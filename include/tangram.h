@@ -60,7 +60,7 @@ enum { TG_F32 = 0, TG_BF16 = 1 };
 /* head grouping for tg_cluster_heads */
 enum { TG_GROUP_CLUSTERED = 0, TG_GROUP_ADJACENT = 1 };
 /* partition modes for tg_build_plan */
-enum { TG_PLAN_AOT = 0, TG_PLAN_NAIVE = 1, TG_PLAN_UNIFORM = 2 };
+enum { TG_PLAN_AOT = 0, TG_PLAN_NAIVE = 1, TG_PLAN_UNIFORM = 2, TG_PLAN_AOT_FILL = 3 };
 
 /* Model / cache geometry.  H = num_kv_heads (compression is per KV head,
  * Section 2.1), G = H / heads_per_group groups per layer (must divide),
@@ -154,6 +154,11 @@ int32_t tg_decode_max_ctas(const tg_geometry* geom, int32_t dtype, int32_t devic
  *   AOT:     s_u = min(n_u, max(1, floor((2*kv_len*split_target + W) / (2*W))))
  *   NAIVE:   s_u = 1, and one bin per unit (n_bins ignored: B*H bins)
  *   UNIFORM: s_u = min(n_u, max(1, ceil(n_bins / (B*H)))), one bin per chunk
+ *   AOT_FILL: the units' pages laid end to end in unit order are cut into
+ *            n_bins ranges [k*NP/n_bins, (k+1)*NP/n_bins) (NP = sum n_u); bin k
+ *            gets the pieces of the units its range covers (in unit order), so
+ *            every bin holds an equal share of the pages and every unit gets
+ *            bins in proportion to its length; s_u = number of pieces of u.
  *   chunk c < s_u of unit u covers pages [c*n_u/s_u, (c+1)*n_u/s_u) and tokens
  *   [p0*P, min(p1*P, kv_len)).  out_idx = -1 when s_u == 1, else
  *   unit_partial_base[u] + c (partials numbered over units in order).
@@ -162,10 +167,10 @@ int32_t tg_decode_max_ctas(const tg_geometry* geom, int32_t dtype, int32_t devic
  *   order within a bin.  Items are emitted bin by bin; bin k owns
  *   items[bin_offsets[k] .. bin_offsets[k+1]).
  * Arguments (host): kv_len [B][L][H] and pt_offsets [B*L*G+1] from tg_reserve;
- *   group_of, slot_of [L][H]; 0 <= layer < L; n_bins >= 1 (AOT, UNIFORM);
+ *   group_of, slot_of [L][H]; 0 <= layer < L; n_bins >= 1 (AOT, AOT_FILL, UNIFORM);
  *   split_target >= 1 (AOT); items [item_capacity] out, or NULL for a size
  *   query (num_items, num_partials and the bin count are still written);
- *   bin_offsets [bins+1] out, where bins = n_bins (AOT), B*H (NAIVE) or the
+ *   bin_offsets [bins+1] out, where bins = n_bins (AOT, AOT_FILL), B*H (NAIVE) or the
  *   number of chunks (UNIFORM) - its capacity is bin_capacity entries;
  *   unit_splits [B][H] out; unit_partial_base [B][H] out (-1 when unsplit);
  *   num_items, num_bins, num_partials out.

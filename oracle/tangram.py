@@ -49,7 +49,7 @@ import math
 
 import numpy as np
 
-MODE_AOT, MODE_NAIVE, MODE_UNIFORM = 0, 1, 2
+MODE_AOT, MODE_NAIVE, MODE_UNIFORM, MODE_FILL = 0, 1, 2, 3
 GROUP_CLUSTERED, GROUP_ADJACENT = 0, 1
 
 
@@ -225,12 +225,19 @@ def partition_plan(kv_len, offsets, group_of, slot_of, layer, *, num_layers, num
     unit.  UNIFORM: every unit gets the same split count ceil(n_bins/units),
     one bin per chunk.
 
+    FILL: the units' pages are laid end to end in (b, h) order and cut into
+    n_bins equal page ranges, one per bin; a unit is split wherever a range
+    boundary falls inside it, so every bin gets floor/ceil of total/n_bins
+    pages and every unit gets bins in proportion to its length.
+
     Returns dict(items=[(pt_base, b, h, slot, t0, t1, out_idx)], bin_offsets,
     unit_splits [B][H], unit_partial_base [B][H], num_partials, bin_load).
     """
     Bn, L, H = kv_len.shape
     P = page_size
     lens = [[int(kv_len[b, layer, h]) for h in range(H)] for b in range(Bn)]
+    if mode == MODE_FILL:
+        return _fill_plan(lens, offsets, group_of, slot_of, layer, num_layers, num_groups, P, n_bins)
     W = sum(sum(r) for r in lens)
     n_units = Bn * H
     splits = np.zeros((Bn, H), dtype=np.int64)
@@ -285,6 +292,49 @@ def partition_plan(kv_len, offsets, group_of, slot_of, layer, *, num_layers, num
     return dict(items=items, bin_offsets=np.array(bin_offsets, dtype=np.int64),
                 unit_splits=splits, unit_partial_base=base, num_partials=nparts,
                 bin_load=np.array(bin_load, dtype=np.int64))
+
+
+def _fill_plan(lens, offsets, group_of, slot_of, layer, num_layers, num_groups, P, n_bins):
+    Bn, H = len(lens), len(lens[0])
+    units = [(b, h) for b in range(Bn) for h in range(H)]
+    npages = [-(-lens[b][h] // P) for b, h in units]
+    start = [0]
+    for n in npages:
+        start.append(start[-1] + n)
+    total = start[-1]
+    pieces = []                               # (bin, unit index, first page, end page)
+    for k in range(n_bins):
+        lo, hi = k * total // n_bins, (k + 1) * total // n_bins
+        for u in range(len(units)):
+            a, z = max(lo, start[u]), min(hi, start[u + 1])
+            if a < z:
+                pieces.append((k, u, a - start[u], z - start[u]))
+    splits = np.zeros((Bn, H), dtype=np.int64)
+    for _, u, _, _ in pieces:
+        b, h = units[u]
+        splits[b, h] += 1
+    base = np.full((Bn, H), -1, dtype=np.int64)
+    nparts = 0
+    for b, h in units:
+        if splits[b, h] > 1:
+            base[b, h] = nparts
+            nparts += int(splits[b, h])
+    seen = np.zeros((Bn, H), dtype=np.int64)  # pieces of each unit come in page order
+    bins = [[] for _ in range(n_bins)]
+    for k, u, p0, p1 in pieces:
+        b, h = units[u]
+        c = int(seen[b, h])
+        seen[b, h] += 1
+        pt_base = int(offsets[(b * num_layers + layer) * num_groups + int(group_of[layer, h])])
+        out_idx = -1 if splits[b, h] == 1 else int(base[b, h]) + c
+        bins[k].append((pt_base, b, h, int(slot_of[layer, h]), p0 * P, min(p1 * P, lens[b][h]), out_idx))
+    items, bin_offsets, bin_load = [], [0], []
+    for blist in bins:
+        items.extend(blist)
+        bin_offsets.append(len(items))
+        bin_load.append(sum(it[5] - it[4] for it in blist))
+    return dict(items=items, bin_offsets=np.array(bin_offsets, dtype=np.int64), unit_splits=splits,
+                unit_partial_base=base, num_partials=nparts, bin_load=np.array(bin_load, dtype=np.int64))
 
 
 # ------------------------------------------------------------- attention

@@ -33,6 +33,8 @@ HIP_FLAGS = [
     "-fno-strict-aliasing",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
+# per-source additions: the decode kernels keep MFMA accumulators in VGPRs
+HIP_EXTRA = {"tg_decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-ffp-contract=off", "-Wall", "-Wextra",
               f"-I{INCLUDE}", f"-I{CSRC}"]
 
@@ -54,7 +56,7 @@ def build(verbose: bool = False) -> str:
         jobs.append(["g++", *HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
     for src in HIP_SOURCES:
         obj = os.path.join(BUILD, src + ".o")
-        jobs.append([HIPCC, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        jobs.append([HIPCC, *HIP_FLAGS, *HIP_EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj])
     workers = max(1, min(len(jobs), int(os.environ.get("MAX_JOBS", os.cpu_count() or 4))))
     with cf.ThreadPoolExecutor(workers) as ex:
         for out in ex.map(_run, jobs):

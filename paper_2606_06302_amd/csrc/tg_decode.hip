@@ -108,6 +108,8 @@ struct DecodeParams {
   int32_t heads_per_group;
   int32_t num_q_heads;
   int32_t num_kv_heads;
+  int32_t n_bins;
+  int32_t gqa;               // query heads per KV head
   float scale_log2;          // sm_scale * log2(e)
   float scale;               // sm_scale
 };
@@ -293,273 +295,318 @@ __global__ void __launch_bounds__(kBlock) tg_decode_kernel(DecodeParams p, const
 }
 
 // ---------------------------------------------------------------------------
-// Fast path for bf16, head_dim 128 and G = gqa in {4, 8, 16}.
+// Fast path for bf16 and head_dim 128, any gqa G in 1..16: matrix cores.
 //
-// A wave works on a step of SP consecutive pages of an item (SP*16 tokens).
-// Steps of an item are dealt round-robin to the 4 waves.  Each wave streams
-// its steps through registers into its own LDS buffers: while step n is
-// computed from LDS, step n+1 (SP*8 KiB) is already in flight into the
-// staging registers - one unconditional issue per step, so the loads land
-// directly in the loop-carried registers and are only waited for when they
-// are written to LDS one iteration later.  Page ids are read with vector
-// loads (kept off the LDS/scalar counter) one step ahead of their use.
-//   * q.k: lane (h = lane % G, row = lane / G) holds the whole 128-dim query of
-//     head h and computes complete dot products for tokens row, row + 64/G, ...
-//     of the step (no cross-lane reduction).  K slabs are stored in LDS with
-//     chunk c of token row r at position c ^ r, so the 64/G tokens read in one
-//     instruction hit distinct banks while lanes of one token broadcast.
-//   * p.v: lane owns dims (2*lane, 2*lane+1) of all G heads; V rows of two
-//     tokens are interleaved with v_perm_b32 and p is rounded to bf16 pairs, so
-//     each v_dot2_f32_bf16 accumulates two tokens at once (fp32 accumulate).
-//   * The running max of a head is only raised when a step exceeds it by more
-//     than 8 (in log2 units), so accumulator rescales are rare; p stays <= 2^8.
-template <int SP>
-struct Stage {
-  u4 k[4 * SP], v[4 * SP];
-};
+// Every wave is an independent worker: bin 4*blockIdx.x + wave of the plan.
+// There is no barrier and no cross-wave merge; a wave runs its bin's items one
+// after the other, page by page.
+//
+// Data movement.  Pages stream from HBM straight into a ring of R page buffers
+// in the wave's own LDS with gfx950's global_load_lds_dwordx4 (no staging
+// registers): page k+R-1 is issued before page k is computed, so R-1 pages
+// (8 KiB each) stay in flight while the wave computes.  The DMA is issued from
+// inline assembly, invisible to the compiler's wait-count pass (which would
+// otherwise drain every load before each LDS read), and the wave waits for
+// page k with an explicit vmcnt that counts the DMA instructions issued after
+// it; any other vector memory operation issued later (output stores) only
+// makes that wait stricter.  Page ids and work items are read through the
+// constant address space, i.e. with scalar loads, which the vector memory
+// counter does not see.  The queries of an item are DMA'd with its first page
+// into one of R-1 per-wave q slots and moved to registers when the item starts.
+//
+// Arithmetic, per 16-token page, with the query heads of the KV head as the
+// 16 columns of the MFMA tiles (columns past G repeat a real head and are
+// never stored):
+//   * S^T[16 tok][16 heads] = K q^T: 4 x v_mfma_f32_16x16x32_bf16, A = K rows
+//     read from LDS (16 bytes per lane), B = q from registers.  Lane
+//     (col, rb) = (lane % 16, lane / 16) receives tokens 4rb..4rb+3 of head col.
+//   * online softmax on those 4 values per lane; the row max and sum of a head
+//     combine the 4 lanes of its column with the gfx950 permlane swaps.  The
+//     running max is only raised when a page exceeds it by more than 8 (in
+//     log2 units), so rescales are rare and p stays <= 2^8.
+//   * O^T[16 dims][16 heads] += V^T P^T: 8 x v_mfma_f32_16x16x16_bf16, one per
+//     16 dims.  P^T is the S^T tile of the same lane rounded to bf16 (the
+//     result layout of the first product is the operand layout of the second),
+//     and V^T comes from LDS with ds_read_b64_tr_b16, whose 4x4 lane transpose
+//     turns row-major V rows into the 4-consecutive-token operand.
+//   * LDS layout: chunk c (16 bytes) of token row r sits at position c ^ r in
+//     the K slab and at c ^ (2r mod 16) in the V slab (the DMA lanes pick their
+//     source chunk accordingly), so both operand reads are bank-conflict free.
+// The accumulator of a lane belongs to one head, so rescaling and the final
+// normalisation need no cross-lane traffic.
+constexpr int kFastWorkers = kWaves;   // bins per workgroup in the fast path
 
-// Loads the K and V slabs of `slot` in pages pg[0..SP): lane l takes 16-byte
-// chunks l, l+64, l+128, l+192 of every slab.
-template <int SP>
-__device__ __forceinline__ Stage<SP> fetch_step(const DecodeParams& p, const u4* __restrict__ pool,
-                                                const int64_t (&pg)[SP], int slot, int lane) {
-  Stage<SP> s;
-#pragma unroll
-  for (int q = 0; q < SP; ++q) {
-    const u4* base = pool + pg[q] * p.page_chunks;
-    const u4* kb = base + slot * 256 + lane;
-    const u4* vb = base + (p.heads_per_group + slot) * 256 + lane;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {   // streamed once: non-temporal
-      s.k[q * 4 + j] = __builtin_nontemporal_load(kb + j * 64);
-      s.v[q * 4 + j] = __builtin_nontemporal_load(vb + j * 64);
-    }
-  }
-  return s;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4_vs __attribute__((__vector_size__(4 * sizeof(__bf16))));
+
+#define TG_CONST __attribute__((address_space(4)))
+#define TG_LDS __attribute__((address_space(3)))
+
+__device__ __forceinline__ uint32_t lds_address(const void* ptr) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const TG_LDS void*)ptr));
 }
 
-template <int G, int SP>
-__global__ void __launch_bounds__(kBlock) tg_decode_fast_kernel(DecodeParams p, const tg_work_item* __restrict__ items,
-                                                               const int32_t* pt_pages,
-                                                               const int32_t* __restrict__ bin_offsets,
+// 16 bytes per lane from global memory into LDS at m0_base + 16 * lane.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t m0_base) {
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(m0_base) : "memory");
+}
+
+// vmcnt(n) with expcnt/lgkmcnt left alone; the memory clobber keeps LDS reads
+// below it.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ void wait_lgkmcnt0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// field-wise copy: the implicit copy constructor cannot bind a constant-space object
+__device__ __forceinline__ tg_work_item load_item(const TG_CONST tg_work_item* src) {
+  tg_work_item r;
+  r.pt_base = src->pt_base;
+  r.b = src->b;
+  r.kv_head = src->kv_head;
+  r.slot = src->slot;
+  r.tok_begin = src->tok_begin;
+  r.tok_end = src->tok_end;
+  r.out_idx = src->out_idx;
+  return r;
+}
+
+__device__ __forceinline__ f32x4 mfma_qk(const u4& a, const u4& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0,
+                                                 0);
+}
+__device__ __forceinline__ f32x4 mfma_pv(const s16x4& a, const s16x4& b, const f32x4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+// Lane l of each 16-lane block receives element l % 4 of the 8-byte rows
+// addressed by lanes l/4, l/4 + 4, l/4 + 8, l/4 + 12 of the block.
+__device__ __forceinline__ s16x4 lds_read_tr16(const void* ptr) {
+  return __builtin_bit_cast(s16x4, __builtin_amdgcn_ds_read_tr16_b64_v4bf16((TG_LDS bf16x4_vs*)ptr));
+}
+
+// This file is built with -mllvm -amdgpu-mfma-vgpr-form: the accumulators stay
+// in VGPRs, where the rescale multiplies them in place, instead of being
+// copied between AGPRs and VGPRs on every page.
+template <int QMAX>   // 8 or 16: the q slots hold up to QMAX query heads
+__global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, const tg_work_item* __restrict__ items_g,
+                                                               const int32_t* __restrict__ pt_g,
+                                                               const int32_t* __restrict__ bin_offsets_g,
                                                                const u4* __restrict__ pool) {
   constexpr int D = 128;
-  constexpr int kTok = SP * kPage;     // tokens per step
-  constexpr int TR = 64 / G;           // token rows per q.k pass
-  constexpr int TPL = kTok / TR;       // tokens per lane in q.k
+  constexpr int R = QMAX <= 8 ? 4 : 3;   // LDS page buffers per wave
+  constexpr int NQ = R - 1;              // LDS query buffers per wave
+  constexpr int kQChunks = QMAX * (D / 8);
+  constexpr int kDma = 8;                // DMA instructions per page: 4 K + 4 V
   constexpr float kSlack = 8.0f;
-  constexpr int kBufU4 = SP * 512;     // 16-byte slots of one wave's K+V buffer
-  constexpr int kAccStride = kBufU4 * 4;
-  static_assert(G == 4 || G == 8 || G == 16, "fast path covers gqa 4, 8, 16");
-  static_assert(G * D <= kAccStride, "accumulators must fit the wave's buffer");
+  static_assert(kPage == 16, "one page is one 4 KiB K slab and one 4 KiB V slab");
 
-  // per wave: SP swizzled K slabs then SP V slabs; the end-of-item merge reuses them
-  __shared__ u4 sm_kv[kWaves][kBufU4];
-  __shared__ uint32_t sm_p[kWaves][kTok / 2][G];
-  __shared__ float sm_alpha[kWaves][G];
-  __shared__ float sm_m[kWaves][G];
-  __shared__ float sm_l[kWaves][G];
+  __shared__ u4 sm_ring[kWaves][R][512];   // page: K slab, then V slab
+  __shared__ u4 sm_q[kWaves][NQ][kQChunks];
+
+  const TG_CONST tg_work_item* const items = (const TG_CONST tg_work_item*)items_g;
+  const TG_CONST int32_t* const pt = (const TG_CONST int32_t*)pt_g;
+  const TG_CONST int32_t* const bin_offsets = (const TG_CONST int32_t*)bin_offsets_g;
 
   const int lane = threadIdx.x & 63;
   const int wave = wave_id();
-  const int h = lane % G;
-  const int tr = lane / G;
-  const int it_begin = bin_offsets[blockIdx.x], it_end = bin_offsets[blockIdx.x + 1];
+  const int bin = blockIdx.x * kFastWorkers + wave;
+  if (bin >= p.n_bins) return;
+  const int it_begin = bin_offsets[bin], it_end = bin_offsets[bin + 1];
   if (it_begin >= it_end) return;
+  const int G = p.gqa;
+  const int col = lane & 15;            // head column of the MFMA tiles
+  const int rb = lane >> 4;             // row block: tokens / dims 4rb..4rb+3
+  const int hq = col < G ? col : col % G;
   const float cs = p.scale_log2;
-  u4* const kbuf = &sm_kv[wave][0];
-  uint32_t* const vbuf = reinterpret_cast<uint32_t*>(&sm_kv[wave][SP * 256]);
-  uint16_t* const pbuf16 = reinterpret_cast<uint16_t*>(&sm_p[wave][0][0]);
+  const uint32_t ring_lds = lds_address(&sm_ring[wave][0][0]);
+  const uint32_t q_lds = lds_address(&sm_q[wave][0][0]);
+  const u4* const qsrc = static_cast<const u4*>(p.q);
+  const int nq = G * (D / 8);           // 16-byte chunks of one item's queries
 
-  // This wave's steps in processing order: steps wave, wave+4, ... of every
-  // item of the bin.  The cursor caches its item's step/page counts, table
-  // base and slot, so items are only read when the cursor enters a new item.
+  // DMA cursor over every page of every item of the bin; it caches the
+  // item's page count, table base, slot and query offset.
   struct Cursor {
-    int it, si, ns, np, slot;
-    int64_t base;   // index into pt_pages of the item's first page
+    int it, pi, np, slot;
+    int64_t pbase, qoff;
   };
   auto enter = [&](Cursor& cu, int it) {
-    const tg_work_item& im = items[it];
+    const tg_work_item im = load_item(items + it);
     cu.it = it;
-    cu.si = wave;
+    cu.pi = 0;
     cu.np = (im.tok_end - im.tok_begin + kPage - 1) / kPage;
-    cu.ns = (cu.np + SP - 1) / SP;
     cu.slot = im.slot;
-    cu.base = im.pt_base + im.tok_begin / kPage;
+    cu.pbase = im.pt_base + im.tok_begin / kPage;
+    cu.qoff = ((int64_t)im.b * p.num_q_heads + (int64_t)im.kv_head * G) * (D / 8);
   };
-  // moves to the next step of this wave; returns false (cursor unchanged) at the end
-  auto advance = [&](Cursor& cu) {
-    if (cu.si + kWaves < cu.ns) {
-      cu.si += kWaves;
+  auto advance = [&](Cursor& cu) {   // false (cursor unchanged) past the bin's last page
+    if (cu.pi + 1 < cu.np) {
+      ++cu.pi;
       return true;
     }
-    for (int j = cu.it + 1; j < it_end; ++j) {
-      Cursor t;
-      enter(t, j);
-      if (t.ns > wave) {
-        cu = t;
-        return true;
-      }
+    if (cu.it + 1 < it_end) {
+      enter(cu, cu.it + 1);
+      return true;
     }
     return false;
   };
-  // Page ids of a step, read with a lane-varying address so the value stays in a
-  // VGPR (lane q holds page q of the step) and is only waited for when
-  // ids_of() extracts it one iteration later.  Pages past the item's end
-  // repeat its last page (their rows are masked).
-  auto load_ids = [&](const Cursor& cu) {
-    return pt_pages[cu.base + min(cu.si * SP + (lane & (SP - 1)), cu.np - 1)];
-  };
-  auto ids_of = [&](int ids, int64_t (&pg)[SP]) {
+  // queries (on an item's first page), then the page's K slab, then its V slab
+  auto issue = [&](const Cursor& cu, int32_t id, int ring) {
+    if (cu.pi == 0) {
+      const u4* qb = qsrc + cu.qoff;
+      const uint32_t dst = q_lds + ((cu.it - it_begin) % NQ) * (kQChunks * 16);
 #pragma unroll
-    for (int q = 0; q < SP; ++q) pg[q] = __builtin_amdgcn_readlane(ids, q);
+      for (int j = 0; j < kQChunks / 64; ++j)
+        if (j * 64 < nq) lds_dma16(qb + min(j * 64 + lane, nq - 1), dst + j * 1024);
+    }
+    const u4* base = pool + (int64_t)id * p.page_chunks;
+    const u4* kb = base + cu.slot * 256;
+    const u4* vb = base + (p.heads_per_group + cu.slot) * 256;
+    const uint32_t dst = ring_lds + ring * 8192;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = j * 4 + (lane >> 4);   // token row written by this lane
+      const int pos = lane & 15;           // chunk position within the row
+      lds_dma16(kb + r * 16 + (pos ^ r), dst + j * 1024);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = j * 4 + (lane >> 4);
+      const int pos = lane & 15;
+      lds_dma16(vb + r * 16 + (pos ^ ((2 * r) & 15)), dst + 4096 + j * 1024);
+    }
   };
-  // c: step whose data is in flight into `st`; n: the step after it, whose page
-  // ids are in flight into n_ids.  Past the end n repeats the last step (a
-  // harmless reload).
-  Cursor c;
-  enter(c, it_begin);
-  if (c.ns <= wave && !advance(c)) c.si = 0;   // a wave without steps loads one it never uses
-  Cursor n = c;
-  advance(n);
-  int n_ids = load_ids(n);
-  Stage<SP> st;
-  {
-    int64_t pg[SP];
-    ids_of(load_ids(c), pg);
-    st = fetch_step<SP>(p, pool, pg, c.slot, lane);
+
+  Cursor d;
+  enter(d, it_begin);
+  bool d_live = true;
+  int32_t d_id = pt[d.pbase];
+#pragma unroll
+  for (int r = 0; r < R - 1; ++r) {
+    if (d_live) {
+      issue(d, d_id, r);
+      d_live = advance(d);
+      if (d_live) d_id = pt[d.pbase + d.pi];
+    }
   }
 
-  for (int it = it_begin; it < it_end; ++it) {
-    const tg_work_item item = items[it];
-    const int qrow = item.kv_head * G + h;
-    u4 qv[16];
-    {
-      const u4* qb = reinterpret_cast<const u4*>(static_cast<const uint16_t*>(p.q) +
-                                                 ((int64_t)item.b * p.num_q_heads + qrow) * D);
-#pragma unroll
-      for (int c = 0; c < 16; ++c) qv[c] = qb[c];
-    }
-    float m = -INFINITY, l = 0.f;
-    float acc[G][2];
-#pragma unroll
-    for (int g = 0; g < G; ++g) acc[g][0] = acc[g][1] = 0.f;
-    const int ntok = item.tok_end - item.tok_begin;
-    const int ns = (ntok + kTok - 1) / kTok;
+  // lane-constant parts of the operand addresses
+  const int k_off = col * 16;                                  // A of q.k: token row col
+  const int v_tok = lane >> 2;                                 // source row of the transposed read
+  const int v_off = 4096 + v_tok * 256 + (lane & 3) * 8;       // bytes within the page buffer
+  const int v_swz = v_tok & 7;
 
-    for (int si = wave; si < ns; si += kWaves) {
-      // staging registers -> LDS
+  int it = it_begin, pi = 0, np = 0, ntok = 0, k = 0;
+  tg_work_item item;
+  u4 qv[4];
+  float m = -INFINITY, l = 0.f;
+  f32x4 acc[8];
+  for (;;) {
+    if (pi == 0) {   // item start: its queries were DMA'd just before its first page
+      item = load_item(items + it);
+      ntok = item.tok_end - item.tok_begin;
+      np = (ntok + kPage - 1) / kPage;
+      if (d_live)
+        wait_vmcnt<kDma * (R - 1)>();
+      else
+        wait_vmcnt<0>();
+      const u4* qrow = &sm_q[wave][(it - it_begin) % NQ][hq * 16 + rb];
 #pragma unroll
-      for (int q = 0; q < SP; ++q)
+      for (int c = 0; c < 4; ++c) qv[c] = qrow[4 * c];
+      wait_lgkmcnt0();   // the slot may be refilled by the DMA issued next
+      m = -INFINITY;
+      l = 0.f;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int ci = j * 64 + lane;
-          const int r = ci >> 4, cc = ci & 15;
-          kbuf[q * 256 + r * 16 + (cc ^ r)] = st.k[q * 4 + j];
-          reinterpret_cast<u4*>(vbuf)[q * 256 + ci] = st.v[q * 4 + j];
-        }
-      // the next step of this wave (possibly in a later item) goes in flight;
-      // the cursor moves first, so item reads never wait on page data
-      {
-        Cursor nn = n;
-        advance(nn);
-        const int nn_ids = load_ids(nn);
-        int64_t pg[SP];
-        ids_of(n_ids, pg);
-        st = fetch_step<SP>(p, pool, pg, n.slot, lane);
-        n = nn;
-        n_ids = nn_ids;
-      }
+      for (int mm = 0; mm < 8; ++mm) acc[mm] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    if (d_live) {   // keep R-1 pages in flight: issue page k+R-1, then wait for page k
+      issue(d, d_id, (k + R - 1) % R);
+      d_live = advance(d);
+      if (d_live) d_id = pt[d.pbase + d.pi];
+      wait_vmcnt<kDma * (R - 1)>();
+    } else {
+      wait_vmcnt<0>();
+    }
+    const int rs = k % R;
+    const u4* const kbuf = &sm_ring[wave][rs][0];
+    const char* const pbuf = reinterpret_cast<const char*>(&sm_ring[wave][rs][0]);
+    const int nvalid = min(kPage, ntok - pi * kPage);
 
-      const int nvalid = min(kTok, ntok - si * kTok);
-      float s[TPL];
+    // S^T = K q^T
+    f32x4 s = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int k = 0; k < TPL; ++k) {
-        const int t = tr + k * TR;
-        const int q = t >> 4, r = t & 15;
-        float a = 0.f;
+    for (int c = 0; c < 4; ++c) s = mfma_qk(kbuf[k_off + ((4 * c + rb) ^ col)], qv[c], s);
+    float sv[4];
 #pragma unroll
-        for (int cc = 0; cc < 16; ++cc) a = chunk_dot<uint16_t>(kbuf[q * 256 + r * 16 + (cc ^ r)], qv[cc], a);
-        s[k] = t < nvalid ? a : -INFINITY;
-      }
-      float mx = s[0];
+    for (int i = 0; i < 4; ++i) sv[i] = 4 * rb + i < nvalid ? s[i] : -INFINITY;
+    float mx = fmaxf(fmaxf(sv[0], sv[1]), fmaxf(sv[2], sv[3]));
+    mx = swap32_max(swap16_max(mx));
+    const bool raise = (mx - m) * cs > kSlack;
+    if (__any(raise)) {
+      const float m_new = raise ? mx : m;
+      const float alpha = fast_exp2((m - m_new) * cs);   // 0 when m was -inf
+      l *= alpha;
+      m = m_new;
 #pragma unroll
-      for (int k = 1; k < TPL; ++k) mx = fmaxf(mx, s[k]);
-      if constexpr (G == 4) {
-        mx = fmaxf(mx, dpp<0x124>(mx));   // row_ror:4
-        mx = fmaxf(mx, dpp<kRowRor8>(mx));
-      } else if constexpr (G == 8) {
-        mx = fmaxf(mx, dpp<kRowRor8>(mx));
-      }
-      mx = swap32_max(swap16_max(mx));
-      const bool raise = (mx - m) * cs > kSlack;
-      if (__any(raise)) {
-        const float m_new = raise ? mx : m;
-        const float alpha = fast_exp2((m - m_new) * cs);   // 0 when m was -inf
-        l *= alpha;
-        m = m_new;
-        if (tr == 0) sm_alpha[wave][h] = alpha;
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-          const float a = sm_alpha[wave][g];
-          acc[g][0] *= a;
-          acc[g][1] *= a;
-        }
-      }
-      const float mcs = m * cs;
-#pragma unroll
-      for (int k = 0; k < TPL; ++k) {
-        const int t = tr + k * TR;
-        const float pk = fast_exp2(fmaf(s[k], cs, -mcs));
-        l += pk;
-        pbuf16[((t >> 1) * G + h) * 2 + (t & 1)] = f32_to_bf16(pk);
-      }
-      const bool partial = nvalid < kTok;
-#pragma unroll
-      for (int pr = 0; pr < kTok / 2; ++pr) {
-        const int t0 = 2 * pr, t1 = 2 * pr + 1;
-        uint32_t v0 = vbuf[(t0 >> 4) * 1024 + (t0 & 15) * 64 + lane];
-        uint32_t v1 = vbuf[(t1 >> 4) * 1024 + (t1 & 15) * 64 + lane];
-        if (partial) {   // rows past the retained length may hold anything
-          if (t0 >= nvalid) v0 = 0u;
-          if (t1 >= nvalid) v1 = 0u;
-        }
-        const uint32_t lo = __builtin_amdgcn_perm(v1, v0, 0x05040100u);
-        const uint32_t hi = __builtin_amdgcn_perm(v1, v0, 0x07060302u);
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-          const uint32_t pp = sm_p[wave][pr][g];
-          acc[g][0] = dot2_bf16(pp, lo, acc[g][0]);
-          acc[g][1] = dot2_bf16(pp, hi, acc[g][1]);
-        }
-      }
+      for (int mm = 0; mm < 8; ++mm) acc[mm] *= alpha;
     }
-    // this wave's state -> LDS (its own K/V buffer holds its accumulators)
-    if constexpr (G == 4) {
-      l += dpp<0x124>(l);
-      l += dpp<kRowRor8>(l);
-    } else if constexpr (G == 8) {
-      l += dpp<kRowRor8>(l);
+    const float mcs = m * cs;
+    s16x4 pb;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float pk = fast_exp2(fmaf(sv[i], cs, -mcs));
+      l += pk;
+      pb[i] = (short)f32_to_bf16(pk);
     }
+    // O^T += V^T P^T
+    const bool partial = nvalid < kPage;
+#pragma unroll
+    for (int mm = 0; mm < 8; ++mm) {
+      s16x4 a = lds_read_tr16(pbuf + v_off + ((mm ^ v_swz) << 5));
+      if (partial) {   // rows past the retained length may hold anything
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (4 * rb + j >= nvalid) a[j] = 0;
+      }
+      acc[mm] = mfma_pv(a, pb, acc[mm]);
+    }
+    ++k;
+    if (++pi < np) continue;
+
+    // item end: the head's sum over all 16 token rows, then normalise and store
     l = swap32_sum(swap16_sum(l));
-    if (tr == 0) {
-      sm_m[wave][h] = m;
-      sm_l[wave][h] = l;
-    }
-    float* accw = reinterpret_cast<float*>(&sm_kv[wave][0]);
+    if (col < G) {
+      const float lse_nat = m * p.scale + logf(l);
+      const float inv = 1.f / l;
+      const int qh = item.kv_head * G + col;
+      if (item.out_idx < 0) {
+        uint2* orow = reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) +
+                                               ((int64_t)item.b * p.num_q_heads + qh) * D + 4 * rb);
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      accw[g * D + 2 * lane] = acc[g][0];
-      accw[g * D + 2 * lane + 1] = acc[g][1];
+        for (int mm = 0; mm < 8; ++mm) {
+          const f32x4 o = acc[mm] * inv;
+          orow[mm * 4] = make_uint2(uint32_t(f32_to_bf16(o[0])) | (uint32_t(f32_to_bf16(o[1])) << 16),
+                                    uint32_t(f32_to_bf16(o[2])) | (uint32_t(f32_to_bf16(o[3])) << 16));
+        }
+        if (p.lse && rb == 0) p.lse[(int64_t)item.b * p.num_q_heads + qh] = lse_nat;
+      } else {
+        f32x4* prow = reinterpret_cast<f32x4*>(p.part_o + ((int64_t)item.out_idx * G + col) * D + 4 * rb);
+#pragma unroll
+        for (int mm = 0; mm < 8; ++mm) prow[mm * 4] = acc[mm] * inv;
+        if (rb == 0) p.part_lse[(int64_t)item.out_idx * G + col] = lse_nat;
+      }
     }
-    __syncthreads();
-    finish_item<uint16_t, G, D>(p, item, sm_m, sm_l, reinterpret_cast<const float*>(&sm_kv[0][0]), kAccStride);
-    __syncthreads();
+    pi = 0;
+    if (++it == it_end) break;
   }
+  wait_vmcnt<0>();
 }
 
-constexpr int kFastStep = 2;   // pages per wave step in the fast path
-
+// ---------------------------------------------------------------------------
 // Log-sum-exp merge of the split partials of every unit (b, h) with more than
 // one split: lse* = log sum_i e^{lse_i}, O = sum_i e^{lse_i - lse*} o_i.
 // Grid (units, ceil(gqa*D / 256)): each thread owns one output element and
@@ -618,20 +665,20 @@ constexpr int kMaxGqa = 16;
 const std::array<DecodeFn, kMaxGqa> kDecodeF32D64 = make_decode_table<float, 64>(std::make_integer_sequence<int, kMaxGqa>{});
 const std::array<DecodeFn, kMaxGqa> kDecodeF32D128 = make_decode_table<float, 128>(std::make_integer_sequence<int, kMaxGqa>{});
 const std::array<DecodeFn, kMaxGqa> kDecodeBF16D64 = make_decode_table<uint16_t, 64>(std::make_integer_sequence<int, kMaxGqa>{});
-const std::array<DecodeFn, kMaxGqa> kDecodeBF16D128 = make_decode_table<uint16_t, 128>(std::make_integer_sequence<int, kMaxGqa>{});
 
 DecodeFn pick_decode(int dtype, int d, int gqa) {
   if (gqa < 1 || gqa > kMaxGqa) return nullptr;
-  if (dtype == TG_BF16 && d == 128) {
-    if (gqa == 4) return &tg_decode_fast_kernel<4, kFastStep>;
-    if (gqa == 8) return &tg_decode_fast_kernel<8, kFastStep>;
-    if (gqa == 16) return &tg_decode_fast_kernel<16, kFastStep>;
-  }
+  if (dtype == TG_BF16 && d == 128) return gqa <= 8 ? &tg_decode_mfma_kernel<8> : &tg_decode_mfma_kernel<16>;
   if (dtype == TG_F32 && d == 64) return kDecodeF32D64[gqa - 1];
   if (dtype == TG_F32 && d == 128) return kDecodeF32D128[gqa - 1];
   if (dtype == TG_BF16 && d == 64) return kDecodeBF16D64[gqa - 1];
-  if (dtype == TG_BF16 && d == 128) return kDecodeBF16D128[gqa - 1];
   return nullptr;
+}
+
+// bins run by one workgroup of the kernel pick_decode() selects
+int workers_per_wg(int dtype, int d, int gqa) {
+  (void)gqa;
+  return (dtype == TG_BF16 && d == 128) ? kFastWorkers : 1;
 }
 
 int32_t check_decode_shape(const tg_geometry* g, int dtype) {
@@ -674,7 +721,7 @@ int32_t tg_decode_max_ctas(const tg_geometry* geom, int32_t dtype, int32_t devic
   hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fn), kBlock, 0);
   if (prev != device) (void)hipSetDevice(prev);
   if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "occupancy query failed: %s", hipGetErrorString(e));
-  *n_cta = per_cu * cus;
+  *n_cta = per_cu * cus * workers_per_wg(dtype, geom->head_dim, geom->num_q_heads / geom->num_kv_heads);
   return TG_OK;
 }
 
@@ -711,12 +758,16 @@ int32_t tg_decode(const tg_decode_args* a, void* hip_stream) {
   p.heads_per_group = g.heads_per_group;
   p.num_q_heads = g.num_q_heads;
   p.num_kv_heads = g.num_kv_heads;
+  p.n_bins = a->n_bins;
+  p.gqa = gqa;
   p.scale = a->sm_scale != 0.f ? a->sm_scale : 1.0f / std::sqrt((float)g.head_dim);
   p.scale_log2 = p.scale * kLog2e;
   if (a->num_items == 0) return TG_OK;
   hipStream_t st = static_cast<hipStream_t>(hip_stream);
   DecodeFn fn = pick_decode(a->dtype, g.head_dim, gqa);
-  hipLaunchKernelGGL(fn, dim3(a->n_bins), dim3(kBlock), 0, st, p, a->items, a->pt_pages, a->bin_offsets, p.pool);
+  const int wpw = workers_per_wg(a->dtype, g.head_dim, gqa);
+  hipLaunchKernelGGL(fn, dim3((a->n_bins + wpw - 1) / wpw), dim3(kBlock), 0, st, p, a->items, a->pt_pages,
+                     a->bin_offsets, p.pool);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
   if (a->num_partials > 0) {

@@ -49,6 +49,71 @@ static bool ratio_ok(double r) { return r > 0.0 && r <= 1.0; }  // false for NaN
 using tg::ceil_div;
 using tg::fail;
 
+// TG_PLAN_AOT_FILL: the units' pages laid end to end (unit order b, h) and cut
+// into n_bins equal page ranges; a unit is split wherever a boundary falls in it.
+static int32_t fill_plan(int L, int G, int H, int64_t P, int batch, int layer, const std::vector<int64_t>& len,
+                         const std::vector<int64_t>& base, const int32_t* slot_of, int32_t n_bins,
+                         tg_work_item* items, int32_t item_capacity, int32_t* bin_offsets, int32_t bin_capacity,
+                         int32_t* unit_splits, int32_t* unit_partial_base, int32_t* num_items, int32_t* num_bins,
+                         int32_t* num_partials) {
+  (void)L;
+  (void)G;
+  const int64_t n_units = (int64_t)batch * H;
+  std::vector<int64_t> start(n_units + 1, 0);
+  for (int64_t u = 0; u < n_units; ++u) start[u + 1] = start[u] + ceil_div(len[u], P);
+  const int64_t total = start[n_units];
+  // pass 1: count pieces per unit (bins walk the units monotonically)
+  std::vector<int64_t> pieces(n_units, 0);
+  int64_t n_items = 0;
+  for (int64_t k = 0, u = 0; k < n_bins; ++k) {
+    const int64_t lo = k * total / n_bins, hi = (k + 1) * total / n_bins;
+    while (u < n_units && start[u + 1] <= lo) ++u;
+    for (int64_t v = u; v < n_units && start[v] < hi; ++v)
+      if (std::max(lo, start[v]) < std::min(hi, start[v + 1])) {
+        ++pieces[v];
+        ++n_items;
+      }
+  }
+  int64_t nparts = 0;
+  for (int64_t u = 0; u < n_units; ++u) {
+    unit_splits[u] = (int32_t)pieces[u];
+    unit_partial_base[u] = pieces[u] > 1 ? (int32_t)nparts : -1;
+    if (pieces[u] > 1) nparts += pieces[u];
+  }
+  if (n_items > INT32_MAX || nparts > INT32_MAX) return fail(TG_ERR_INVALID_ARG, "plan too large");
+  *num_items = (int32_t)n_items;
+  *num_bins = n_bins;
+  *num_partials = (int32_t)nparts;
+  if (!items) return TG_OK;  // size query
+  if (!bin_offsets) return fail(TG_ERR_INVALID_ARG, "bin_offsets is NULL");
+  if (item_capacity < n_items) return fail(TG_ERR_BUFFER_TOO_SMALL, "items holds %d, need %lld", item_capacity, (long long)n_items);
+  if (bin_capacity < (int64_t)n_bins + 1) return fail(TG_ERR_BUFFER_TOO_SMALL, "bin_offsets holds %d, need %d", bin_capacity, n_bins + 1);
+  // pass 2: emit
+  std::vector<int64_t> seen(n_units, 0);
+  int64_t it = 0;
+  bin_offsets[0] = 0;
+  for (int64_t k = 0, u = 0; k < n_bins; ++k) {
+    const int64_t lo = k * total / n_bins, hi = (k + 1) * total / n_bins;
+    while (u < n_units && start[u + 1] <= lo) ++u;
+    for (int64_t v = u; v < n_units && start[v] < hi; ++v) {
+      const int64_t a = std::max(lo, start[v]), z = std::min(hi, start[v + 1]);
+      if (a >= z) continue;
+      tg_work_item w;
+      w.pt_base = base[v];
+      w.b = (int32_t)(v / H);
+      w.kv_head = (int32_t)(v % H);
+      w.slot = slot_of[(int64_t)layer * H + w.kv_head];
+      w.tok_begin = (int32_t)((a - start[v]) * P);
+      w.tok_end = (int32_t)std::min((z - start[v]) * P, len[v]);
+      w.out_idx = pieces[v] == 1 ? -1 : (int32_t)(unit_partial_base[v] + seen[v]);
+      ++seen[v];
+      items[it++] = w;
+    }
+    bin_offsets[k + 1] = (int32_t)it;
+  }
+  return TG_OK;
+}
+
 extern "C" {
 
 const char* tg_status_string(int32_t code) {
@@ -205,7 +270,7 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
   const int64_t P = geom->page_size;
   if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
   if (layer < 0 || layer >= L) return fail(TG_ERR_INVALID_ARG, "layer %d out of range", layer);
-  if (mode != TG_PLAN_AOT && mode != TG_PLAN_NAIVE && mode != TG_PLAN_UNIFORM)
+  if (mode != TG_PLAN_AOT && mode != TG_PLAN_NAIVE && mode != TG_PLAN_UNIFORM && mode != TG_PLAN_AOT_FILL)
     return fail(TG_ERR_INVALID_ARG, "unknown plan mode %d", mode);
   if (mode != TG_PLAN_NAIVE && n_bins < 1) return fail(TG_ERR_INVALID_ARG, "n_bins must be >= 1");
   if (mode == TG_PLAN_AOT && split_target < 1) return fail(TG_ERR_INVALID_ARG, "split_target must be >= 1");
@@ -228,6 +293,9 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
       base[u] = pt_offsets[t];
       W += len[u];
     }
+  if (mode == TG_PLAN_AOT_FILL)
+    return fill_plan(L, G, H, P, batch, layer, len, base, slot_of, n_bins, items, item_capacity, bin_offsets,
+                     bin_capacity, unit_splits, unit_partial_base, num_items, num_bins, num_partials);
   // split counts
   std::vector<int64_t> splits(n_units);
   int64_t total = 0, nparts = 0;

@@ -42,7 +42,7 @@ def _small_session(wl, mode=0, n_bins=None, split_target=None, free_seed=None, p
 
 
 @pytest.mark.parametrize("mode,n_bins,st", [(0, 8, 16), (0, 1, 1), (0, 512, 2048), (0, 3, 40), (1, None, None),
-                                            (2, 64, None)])
+                                            (2, 64, None), (3, 8, None), (3, 300, None)])
 def test_config1_tiny_fp32_all_plans(mode, n_bins, st):
     _gpu()
     wl = config(1)
@@ -53,6 +53,7 @@ def test_config1_tiny_fp32_all_plans(mode, n_bins, st):
 
 @pytest.mark.parametrize("dtype,d,gqa,Hp,H", [("bf16", 128, 4, 2, 8), ("bf16", 128, 8, 2, 8), ("bf16", 128, 1, 1, 4),
                                               ("bf16", 128, 3, 2, 4), ("bf16", 64, 5, 4, 4), ("bf16", 128, 16, 2, 2),
+                                              ("bf16", 128, 5, 4, 4), ("bf16", 128, 7, 1, 2), ("bf16", 128, 12, 2, 2),
                                               ("f32", 128, 2, 2, 4), ("f32", 64, 7, 1, 2), ("bf16", 64, 2, 8, 8)])
 def test_shapes_vs_oracle(dtype, d, gqa, Hp, H):
     _gpu()
@@ -69,7 +70,7 @@ def test_config2_shape_scaled_plan_modes_agree():
     g = Geometry(1, 8, 32, 128, 16, 2)
     wl = custom(2002, g, 6, "bf16", 2048, kv_scale=0.5)
     outs = []
-    for mode, nb, stg in [(0, 512, 2048), (0, 7, 9), (1, 1, 1), (2, 100, 1)]:
+    for mode, nb, stg in [(0, 512, 2048), (0, 7, 9), (1, 1, 1), (2, 100, 1), (3, 512, 1), (3, 5, 1)]:
         say(f"config2-scaled mode={mode} n_bins={nb}")
         s = _small_session(wl, mode=mode, n_bins=nb, split_target=stg)
         compare_layer(s, 0, what=f"mode {mode}")
@@ -161,7 +162,7 @@ def test_full_size_config_sampled(cfg):
     _gpu()
     wl = config(cfg)
     say(f"config {cfg} full size: B={wl.batch} ctx range {wl.ctx_len.min()}..{wl.ctx_len.max()}")
-    for mode in (0, 1):
+    for mode in (0, 1, 3):
         s = DecodeSession(wl, mode=mode)
         s.run_step()
         torch.cuda.synchronize()

@@ -62,6 +62,10 @@ def test_config1_matches_hand_values_and_oracle():
     pl = tg.tg_build_plan(wl.geom, 2, 0, res["kv_len"], res["pt_offsets"], gof,
                           tg.tg_cluster_heads(wl.geom, wl.budget)[2], 0, 8, 16)
     assert [list(t) for t in _items_as_tuples(pl["items"])] == GOLD["plan_split_target16_bins8"]["items"]
+    fill = tg.tg_build_plan(wl.geom, 2, 0, res["kv_len"], res["pt_offsets"], gof,
+                            tg.tg_cluster_heads(wl.geom, wl.budget)[2], tg.TG_PLAN_AOT_FILL, 8, 1)
+    assert [list(t) for t in _items_as_tuples(fill["items"])] == GOLD["plan_fill_bins8"]["items"]
+    assert fill["bin_offsets"].tolist() == GOLD["plan_fill_bins8"]["bin_offsets"]
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 4, 5])
@@ -71,7 +75,7 @@ def test_workload_configs_bit_exact(cfg):
     need = tg.tg_reserve(wl.geom, wl.ctx_len, wl.ratio, None, gof, np.zeros(0, np.int32), 0, size_query=True)
     pool = pool_pages_for(need["pages_needed"])
     free = free_list(wl, pool)
-    for mode, nb, stg in [(0, 512, 2048), (1, 1, 1), (2, 512, 1)]:
+    for mode, nb, stg in [(0, 512, 2048), (1, 1, 1), (2, 512, 1), (3, 512, 1)]:
         _full_compare(wl.geom, wl.batch, wl.ctx_len, wl.ratio, wl.budget, free, pool, mode=mode, n_bins=nb,
                       split_target=stg)
 
@@ -110,7 +114,7 @@ def test_random_geometries_bit_exact(data):
     need = tg.tg_reserve(geom, ctx, ratio, budget, gof, np.zeros(0, np.int32), 0, size_query=True)["pages_needed"]
     pool = need + int(rng.integers(0, 30))
     free = rng.permutation(pool).astype(np.int32)
-    mode = data.draw(st.sampled_from([0, 1, 2]))
+    mode = data.draw(st.sampled_from([0, 1, 2, 3]))
     _full_compare(geom, B, ctx, ratio, budget, free, pool, grouping=grouping, mode=mode,
                   n_bins=data.draw(st.integers(1, 64)), split_target=data.draw(st.integers(1, 300)))
 

@@ -214,6 +214,15 @@ def test_plan_config1_hand():
     assert max(gold["bin_load"]) / np.mean(gold["bin_load"]) == pytest.approx(256 / 240)
 
 
+def test_fill_plan_config1_hand():
+    _, _, _, plan = _cfg1_plan(mode=oracle.MODE_FILL, n_bins=8)
+    gold = GOLD["plan_fill_bins8"]
+    assert [list(it) for it in plan["items"]] == gold["items"]
+    assert plan["bin_offsets"].tolist() == gold["bin_offsets"]
+    assert plan["bin_load"].tolist() == gold["bin_load"]
+    assert plan["unit_splits"].tolist() == gold["unit_splits"] and plan["num_partials"] == gold["num_partials"]
+
+
 def test_plan_reduces_to_algorithm1():
     """One request, P=1 and lengths exactly B*N: the executed split counts are
     Algorithm 1's split map with H_p = 1."""
@@ -236,6 +245,12 @@ def _check_plan_invariants(plan, kv, offsets, group_of, slot_of, layer, L, G, P,
         assert len(bo) == n_bins + 1
         loads = plan["bin_load"]
         assert loads.max() <= loads.mean() + max(it[5] - it[4] for it in items) + 1e-9   # Graham's LPT bound
+    if mode == oracle.MODE_FILL:
+        assert len(bo) == n_bins + 1
+        # every bin holds floor or ceil of total/n_bins pages
+        pages = [sum(-(-(it[5] - it[4] + it[4] % P) // P) for it in items[bo[k]:bo[k + 1]]) for k in range(n_bins)]
+        total = sum(-(-kv[b, layer, h] // P) for b in range(kv.shape[0]) for h in range(kv.shape[2]))
+        assert sum(pages) == total and max(pages) - min(pages) <= 1
     seen = {}
     for (pt_base, b, h, slot, t0, t1, out_idx) in items:
         assert pt_base == offsets[(b * L + layer) * G + group_of[layer, h]] and slot == slot_of[layer, h]
@@ -258,7 +273,7 @@ def _check_plan_invariants(plan, kv, offsets, group_of, slot_of, layer, L, G, P,
     assert nparts == plan["num_partials"]
 
 
-@pytest.mark.parametrize("mode", [oracle.MODE_AOT, oracle.MODE_NAIVE, oracle.MODE_UNIFORM])
+@pytest.mark.parametrize("mode", [oracle.MODE_AOT, oracle.MODE_NAIVE, oracle.MODE_UNIFORM, oracle.MODE_FILL])
 def test_plan_invariants_random(mode):
     rng = np.random.default_rng(21 + mode)
     for _ in range(25):
@@ -380,7 +395,8 @@ def test_decode_placement_invariance_bitwise():
 
 
 @pytest.mark.parametrize("mode,n_bins,st", [(oracle.MODE_AOT, 5, 7), (oracle.MODE_AOT, 64, 300),
-                                            (oracle.MODE_NAIVE, 1, 1), (oracle.MODE_UNIFORM, 40, 1)])
+                                            (oracle.MODE_NAIVE, 1, 1), (oracle.MODE_UNIFORM, 40, 1),
+                                            (oracle.MODE_FILL, 7, 1), (oracle.MODE_FILL, 100, 1)])
 def test_decode_split_invariance(mode, n_bins, st):
     c = small_case(5, Bn=3, L=2, H=4, gqa=2, d=8, Hp=2, P=4, ctx=(30, 90))
     for layer in range(2):
