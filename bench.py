@@ -56,14 +56,15 @@ def copy_probe(nbytes):
     print(json.dumps({"copy_probe_bytes": nbytes}))
 
 
-def measured_traffic(workload, mode):
+def measured_traffic(workload, mode, n_bins):
     """HBM bytes per decode launch from committed rocprofv3 counter runs, if they
-    were taken on the current decode source; else None."""
+    were taken on the current decode source and the same plan; else None."""
     try:
         rec = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    if rec.get("source_sha") != source_sha() or rec.get("workload") != workload or rec.get("mode") != mode:
+    if (rec.get("source_sha") != source_sha() or rec.get("workload") != workload or rec.get("mode") != mode
+            or rec.get("n_bins") != n_bins):
         return None
     return rec.get("hbm_bytes_per_launch")
 
@@ -236,7 +237,7 @@ def main():
     imb = [s.bin_load_stats(l) for l in s.layers]
     planned_imbalance = float(np.mean([mx / mean for mx, mean in imb]))
     value = kv_bytes_step / (ms_per_step * 1e-3) / 1e9
-    traffic = measured_traffic(wl.name, args.mode)
+    traffic = measured_traffic(wl.name, args.mode, s.n_bins)
     res = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
