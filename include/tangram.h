@@ -254,6 +254,13 @@ int32_t tg_decode(const tg_decode_args* args, void* hip_stream);
  *   kv_pool, pt_pages, pt_offsets [B*L*G+1] int64, kv_len [B][L][H] int32,
  *   group_of, slot_of [L][H] int32   (device copies of the host tables)
  *   out   [B][C][Hq][d] bf16
+ *   block_order [num_blocks] int32 from tg_prefill_schedule for the same
+ *     geometry, batch, chunk_len, layer and lengths, or NULL: then workgroups
+ *     take the (request, KV head) units round-robin over 8 XCDs by index.
+ * Work unit: one workgroup per TG_PREFILL_ROWS consecutive query rows
+ * (row = i*gqa + j for query head h*gqa + j) of one (b, h); it walks the
+ * history and then its causal part of the chunk in tiles of
+ * TG_PREFILL_TILE keys.  The result does not depend on block_order.
  * Supported: dtype TG_BF16, head_dim 128, page_size 16, gqa 1..16,
  * chunk_len >= 1.  The kernel needs no workspace (workspace may be NULL). */
 typedef struct {
@@ -275,7 +282,30 @@ typedef struct {
   float sm_scale;
   void* workspace;
   size_t workspace_bytes;
+  const int32_t* block_order;
+  int32_t num_blocks;
 } tg_prefill_args;
+
+enum { TG_PREFILL_ROWS = 256, TG_PREFILL_TILE = 64 };
+
+/* 4a. Ahead-of-time workgroup schedule for tg_prefill (host, integer; the
+ * prefill analogue of the balanced decode partition of Section 4.3).
+ * The cost of block (b, h, row tile rt) is its tile count
+ *   ceil(kv_len[b][layer][h] / TG_PREFILL_TILE) + floor(i_last / TG_PREFILL_TILE) + 1,
+ * i_last = min(C-1, (min((rt+1)*TG_PREFILL_ROWS, C*gqa) - 1) / gqa).
+ * Units u = b*H + h are placed on n_xcd XCDs longest-processing-time first
+ * (descending unit cost, ties by u; each to the least-loaded XCD, ties to the
+ * lowest index), so that all row tiles of a unit share one L2; each XCD's
+ * blocks run in descending cost (ties by u, rt).  Workgroup k runs on XCD
+ * k % n_xcd, so order[k] = the (k / n_xcd)-th block of XCD k % n_xcd,
+ * encoded u*row_tiles + rt, or -1 past that XCD's list.
+ * Arguments: kv_len [B][L][H] host; n_xcd in 1..64; order [capacity] out or
+ * NULL for a size query; num_blocks out (= n_xcd * longest XCD list).
+ * Errors: TG_ERR_INVALID_ARG; TG_ERR_BUFFER_TOO_SMALL when capacity <
+ * num_blocks (num_blocks still written). */
+int32_t tg_prefill_schedule(const tg_geometry* geom, int32_t batch, int32_t chunk_len, int32_t layer,
+                            const int32_t* kv_len, int32_t n_xcd, int32_t* order, int32_t capacity,
+                            int32_t* num_blocks);
 
 size_t  tg_prefill_workspace_bytes(const tg_prefill_args* args);
 int32_t tg_prefill(const tg_prefill_args* args, void* hip_stream);

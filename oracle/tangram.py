@@ -27,6 +27,10 @@ in the paper's order and notation:
                         (KV-dimension parallelism, Section 2.2.3).
   * prefill_attention - chunked prefill (Section 2.2.1): a chunk attends to the
                         compressed history of its head and, causally, to itself.
+  * prefill_schedule  - ahead-of-time placement of the chunked-prefill
+                        workgroups: the same idea as the decode partition
+                        (cost known from the retained lengths before the step,
+                        Section 4.3), longest-processing-time onto the XCDs.
 
 Readings of points the paper leaves open (each also listed in the design doc):
   - ceil(B*N) is the IEEE fp64 product followed by ceil, with no epsilon.
@@ -444,3 +448,52 @@ def prefill_attention(q, k_new, v_new, pool, layer, *, geom, kv_len, offsets, pa
         w = np.exp(z - m)
         O[b, :, qh] = (w @ Vall) / w.sum(axis=1, keepdims=True)
     return O
+
+
+# ------------------------------------------------------------- prefill schedule
+
+def prefill_schedule(kv_len, layer, chunk_len, gqa, n_xcd, rows_per_block=256, keys_per_tile=64):
+    """Workgroup order for chunked prefill, decided ahead of time from the
+    retained lengths (the balancing idea of Section 4.3 applied to prefill).
+
+    Block (b, h, rt) covers query rows [rt*rows_per_block, (rt+1)*rows_per_block)
+    of unit (b, h), row = i*gqa + j.  It walks ceil(hist/keys_per_tile) history
+    tiles and the chunk tiles up to its last chunk row i_last, so its cost is
+    ceil(hist/T) + floor(i_last/T) + 1.  Units (all their row tiles together)
+    go to XCDs longest first, each to the least-loaded XCD (lowest index on a
+    tie); each XCD runs its blocks longest first (ties by unit, then row tile).
+    Workgroup k runs on XCD k % n_xcd, so slot k holds the (k // n_xcd)-th block
+    of that XCD, coded unit*row_tiles + rt, or -1 past its list.
+    """
+    kv = np.asarray(kv_len)
+    Bn, H = kv.shape[0], kv.shape[2]
+    C = chunk_len
+    n_rows = C * gqa
+    row_tiles = -(-n_rows // rows_per_block)
+
+    def chunk_tiles(rt):
+        last_row = min((rt + 1) * rows_per_block, n_rows) - 1
+        i_last = min(C - 1, last_row // gqa)
+        return i_last // keys_per_tile + 1
+
+    def hist_tiles(u):
+        b, h = divmod(u, H)
+        return -(-int(kv[b, layer, h]) // keys_per_tile)
+
+    units = list(range(Bn * H))
+    cost = {u: sum(hist_tiles(u) + chunk_tiles(rt) for rt in range(row_tiles)) for u in units}
+    by_cost = sorted(units, key=lambda u: (-cost[u], u))
+    load = [0] * n_xcd
+    lists = [[] for _ in range(n_xcd)]
+    for u in by_cost:
+        x = min(range(n_xcd), key=lambda k: (load[k], k))
+        load[x] += cost[u]
+        lists[x].extend((u, rt) for rt in range(row_tiles))
+    for x in range(n_xcd):
+        lists[x].sort(key=lambda ur: (-(hist_tiles(ur[0]) + chunk_tiles(ur[1])), ur[0], ur[1]))
+    longest = max(len(v) for v in lists)
+    order = []
+    for k in range(n_xcd * longest):
+        v, j = lists[k % n_xcd], k // n_xcd
+        order.append(v[j][0] * row_tiles + v[j][1] if j < len(v) else -1)
+    return np.array(order, dtype=np.int64), load

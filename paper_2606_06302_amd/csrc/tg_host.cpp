@@ -379,4 +379,71 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
   return TG_OK;
 }
 
+// Ahead-of-time workgroup schedule of tg_prefill: LPT placement of the
+// (request, KV head) units on the XCDs, longest blocks first on each XCD.
+int32_t tg_prefill_schedule(const tg_geometry* geom, int32_t batch, int32_t chunk_len, int32_t layer,
+                            const int32_t* kv_len, int32_t n_xcd, int32_t* order, int32_t capacity,
+                            int32_t* num_blocks) {
+  if (int32_t rc = tg::check_geometry(geom)) return rc;
+  if (!kv_len || !num_blocks) return fail(TG_ERR_INVALID_ARG, "NULL array");
+  if (batch < 1 || chunk_len < 1) return fail(TG_ERR_INVALID_ARG, "batch and chunk_len must be >= 1");
+  if (layer < 0 || layer >= geom->num_layers) return fail(TG_ERR_INVALID_ARG, "layer %d out of range", layer);
+  if (n_xcd < 1 || n_xcd > 64) return fail(TG_ERR_INVALID_ARG, "n_xcd must be in 1..64");
+  const int64_t L = geom->num_layers, H = geom->num_kv_heads, gqa = geom->num_q_heads / geom->num_kv_heads;
+  const int64_t C = chunk_len, rows = C * gqa;
+  const int64_t row_tiles = tg::ceil_div(rows, TG_PREFILL_ROWS);
+  const int64_t n_units = (int64_t)batch * H;
+  if (n_units * row_tiles > INT32_MAX / 2) return fail(TG_ERR_INVALID_ARG, "too many prefill blocks");
+  // cost of every block and unit
+  std::vector<int64_t> chunk_tiles(row_tiles), unit_cost(n_units);
+  for (int64_t rt = 0; rt < row_tiles; ++rt) {
+    const int64_t i_last = std::min(C - 1, (std::min((rt + 1) * TG_PREFILL_ROWS, rows) - 1) / gqa);
+    chunk_tiles[rt] = i_last / TG_PREFILL_TILE + 1;
+  }
+  std::vector<int64_t> hist_tiles(n_units);
+  for (int64_t u = 0; u < n_units; ++u) {
+    const int64_t b = u / H, h = u % H;
+    const int64_t len = kv_len[(b * L + layer) * H + h];
+    if (len < 0) return fail(TG_ERR_INVALID_ARG, "negative kv_len at request %lld head %lld", (long long)b,
+                             (long long)h);
+    hist_tiles[u] = tg::ceil_div(len, TG_PREFILL_TILE);
+    unit_cost[u] = 0;
+    for (int64_t rt = 0; rt < row_tiles; ++rt) unit_cost[u] += hist_tiles[u] + chunk_tiles[rt];
+  }
+  // units to XCDs, longest first, each to the least-loaded XCD (ties: lowest index)
+  std::vector<int64_t> units(n_units);
+  for (int64_t u = 0; u < n_units; ++u) units[u] = u;
+  std::stable_sort(units.begin(), units.end(),
+                   [&](int64_t a, int64_t b) { return unit_cost[a] > unit_cost[b]; });
+  std::vector<int64_t> load(n_xcd, 0);
+  std::vector<std::vector<std::pair<int64_t, int64_t>>> blocks(n_xcd);   // (u, rt)
+  for (int64_t u : units) {
+    int x = 0;
+    for (int k = 1; k < n_xcd; ++k)
+      if (load[k] < load[x]) x = k;
+    load[x] += unit_cost[u];
+    for (int64_t rt = 0; rt < row_tiles; ++rt) blocks[x].emplace_back(u, rt);
+  }
+  size_t longest = 0;
+  for (auto& v : blocks) {
+    std::stable_sort(v.begin(), v.end(), [&](const std::pair<int64_t, int64_t>& a, const std::pair<int64_t, int64_t>& b) {
+      const int64_t ca = hist_tiles[a.first] + chunk_tiles[a.second];
+      const int64_t cb = hist_tiles[b.first] + chunk_tiles[b.second];
+      if (ca != cb) return ca > cb;
+      return a < b;
+    });
+    longest = std::max(longest, v.size());
+  }
+  const int64_t total = (int64_t)n_xcd * (int64_t)longest;
+  *num_blocks = (int32_t)total;
+  if (!order) return TG_OK;   // size query
+  if (capacity < total) return fail(TG_ERR_BUFFER_TOO_SMALL, "order holds %d, need %lld", capacity, (long long)total);
+  for (int64_t k = 0; k < total; ++k) {
+    const auto& v = blocks[k % n_xcd];
+    const size_t j = (size_t)(k / n_xcd);
+    order[k] = j < v.size() ? (int32_t)(v[j].first * row_tiles + v[j].second) : -1;
+  }
+  return TG_OK;
+}
+
 }  // extern "C"

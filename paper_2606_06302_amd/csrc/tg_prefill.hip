@@ -7,21 +7,36 @@
 //
 // Work decomposition.  The gqa query heads of a KV head are packed into the
 // row dimension (row r = i*gqa + j), so every K/V tile is reused by gqa*rows
-// queries.  One workgroup (4 waves) owns 128 consecutive rows of one (b, h);
-// wave w owns 32 of them.  Key tiles of 32 keys: first the paged history (two
-// pages per tile), then the chunk's own keys up to the workgroup's last row.
-// Block ids are mapped XCD-aware: all row tiles of a (b, h) run on the same
-// XCD (block id mod 8), so the history they share is read into one L2.
+// queries.  One workgroup (4 waves) owns 256 consecutive rows of one (b, h);
+// wave w owns 64 of them as two 32-row column blocks.  Key tiles of 64 keys:
+// first the paged history (four pages per tile), then the chunk's own keys up
+// to the workgroup's last row.  Blocks are placed XCD-aware: all row tiles of
+// a (b, h) run on the same XCD (block id mod 8), so the history they share is
+// read into one L2; the host schedule (tg_prefill_schedule) balances the units
+// over the XCDs by their tile counts and starts the longest blocks first.
 //
-// Per key tile, each wave does (v_mfma_f32_32x32x16_bf16, fp32 accumulate):
+// Data movement.  Tiles stream into a 3-deep LDS ring with gfx950's
+// global_load_lds_dwordx4 (no staging registers); wave w fetches key rows
+// 16w..16w+15 of a tile (one page of history).  The DMA is issued from inline
+// assembly (invisible to the compiler's wait-count pass), every wave waits for
+// its own part with an explicit vmcnt, and one barrier per tile then makes the
+// whole tile visible and retires every read of the slot the next DMA refills.
+// Page ids and table entries are read with scalar loads.
+//
+// Per 32-key block and 32-row column block (v_mfma_f32_32x32x16_bf16, fp32
+// accumulate):
 //   S^T[key][row] = K Q^T   (A = K rows from LDS, B = Q rows in registers)
 //   online softmax per row  (a lane owns one row: max over its 16 keys plus
 //                            one permlane32 swap with the lane holding the rest)
-//   O^T[dv][row] += V^T P^T (A = V^T from LDS, B = P^T straight from the
-//                            lane's own S^T registers, rounded to bf16)
-// The B layout of P^T requires the 32 keys of a tile in the order
-// sigma(kappa) = 16*(kappa/16) + 8*((kappa%8)/4) + 4*((kappa%16)/8) + kappa%4,
-// so V^T is written to LDS transposed in that order.
+//   O^T[dv][row] += V^T P^T (B = P^T straight from the lane's own S^T
+//                            registers, rounded to bf16; A = V^T read from the
+//                            row-major V tile with ds_read_b64_tr_b16)
+// The lane in half hf = lane / 32 holds S^T keys {4hf..4hf+3, 8+4hf..8+4hf+3}
+// of each 16-key half block and feeds them as B's 8 k-indices, so the A
+// operand takes the same keys: two transposed reads of 4 consecutive keys.
+// LDS layout: chunk c (16 bytes) of key row r sits at position c ^ (r mod 16)
+// in the K tile and c ^ 4(r mod 4) in the V tile, so the K operand reads and
+// the transposed V reads are bank-conflict free.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -34,33 +49,40 @@ namespace {
 using namespace tgd;
 
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u2v __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4_vs __attribute__((__vector_size__(4 * sizeof(__bf16))));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kD = 128;          // head_dim
+#define TG_CONST __attribute__((address_space(4)))
+#define TG_LDS __attribute__((address_space(3)))
+
+constexpr int kD = 128;              // head_dim
+constexpr int kChunks = kD / 8;      // 16-byte chunks per row
 constexpr int kPage = 16;
 constexpr int kWaves = 4;
 constexpr int kBlock = 64 * kWaves;
-constexpr int kRows = 32 * kWaves;   // query rows per workgroup
-constexpr int kKeys = 32;            // keys per tile
-constexpr int kKRow = kD * 2 + 16;   // LDS bytes per K row (padded)
-constexpr int kVRow = kKeys * 2 + 16;   // LDS bytes per V^T row (padded)
-constexpr int kKBytes = kKeys * kKRow;
-constexpr int kVBytes = kD * kVRow;
-constexpr int kBufBytes = kKBytes + kVBytes;
+constexpr int kRowsPerWave = 64;
+constexpr int kRows = kRowsPerWave * kWaves;   // query rows per workgroup
+constexpr int kTile = 64;                      // keys per tile = 4 pages
+static_assert(kRows == TG_PREFILL_ROWS && kTile == TG_PREFILL_TILE, "tg_prefill_schedule costs these tiles");
+constexpr int kRing = 3;                       // LDS tile buffers
+constexpr int kTileBytes = 2 * kTile * kD * 2; // K + V
+constexpr int kDmaPerTile = 8;                 // per wave: 4 K + 4 V instructions
 constexpr float kSlack = 8.0f;
 
 struct PrefillParams {
   const uint16_t* q;        // [B][C][Hq][d]
-  const uint16_t* k_new;    // [B][C][H][d]
-  const uint16_t* v_new;
-  const uint16_t* pool;     // [pages][2][Hp][P][d]
+  const u4* k_new;          // [B][C][H][d]
+  const u4* v_new;
+  const u4* pool;           // [pages][2][Hp][P][d]
   const int32_t* pt_pages;
   const int64_t* pt_offsets;
   const int32_t* kv_len;    // [B][L][H]
   const int32_t* group_of;  // [L][H]
   const int32_t* slot_of;
   uint16_t* out;            // [B][C][Hq][d]
+  const int32_t* block_order;   // [gridDim.x] (unit * row_tiles + row tile) or -1, or NULL
   int32_t batch, chunk, layer, num_layers, num_kv_heads, num_groups, heads_per_group, gqa;
   int32_t row_tiles;        // ceil(chunk*gqa / kRows)
   float scale_log2;
@@ -71,185 +93,252 @@ __device__ __forceinline__ f32x16 mfma(const u4& a, const u4& b, const f32x16& c
                                                  0);
 }
 
-// kappa position (0..31) of key n (0..31) of a tile: inverse of sigma
-__device__ __forceinline__ int kappa_of(int n) {
-  const int ks = n >> 4, a = (n >> 3) & 1, hf = (n >> 2) & 1, b = n & 3;
-  return ks * 16 + hf * 8 + a * 4 + b;
+__device__ __forceinline__ uint32_t lds_address(const void* ptr) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const TG_LDS void*)ptr));
+}
+
+// 16 bytes per lane from global memory into LDS at m0_base + 16 * lane.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t m0_base) {
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(m0_base) : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+__device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Lane l of each 16-lane block receives element l % 4 of the 8-byte rows
+// addressed by lanes l/4, l/4 + 4, l/4 + 8, l/4 + 12 of the block.
+__device__ __forceinline__ u2v lds_read_tr16(const void* ptr) {
+  return __builtin_bit_cast(u2v, __builtin_amdgcn_ds_read_tr16_b64_v4bf16((TG_LDS bf16x4_vs*)ptr));
 }
 
 __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
-  __shared__ __attribute__((aligned(16))) unsigned char smem[2 * kBufBytes];
+  __shared__ u4 ring[kRing][2][kTile * kChunks];   // [slot][K, V][key row * 16 + chunk position]
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int tid = threadIdx.x;
 
-  // XCD-aware block -> (unit, row tile): units round-robin over the 8 XCDs
-  const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
-  const int unit = xcd + 8 * (local / p.row_tiles);
-  const int rt = local % p.row_tiles;
+  // block -> (unit, row tile): the host schedule, or units round-robin over
+  // the 8 XCDs (all row tiles of a unit on one XCD either way)
   const int n_units = p.batch * p.num_kv_heads;
-  if (unit >= n_units) return;
+  int unit, rt;
+  if (p.block_order) {
+    const int code = ((const TG_CONST int32_t*)p.block_order)[blockIdx.x];
+    if (code < 0 || code >= n_units * p.row_tiles) return;
+    unit = code / p.row_tiles;
+    rt = code % p.row_tiles;
+  } else {
+    const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+    unit = xcd + 8 * (local / p.row_tiles);
+    rt = local % p.row_tiles;
+    if (unit >= n_units) return;
+  }
   const int b = unit / p.num_kv_heads, h = unit % p.num_kv_heads;
   const int C = p.chunk, gqa = p.gqa;
   const int Hq = p.num_kv_heads * gqa;
   const int rows_total = C * gqa;
   const int row0 = rt * kRows;
-  const int hist = p.kv_len[((int64_t)b * p.num_layers + p.layer) * p.num_kv_heads + h];
-  const int grp = p.group_of[(int64_t)p.layer * p.num_kv_heads + h];
-  const int slot = p.slot_of[(int64_t)p.layer * p.num_kv_heads + h];
-  const int64_t tbase = p.pt_offsets[((int64_t)b * p.num_layers + p.layer) * p.num_groups + grp];
+
+  const TG_CONST int32_t* kv_len = (const TG_CONST int32_t*)p.kv_len;
+  const TG_CONST int32_t* group_of = (const TG_CONST int32_t*)p.group_of;
+  const TG_CONST int32_t* slot_of = (const TG_CONST int32_t*)p.slot_of;
+  const TG_CONST int64_t* pt_offsets = (const TG_CONST int64_t*)p.pt_offsets;
+  const TG_CONST int32_t* pt_pages = (const TG_CONST int32_t*)p.pt_pages;
+
+  const int hist = kv_len[((int64_t)b * p.num_layers + p.layer) * p.num_kv_heads + h];
+  const int grp = group_of[(int64_t)p.layer * p.num_kv_heads + h];
+  const int slot = slot_of[(int64_t)p.layer * p.num_kv_heads + h];
+  const int64_t tbase = pt_offsets[((int64_t)b * p.num_layers + p.layer) * p.num_groups + grp];
+  const int npages = (hist + kPage - 1) / kPage;
   const int i_last = min(C - 1, (min(row0 + kRows, rows_total) - 1) / gqa);   // last chunk row of the block
-  const int n_hist_tiles = (hist + kKeys - 1) / kKeys;
-  const int n_tiles = n_hist_tiles + (i_last + kKeys) / kKeys;
+  const int n_hist_tiles = (hist + kTile - 1) / kTile;
+  const int n_tiles = n_hist_tiles + (i_last + kTile) / kTile;
 
-  // this lane's query row (B operand of S^T and the row it owns in S^T / O^T)
-  const int my_row = row0 + wave * 32 + (lane & 31);
-  const bool row_ok = my_row < rows_total;
-  const int my_i = row_ok ? my_row / gqa : 0;
-  const int my_j = row_ok ? my_row % gqa : 0;
-  const int wave_i_max = min(C - 1, (min(row0 + wave * 32 + 32, rows_total) - 1) / gqa);
+  // this lane's two query rows (one per column block)
   const int hf = lane >> 5;
-  u4 qb[8];
-  {
-    const u4* qp = reinterpret_cast<const u4*>(p.q + (((int64_t)b * C + my_i) * Hq + h * gqa + my_j) * kD);
+  int my_i[2];
+  bool row_ok[2];
+  u4 qb[2][8];
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) qb[kk] = row_ok ? qp[kk * 2 + hf] : u4(0u);
+  for (int cb = 0; cb < 2; ++cb) {
+    const int r = row0 + wave * kRowsPerWave + cb * 32 + (lane & 31);
+    row_ok[cb] = r < rows_total;
+    my_i[cb] = row_ok[cb] ? r / gqa : 0;
+    const int j = row_ok[cb] ? r % gqa : 0;
+    const u4* qp = reinterpret_cast<const u4*>(p.q + (((int64_t)b * C + my_i[cb]) * Hq + h * gqa + j) * kD);
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) qb[cb][kk] = row_ok[cb] ? qp[kk * 2 + hf] : u4(0u);
   }
+  const int wave_i_max = min(C - 1, (min(row0 + wave * kRowsPerWave + kRowsPerWave, rows_total) - 1) / gqa);
 
-  // K/V tile loaders: thread t fetches K chunks t and t+256 of the tile
-  // (key = idx/16, chunk = idx%16) and V chunk t%16 of keys 2*(t/16), 2*(t/16)+1.
-  auto key_src = [&](int tile, int n, int which) -> const u4* {   // nullptr if the key is masked out
-    if (tile < n_hist_tiles) {
-      const int t = tile * kKeys + n;
-      if (t >= hist) return nullptr;
-      const int64_t page = p.pt_pages[tbase + t / kPage];
-      const uint16_t* base = p.pool + (((page * 2 + which) * p.heads_per_group + slot) * kPage + t % kPage) * kD;
-      return reinterpret_cast<const u4*>(base);
-    }
-    const int c = (tile - n_hist_tiles) * kKeys + n;
-    if (c >= C) return nullptr;
-    const uint16_t* src = which == 0 ? p.k_new : p.v_new;
-    return reinterpret_cast<const u4*>(src + (((int64_t)b * C + c) * p.num_kv_heads + h) * kD);
-  };
-  u4 kreg[2], vreg[2];
-  auto load_tile = [&](int tile) {
+  // DMA of this wave's quarter (key rows 16w..16w+15) of tile t into ring slot s
+  const uint32_t ring_lds = lds_address(&ring[0][0][0]);
+  const int rl = lane >> 4;   // row within a 4-row DMA instruction
+  const int pos = lane & 15;  // chunk position within the row
+  auto issue = [&](int t, int s) {
+    const uint32_t dst = ring_lds + (uint32_t)s * kTileBytes + (uint32_t)wave * (16 * kChunks * 16);
+    if (t < n_hist_tiles) {
+      const int pg = min(t * 4 + wave, npages - 1);   // past the history: any valid page, masked later
+      const int64_t id = pt_pages[tbase + pg];
+      const u4* kb = p.pool + ((id * 2 + 0) * p.heads_per_group + slot) * (kPage * kChunks);
+      const u4* vb = p.pool + ((id * 2 + 1) * p.heads_per_group + slot) * (kPage * kChunks);
 #pragma unroll
-    for (int x = 0; x < 2; ++x) {
-      const int idx = tid + x * kBlock;
-      const u4* src = key_src(tile, idx >> 4, 0);
-      kreg[x] = src ? src[idx & 15] : u4(0u);
-    }
-    const int kp = tid >> 4, c = tid & 15;
+      for (int j = 0; j < 4; ++j) {
+        const int r = j * 4 + rl;   // key row within the page (== tile row mod 16)
+        lds_dma16(kb + r * kChunks + (pos ^ r), dst + j * 1024);
+        lds_dma16(vb + r * kChunks + (pos ^ (4 * (r & 3))), dst + kTile * kChunks * 16 + j * 1024);
+      }
+    } else {
+      const int c0 = (t - n_hist_tiles) * kTile + wave * 16;   // first chunk key of the quarter
+      const u4* kb = p.k_new + h * kChunks;
+      const u4* vb = p.v_new + h * kChunks;
 #pragma unroll
-    for (int x = 0; x < 2; ++x) {
-      const u4* src = key_src(tile, 2 * kp + x, 1);
-      vreg[x] = src ? src[c] : u4(0u);
-    }
-  };
-  auto store_tile = [&](int buf) {
-    unsigned char* kb = smem + buf * kBufBytes;
-    unsigned char* vb = kb + kKBytes;
-#pragma unroll
-    for (int x = 0; x < 2; ++x) {
-      const int idx = tid + x * kBlock;
-      *reinterpret_cast<u4*>(kb + (idx >> 4) * kKRow + (idx & 15) * 16) = kreg[x];
-    }
-    // V^T: dword (v[n][d], v[n+1][d]) at row d, column kappa(n)/2
-    const int kp = tid >> 4, c = tid & 15;
-    const int col = kappa_of(2 * kp) >> 1;
-    const uint32_t* v0 = reinterpret_cast<const uint32_t*>(&vreg[0]);
-    const uint32_t* v1 = reinterpret_cast<const uint32_t*>(&vreg[1]);
-#pragma unroll
-    for (int w = 0; w < 4; ++w) {
-      const uint32_t lo = __builtin_amdgcn_perm(v1[w], v0[w], 0x05040100u);
-      const uint32_t hi = __builtin_amdgcn_perm(v1[w], v0[w], 0x07060302u);
-      const int d = c * 8 + 2 * w;
-      *reinterpret_cast<uint32_t*>(vb + d * kVRow + col * 4) = lo;
-      *reinterpret_cast<uint32_t*>(vb + (d + 1) * kVRow + col * 4) = hi;
+      for (int j = 0; j < 4; ++j) {
+        const int r = j * 4 + rl;
+        const int c = min(c0 + r, C - 1);   // rows past the chunk repeat its last key (masked later)
+        const int64_t roff = ((int64_t)b * C + c) * p.num_kv_heads * kChunks;
+        lds_dma16(kb + roff + (pos ^ r), dst + j * 1024);
+        lds_dma16(vb + roff + (pos ^ (4 * (r & 3))), dst + kTile * kChunks * 16 + j * 1024);
+      }
     }
   };
 
-  f32x16 acc[4];
+  f32x16 acc[2][4];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) acc[t] = f32x16(0.f);
-  float m = -INFINITY, l = 0.f;
+  for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+    for (int d = 0; d < 4; ++d) acc[cb][d] = f32x16(0.f);
+  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
   const float cs = p.scale_log2;
 
-  load_tile(0);
-  store_tile(0);
-  __syncthreads();
-  for (int tile = 0; tile < n_tiles; ++tile) {
-    const int buf = tile & 1;
-    const bool more = tile + 1 < n_tiles;
-    if (more) load_tile(tile + 1);
-    const unsigned char* kb = smem + buf * kBufBytes;
-    const unsigned char* vb = kb + kKBytes;
-    const bool is_chunk = tile >= n_hist_tiles;
-    const int c0 = (tile - n_hist_tiles) * kKeys;   // first chunk key of the tile
-    // skip a chunk tile that is entirely in the future of this wave's rows
-    if (!(is_chunk && c0 > wave_i_max)) {
-      f32x16 s = f32x16(0.f);
+  // lane-constant parts of the LDS operand addresses
+  const int k_row = lane & 31;                                  // A of S^T: key row kb*32 + k_row
+  const int tr_key = (lane & 15) >> 2;                          // transposed read: key within a group of 4
+  const int tr_dim = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);   // dims within a 32-dim block
+  const int tr_chunk = tr_dim >> 3, tr_half = (tr_dim >> 2) & 1;
+
+  // prologue: tiles 0 and 1 in flight
+  issue(0, 0);
+  if (n_tiles > 1) issue(1, 1);
+
+  for (int t = 0; t < n_tiles; ++t) {
+    if (t + 1 < n_tiles)
+      wait_vmcnt<kDmaPerTile>();
+    else
+      wait_vmcnt<0>();
+    barrier();   // tile t complete in LDS; every wave is done with tile t-1
+    if (t + 2 < n_tiles) issue(t + 2, (t + 2) % kRing);
+
+    const int s = t % kRing;
+    const unsigned char* kt = reinterpret_cast<const unsigned char*>(&ring[s][0][0]);
+    const unsigned char* vt = reinterpret_cast<const unsigned char*>(&ring[s][1][0]);
+    const bool is_chunk = t >= n_hist_tiles;
+    const int key0 = is_chunk ? (t - n_hist_tiles) * kTile : t * kTile;   // first key of the tile
+    const int key_end = is_chunk ? C : hist;                                 // keys >= this are invalid
+    if (is_chunk && key0 > wave_i_max) continue;   // tile entirely in the future of this wave's rows
+    const bool edge_hist = !is_chunk && key0 + kTile > hist;
+
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      const int kbase = key0 + kb * 32;
+      if (is_chunk && kbase > wave_i_max) break;
+      // S^T for both column blocks; the K operand is read once
+      f32x16 sc[2] = {f32x16(0.f), f32x16(0.f)};
+      const int krow = kb * 32 + k_row;
 #pragma unroll
       for (int kk = 0; kk < 8; ++kk) {
-        const u4 a = *reinterpret_cast<const u4*>(kb + (lane & 31) * kKRow + (kk * 2 + hf) * 16);
-        s = mfma(a, qb[kk], s);
+        const u4 a = *reinterpret_cast<const u4*>(kt + krow * 256 + (((kk * 2 + hf) ^ (krow & 15)) << 4));
+        sc[0] = mfma(a, qb[0][kk], sc[0]);
+        sc[1] = mfma(a, qb[1][kk], sc[1]);
       }
-      // lane holds keys n(r) = 8*(r/4) + 4*hf + r%4 of its row
-      float mx = -INFINITY;
+      u4 pb[2][2];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int n = 8 * (r >> 2) + 4 * hf + (r & 3);
-        bool ok;
-        if (is_chunk) ok = c0 + n <= my_i && c0 + n < C;
-        else ok = tile * kKeys + n < hist;
-        s[r] = ok ? s[r] : -INFINITY;
-        mx = fmaxf(mx, s[r]);
+      for (int cb = 0; cb < 2; ++cb) {
+        // lane holds keys n(r) = 8*(r/4) + 4*hf + r%4 of its row
+        float mx = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kbase + 8 * (r >> 2) + 4 * hf + (r & 3);
+          const bool ok = key < key_end && (!is_chunk || key <= my_i[cb]);
+          sc[cb][r] = ok ? sc[cb][r] : -INFINITY;
+          mx = fmaxf(mx, sc[cb][r]);
+        }
+        mx = swap32_max(mx);
+        const bool raise = (mx - m[cb]) * cs > kSlack;
+        if (__any(raise)) {   // raise the running max (rare after the first block)
+          const float m_new = raise ? mx : m[cb];
+          const float alpha = fast_exp2((m[cb] - m_new) * cs);   // 0 when m was -inf
+          m[cb] = m_new;
+          l[cb] *= alpha;
+#pragma unroll
+          for (int d = 0; d < 4; ++d) acc[cb][d] *= alpha;
+        }
+        const float mcs = m[cb] * cs;
+        uint32_t pw[8];
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) {
+          const float p0 = fast_exp2(fmaf(sc[cb][r], cs, -mcs));
+          const float p1 = fast_exp2(fmaf(sc[cb][r + 1], cs, -mcs));
+          l[cb] += p0 + p1;
+          pw[r >> 1] = uint32_t(f32_to_bf16(p0)) | (uint32_t(f32_to_bf16(p1)) << 16);
+        }
+        pb[cb][0] = u4{pw[0], pw[1], pw[2], pw[3]};
+        pb[cb][1] = u4{pw[4], pw[5], pw[6], pw[7]};
       }
-      mx = swap32_max(mx);
-      if ((mx - m) * cs > kSlack) {   // raise the running max (rare after the first tile)
-        const float alpha = fast_exp2((m - mx) * cs);
-        m = mx;
-        l *= alpha;
+      // O^T += V^T P^T over the two 16-key halves of the block
 #pragma unroll
-        for (int t = 0; t < 4; ++t) acc[t] *= alpha;
-      }
-      const float mcs = m * cs;
-      uint32_t pw[8];
+      for (int q16 = 0; q16 < 2; ++q16) {
+        const int g0 = kb * 32 + q16 * 16 + 4 * hf;    // tile row of the A operand's first key
+        const int r0 = g0 + tr_key, r1 = g0 + 8 + tr_key;  // source rows of the two transposed reads
 #pragma unroll
-      for (int r = 0; r < 16; r += 2) {
-        const float p0 = fast_exp2(fmaf(s[r], cs, -mcs));
-        const float p1 = fast_exp2(fmaf(s[r + 1], cs, -mcs));
-        l += p0 + p1;
-        pw[r >> 1] = uint32_t(f32_to_bf16(p0)) | (uint32_t(f32_to_bf16(p1)) << 16);
-      }
-      u4 pb0, pb1;
-      pb0.x = pw[0]; pb0.y = pw[1]; pb0.z = pw[2]; pb0.w = pw[3];
-      pb1.x = pw[4]; pb1.y = pw[5]; pb1.z = pw[6]; pb1.w = pw[7];
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const unsigned char* vrow = vb + (t * 32 + (lane & 31)) * kVRow;
-        acc[t] = mfma(*reinterpret_cast<const u4*>(vrow + hf * 16), pb0, acc[t]);
-        acc[t] = mfma(*reinterpret_cast<const u4*>(vrow + 32 + hf * 16), pb1, acc[t]);
+        for (int db = 0; db < 4; ++db) {
+          const int c = 4 * db + tr_chunk;
+          u2v lo = lds_read_tr16(vt + r0 * 256 + ((c ^ (4 * (r0 & 3))) << 4) + tr_half * 8);
+          u2v hi = lds_read_tr16(vt + r1 * 256 + ((c ^ (4 * (r1 & 3))) << 4) + tr_half * 8);
+          if (edge_hist) {   // history rows past the retained length may hold anything
+            const int kl = key0 + g0, kh = key0 + g0 + 8;
+            if (kl + 0 >= hist) lo.x &= 0xffff0000u;
+            if (kl + 1 >= hist) lo.x &= 0x0000ffffu;
+            if (kl + 2 >= hist) lo.y &= 0xffff0000u;
+            if (kl + 3 >= hist) lo.y &= 0x0000ffffu;
+            if (kh + 0 >= hist) hi.x &= 0xffff0000u;
+            if (kh + 1 >= hist) hi.x &= 0x0000ffffu;
+            if (kh + 2 >= hist) hi.y &= 0xffff0000u;
+            if (kh + 3 >= hist) hi.y &= 0x0000ffffu;
+          }
+          const u4 a = u4{lo.x, lo.y, hi.x, hi.y};
+          acc[0][db] = mfma(a, pb[0][q16], acc[0][db]);
+          acc[1][db] = mfma(a, pb[1][q16], acc[1][db]);
+        }
       }
     }
-    if (more) store_tile(buf ^ 1);
-    __syncthreads();
   }
+  wait_vmcnt<0>();
   // row sum over both halves of the row, then O = O^T / l
-  l = swap32_sum(l);
-  if (!row_ok) return;
-  const float inv = 1.f / l;
-  uint16_t* orow = p.out + (((int64_t)b * C + my_i) * Hq + h * gqa + my_j) * kD;
 #pragma unroll
-  for (int t = 0; t < 4; ++t)
+  for (int cb = 0; cb < 2; ++cb) {
+    const float lt = swap32_sum(l[cb]);
+    if (!row_ok[cb]) continue;
+    const int r = row0 + wave * kRowsPerWave + cb * 32 + (lane & 31);
+    const int i = r / gqa, j = r % gqa;
+    const float inv = 1.f / lt;
+    uint16_t* orow = p.out + (((int64_t)b * C + i) * Hq + h * gqa + j) * kD;
 #pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      const int dv = t * 32 + 8 * r4 + 4 * hf;
-      uint32_t w0 = uint32_t(f32_to_bf16(acc[t][r4 * 4 + 0] * inv)) | (uint32_t(f32_to_bf16(acc[t][r4 * 4 + 1] * inv)) << 16);
-      uint32_t w1 = uint32_t(f32_to_bf16(acc[t][r4 * 4 + 2] * inv)) | (uint32_t(f32_to_bf16(acc[t][r4 * 4 + 3] * inv)) << 16);
-      *reinterpret_cast<uint2*>(orow + dv) = make_uint2(w0, w1);
-    }
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int dv = db * 32 + 8 * r4 + 4 * hf;
+        const uint32_t w0 = uint32_t(f32_to_bf16(acc[cb][db][r4 * 4 + 0] * inv)) |
+                            (uint32_t(f32_to_bf16(acc[cb][db][r4 * 4 + 1] * inv)) << 16);
+        const uint32_t w1 = uint32_t(f32_to_bf16(acc[cb][db][r4 * 4 + 2] * inv)) |
+                            (uint32_t(f32_to_bf16(acc[cb][db][r4 * 4 + 3] * inv)) << 16);
+        *reinterpret_cast<uint2*>(orow + dv) = make_uint2(w0, w1);
+      }
+  }
 }
 
 }  // namespace
@@ -277,15 +366,16 @@ int32_t tg_prefill(const tg_prefill_args* a, void* hip_stream) {
     return tg::fail(TG_ERR_INVALID_ARG, "NULL device pointer");
   PrefillParams p;
   p.q = static_cast<const uint16_t*>(a->q);
-  p.k_new = static_cast<const uint16_t*>(a->k_new);
-  p.v_new = static_cast<const uint16_t*>(a->v_new);
-  p.pool = static_cast<const uint16_t*>(a->kv_pool);
+  p.k_new = static_cast<const u4*>(a->k_new);
+  p.v_new = static_cast<const u4*>(a->v_new);
+  p.pool = static_cast<const u4*>(a->kv_pool);
   p.pt_pages = a->pt_pages;
   p.pt_offsets = a->pt_offsets;
   p.kv_len = a->kv_len;
   p.group_of = a->group_of;
   p.slot_of = a->slot_of;
   p.out = static_cast<uint16_t*>(a->out);
+  p.block_order = a->block_order;
   p.batch = a->batch;
   p.chunk = a->chunk_len;
   p.layer = a->layer;
@@ -298,7 +388,8 @@ int32_t tg_prefill(const tg_prefill_args* a, void* hip_stream) {
   const float scale = a->sm_scale != 0.f ? a->sm_scale : 1.0f / std::sqrt((float)kD);
   p.scale_log2 = scale * kLog2e;
   const int units = a->batch * g.num_kv_heads;
-  const int blocks = 8 * ((units + 7) / 8) * p.row_tiles;
+  if (a->block_order && a->num_blocks < 1) return tg::fail(TG_ERR_INVALID_ARG, "block_order needs num_blocks >= 1");
+  const int blocks = a->block_order ? a->num_blocks : 8 * ((units + 7) / 8) * p.row_tiles;
   hipLaunchKernelGGL(tg_prefill_kernel, dim3(blocks), dim3(kBlock), 0, static_cast<hipStream_t>(hip_stream), p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "prefill launch failed: %s", hipGetErrorString(e));

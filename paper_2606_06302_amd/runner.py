@@ -120,7 +120,7 @@ class DecodeSession:
 class PrefillSession:
     """Pool, chunk inputs and output of one chunked-prefill workload (one layer)."""
 
-    def __init__(self, wl, tables: Tables = None, layer=0, fill="device", pool=None, device="cuda"):
+    def __init__(self, wl, tables: Tables = None, layer=0, fill="device", pool=None, device="cuda", schedule=True):
         from workloads import S_K, S_POOL, S_Q, S_V, device_normal_, host_pool, host_prefill_inputs, page_elems
         g = wl.geom
         assert wl.chunk_len >= 1, "prefill workloads need a chunk length"
@@ -151,9 +151,12 @@ class PrefillSession:
         self.d_kv_len = to_device(self.t.kv_len, device)
         self.d_group_of = to_device(self.t.group_of, device)
         self.d_slot_of = to_device(self.t.slot_of, device)
+        # ahead-of-time workgroup schedule from the retained lengths (host integer work)
+        self.order = tg.tg_prefill_schedule(g, B, C, layer, self.t.kv_len) if schedule else None
+        self.d_order = to_device(self.order, device) if schedule else None
         self.args = tg.make_prefill_args(g, B, C, layer, TG_DTYPE[wl.dtype], self.q, self.k_new, self.v_new,
                                          self.pool, self.t.d_pt_pages, self.d_offsets, self.d_kv_len,
-                                         self.d_group_of, self.d_slot_of, self.out)
+                                         self.d_group_of, self.d_slot_of, self.out, block_order=self.d_order)
 
     def run(self, stream=None):
         tg.tg_prefill(self.args, stream)

@@ -52,7 +52,7 @@ class tg_prefill_args(C.Structure):
                 ("kv_pool", C.c_void_p), ("pt_pages", C.c_void_p), ("pt_offsets", C.c_void_p),
                 ("kv_len", C.c_void_p), ("group_of", C.c_void_p), ("slot_of", C.c_void_p),
                 ("out", C.c_void_p), ("sm_scale", C.c_float), ("workspace", C.c_void_p),
-                ("workspace_bytes", C.c_size_t)]
+                ("workspace_bytes", C.c_size_t), ("block_order", C.c_void_p), ("num_blocks", C.c_int32)]
 
 
 # One HIP runtime per process: torch ships its own libamdhip64 (soname
@@ -88,6 +88,7 @@ _SIGS = {
     "tg_decode": (_i32, [C.POINTER(tg_decode_args), _P]),
     "tg_prefill_workspace_bytes": (_sz, [C.POINTER(tg_prefill_args)]),
     "tg_prefill": (_i32, [C.POINTER(tg_prefill_args), _P]),
+    "tg_prefill_schedule": (_i32, [_G, _i32, _i32, _i32, _P, _i32, _P, _i32, _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -238,11 +239,27 @@ def tg_decode(args: tg_decode_args, stream=None):
 
 
 def make_prefill_args(geom, batch, chunk_len, layer, dtype, q, k_new, v_new, kv_pool, pt_pages, pt_offsets,
-                      kv_len, group_of, slot_of, out, sm_scale=0.0, workspace=None) -> tg_prefill_args:
+                      kv_len, group_of, slot_of, out, sm_scale=0.0, workspace=None,
+                      block_order=None) -> tg_prefill_args:
+    """Packs a tg_prefill_args from device tensors (kept alive by the caller); block_order is the
+    device copy of a tg_prefill_schedule result, or None for the default block mapping."""
     return tg_prefill_args(_geom(geom), int(batch), int(chunk_len), int(layer), int(dtype), _dptr(q),
                            _dptr(k_new), _dptr(v_new), _dptr(kv_pool), _dptr(pt_pages), _dptr(pt_offsets),
                            _dptr(kv_len), _dptr(group_of), _dptr(slot_of), _dptr(out), float(sm_scale),
-                           _dptr(workspace), 0 if workspace is None else workspace.numel() * workspace.element_size())
+                           _dptr(workspace), 0 if workspace is None else workspace.numel() * workspace.element_size(),
+                           _dptr(block_order), 0 if block_order is None else int(block_order.numel()))
+
+
+def tg_prefill_schedule(geom, batch, chunk_len, layer, kv_len, n_xcd=8):
+    """-> int32 array: block k runs (unit, row tile) = divmod(order[k], row_tiles), or nothing if -1."""
+    g = _geom(geom)
+    kv = _host(kv_len, np.int32)
+    n = C.c_int32(0)
+    head = (C.byref(g), int(batch), int(chunk_len), int(layer), _ptr(kv), int(n_xcd))
+    _check(_lib.tg_prefill_schedule(*head, None, 0, C.byref(n)), "tg_prefill_schedule")
+    order = np.zeros(max(1, n.value), np.int32)
+    _check(_lib.tg_prefill_schedule(*head, _ptr(order), len(order), C.byref(n)), "tg_prefill_schedule")
+    return order[: n.value]
 
 
 def tg_prefill_workspace_bytes(args: tg_prefill_args) -> int:

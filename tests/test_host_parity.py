@@ -185,3 +185,45 @@ def test_status_strings_and_version():
     assert tg.tg_status_string(0) == "ok"
     assert tg.tg_status_string(tg.TG_ERR_OUT_OF_PAGES) == "out of pages"
     assert tg.tg_version() >> 16 == 1
+
+
+@pytest.mark.parametrize("cfg", [2, 4, 5])
+def test_prefill_schedule_bit_exact_on_configs(cfg):
+    wl = config(cfg)
+    gof = tg.tg_cluster_heads(wl.geom, wl.budget)[1]
+    res = tg.tg_reserve(wl.geom, wl.ctx_len, wl.ratio, None, gof, np.zeros(0, np.int32), 0, size_query=True)
+    C = wl.chunk_len or 512
+    for n_xcd in (8, 3, 1):
+        got = tg.tg_prefill_schedule(wl.geom, wl.batch, C, 0, res["kv_len"], n_xcd)
+        ref, _ = oracle.prefill_schedule(res["kv_len"], 0, C, wl.geom.gqa, n_xcd)
+        assert got.tolist() == ref.tolist()
+
+
+@settings(max_examples=40, deadline=None)
+@given(st.data())
+def test_prefill_schedule_random_bit_exact(data):
+    H = data.draw(st.sampled_from([1, 2, 4, 8]))
+    gqa = data.draw(st.integers(1, 16))
+    L = data.draw(st.integers(1, 3))
+    B = data.draw(st.integers(1, 5))
+    C = data.draw(st.integers(1, 1200))
+    n_xcd = data.draw(st.integers(1, 12))
+    layer = data.draw(st.integers(0, L - 1))
+    rng = np.random.default_rng(data.draw(st.integers(0, 2**31)))
+    kv = rng.integers(0, data.draw(st.sampled_from([1, 70, 3000])), size=(B, L, H)).astype(np.int32)
+    geom = Geometry(L, H, H * gqa, 128, 16, 1)
+    got = tg.tg_prefill_schedule(geom, B, C, layer, kv, n_xcd)
+    ref, _ = oracle.prefill_schedule(kv, layer, C, gqa, n_xcd)
+    assert got.tolist() == ref.tolist()
+
+
+def test_prefill_schedule_errors():
+    geom = Geometry(1, 2, 4, 128, 16, 1)
+    kv = np.ones((1, 1, 2), np.int32)
+    for bad in [dict(n_xcd=0), dict(n_xcd=65)]:
+        with pytest.raises(tg.TangramError):
+            tg.tg_prefill_schedule(geom, 1, 8, 0, kv, **bad)
+    with pytest.raises(tg.TangramError):
+        tg.tg_prefill_schedule(geom, 1, 0, 0, kv)
+    with pytest.raises(tg.TangramError):
+        tg.tg_prefill_schedule(geom, 1, 8, 1, kv)

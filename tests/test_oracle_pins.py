@@ -470,3 +470,51 @@ def test_prefill_full_prefix_equals_masked_sdpa():
             ref = torch.nn.functional.scaled_dot_product_attention(torch.from_numpy(q[b, :, qh])[None], keys, vals,
                                                                    attn_mask=mask)[0].numpy()
             np.testing.assert_allclose(O[b, :, qh], ref, rtol=0, atol=1e-12)
+
+
+# ------------------------------------------------------------- prefill schedule
+
+def test_prefill_schedule_hand():
+    """B=1, H=3, C=300, gqa=1, kv=[64, 200, 1], 2 XCDs, 256-row blocks, 64-key tiles.
+    Row tiles 2: chunk tiles 4 (rows 0..255) and 5 (rows 256..299); history tiles 1, 4, 1.
+    Unit costs 11, 17, 11 -> u1 on XCD0, u0 then u2 on XCD1 (loads 17, 22).
+    XCD0 runs (1,1)=9 then (1,0)=8; XCD1 runs (0,1)=6, (2,1)=6, (0,0)=5, (2,0)=5."""
+    kv = np.array([[[64, 200, 1]]])
+    order, load = oracle.prefill_schedule(kv, 0, 300, 1, 2)
+    assert order.tolist() == [3, 1, 2, 5, -1, 0, -1, 4]
+    assert load == [17, 22]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_prefill_schedule_invariants(seed):
+    rng = np.random.default_rng(seed)
+    B, H, gqa = int(rng.integers(1, 6)), int(rng.choice([1, 2, 4, 8])), int(rng.integers(1, 9))
+    C = int(rng.integers(1, 700))
+    n_xcd = int(rng.integers(1, 9))
+    kv = rng.integers(0, 5000, size=(B, 2, H))
+    order, load = oracle.prefill_schedule(kv, 1, C, gqa, n_xcd)
+    row_tiles = -(-(C * gqa) // 256)
+    codes = [c for c in order.tolist() if c >= 0]
+    assert sorted(codes) == list(range(B * H * row_tiles))            # every block exactly once
+    assert len(order) % n_xcd == 0
+    xcd_of = {}
+    for k, c in enumerate(order.tolist()):
+        if c >= 0:
+            xcd_of.setdefault(c // row_tiles, set()).add(k % n_xcd)
+    assert all(len(v) == 1 for v in xcd_of.values())                 # a unit's row tiles share one XCD
+
+    def cost(c):
+        u, rt = divmod(c, row_tiles)
+        b, h = divmod(u, H)
+        i_last = min(C - 1, (min((rt + 1) * 256, C * gqa) - 1) // gqa)
+        return -(-int(kv[b, 1, h]) // 64) + i_last // 64 + 1
+    unit_cost = {}
+    for c in codes:
+        unit_cost[c // row_tiles] = unit_cost.get(c // row_tiles, 0) + cost(c)
+    # Graham's LPT bound on the XCD loads
+    assert sum(load) == sum(unit_cost.values())
+    assert max(load) <= sum(load) / n_xcd + max(unit_cost.values())
+    for x in range(n_xcd):                                            # longest first on every XCD
+        seq = [cost(c) for c in order.tolist()[x::n_xcd] if c >= 0]
+        assert seq == sorted(seq, reverse=True)
+        assert all(c == -1 for c in order.tolist()[x::n_xcd][len(seq):])

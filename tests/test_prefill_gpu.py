@@ -90,3 +90,30 @@ def test_prefill_config5_full_size_sampled():
     b = int(np.argmax(ps.t.kv_len[:, 0, :].max(axis=1)))
     rows.append((b, int(np.argmax(ps.t.kv_len[b, 0])) * wl.geom.gqa))      # the longest history
     _compare(ps, sorted(set(rows)), "config 5")
+
+
+def test_prefill_block_order_does_not_change_results():
+    """The ahead-of-time schedule only reorders workgroups: outputs are bitwise
+    equal with the default mapping and with schedules for 8 and 3 XCDs."""
+    _gpu()
+    from paper_2606_06302_amd import tangram as tg
+    from paper_2606_06302_amd.device import to_device
+    g = Geometry(1, 8, 32, 128, 16, 2)
+    wl = custom(733, g, 5, "bf16", (50, 3000), chunk_len=300)
+    tables = Tables(wl)
+    pool = torch.from_numpy(poisoned_host_pool(wl, tables)).to(torch.bfloat16).cuda()
+    ps = PrefillSession(wl, tables=tables, fill="host", pool=pool, schedule=False)
+    ps.run()
+    torch.cuda.synchronize()
+    base = ps.out.clone()
+    for n_xcd in (8, 3):
+        order = to_device(tg.tg_prefill_schedule(g, wl.batch, wl.chunk_len, 0, tables.kv_len, n_xcd), "cuda")
+        say(f"block order n_xcd={n_xcd}: {order.numel()} blocks")
+        ps.out.zero_()
+        args = tg.make_prefill_args(g, wl.batch, wl.chunk_len, 0, tg.TG_BF16, ps.q, ps.k_new, ps.v_new, ps.pool,
+                                    tables.d_pt_pages, ps.d_offsets, ps.d_kv_len, ps.d_group_of, ps.d_slot_of,
+                                    ps.out, block_order=order)
+        tg.tg_prefill(args)
+        torch.cuda.synchronize()
+        assert torch.equal(ps.out, base)
+    _compare(ps, [(b, q) for b in range(wl.batch) for q in range(0, 32, 3)], "scheduled")
