@@ -33,8 +33,11 @@ HIP_FLAGS = [
     "-fno-strict-aliasing",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
-# per-source additions: the decode kernels keep MFMA accumulators in VGPRs
-HIP_EXTRA = {"tg_decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# per-source additions: the kernels keep MFMA accumulators in VGPRs, where
+# the online-softmax rescale multiplies them in place (AGPR accumulators are
+# copied to VGPRs and back around every rescale branch)
+HIP_EXTRA = {"tg_decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+             "tg_prefill.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-ffp-contract=off", "-Wall", "-Wextra",
               f"-I{INCLUDE}", f"-I{CSRC}"]
 

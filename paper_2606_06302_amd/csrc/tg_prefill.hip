@@ -7,8 +7,10 @@
 //
 // Work decomposition.  The gqa query heads of a KV head are packed into the
 // row dimension (row r = i*gqa + j), so every K/V tile is reused by gqa*rows
-// queries.  One workgroup (4 waves) owns 256 consecutive rows of one (b, h);
-// wave w owns 64 of them as two 32-row column blocks.  Key tiles of 64 keys:
+// queries.  One workgroup (8 waves, two per SIMD) owns 256 consecutive rows
+// of one (b, h); wave w owns 32 of them (one 32-row MFMA column block).  With
+// two waves per SIMD the matrix core runs one wave's products while the other
+// does its softmax.  Key tiles of 64 keys:
 // first the paged history (four pages per tile), then the chunk's own keys up
 // to the workgroup's last row.  Blocks are placed XCD-aware: all row tiles of
 // a (b, h) run on the same XCD (block id mod 8), so the history they share is
@@ -17,7 +19,7 @@
 //
 // Data movement.  Tiles stream into a 3-deep LDS ring with gfx950's
 // global_load_lds_dwordx4 (no staging registers); wave w fetches key rows
-// 16w..16w+15 of a tile (one page of history).  The DMA is issued from inline
+// 8w..8w+7 of a tile (half a page of history).  The DMA is issued from inline
 // assembly (invisible to the compiler's wait-count pass), every wave waits for
 // its own part with an explicit vmcnt, and one barrier per tile then makes the
 // whole tile visible and retires every read of the slot the next DMA refills.
@@ -34,6 +36,8 @@
 // The lane in half hf = lane / 32 holds S^T keys {4hf..4hf+3, 8+4hf..8+4hf+3}
 // of each 16-key half block and feeds them as B's 8 k-indices, so the A
 // operand takes the same keys: two transposed reads of 4 consecutive keys.
+// V rows of the last history tile past the retained length are zeroed in LDS
+// by the wave that fetched them, so the PV loop needs no mask.
 // LDS layout: chunk c (16 bytes) of key row r sits at position c ^ (r mod 16)
 // in the K tile and c ^ 4(r mod 4) in the V tile, so the K operand reads and
 // the transposed V reads are bank-conflict free.
@@ -53,6 +57,8 @@ typedef uint32_t u2v __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4_vs __attribute__((__vector_size__(4 * sizeof(__bf16))));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
 
 #define TG_CONST __attribute__((address_space(4)))
 #define TG_LDS __attribute__((address_space(3)))
@@ -60,15 +66,18 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int kD = 128;              // head_dim
 constexpr int kChunks = kD / 8;      // 16-byte chunks per row
 constexpr int kPage = 16;
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
 constexpr int kBlock = 64 * kWaves;
-constexpr int kRowsPerWave = 64;
+constexpr int kCB = 1;                         // 32-row MFMA column blocks per wave
+constexpr int kRowsPerWave = 32 * kCB;
 constexpr int kRows = kRowsPerWave * kWaves;   // query rows per workgroup
 constexpr int kTile = 64;                      // keys per tile = 4 pages
 static_assert(kRows == TG_PREFILL_ROWS && kTile == TG_PREFILL_TILE, "tg_prefill_schedule costs these tiles");
 constexpr int kRing = 3;                       // LDS tile buffers
 constexpr int kTileBytes = 2 * kTile * kD * 2; // K + V
-constexpr int kDmaPerTile = 8;                 // per wave: 4 K + 4 V instructions
+constexpr int kDmaRows = kTile / kWaves;       // key rows each wave fetches per tile
+constexpr int kDmaInst = kDmaRows / 4;         // 1 KiB instructions per K or V slab and wave
+constexpr int kDmaPerTile = 2 * kDmaInst;
 constexpr float kSlack = 8.0f;
 
 struct PrefillParams {
@@ -109,6 +118,11 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 __device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// (lo, hi) rounded to bf16 and packed into one dword (one v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2v));
+}
 
 // Lane l of each 16-lane block receives element l % 4 of the 8-byte rows
 // addressed by lanes l/4, l/4 + 4, l/4 + 8, l/4 + 12 of the block.
@@ -160,11 +174,11 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
 
   // this lane's two query rows (one per column block)
   const int hf = lane >> 5;
-  int my_i[2];
-  bool row_ok[2];
-  u4 qb[2][8];
+  int my_i[kCB];
+  bool row_ok[kCB];
+  u4 qb[kCB][8];
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
+  for (int cb = 0; cb < kCB; ++cb) {
     const int r = row0 + wave * kRowsPerWave + cb * 32 + (lane & 31);
     row_ok[cb] = r < rows_total;
     my_i[cb] = row_ok[cb] ? r / gqa : 0;
@@ -174,45 +188,53 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
     for (int kk = 0; kk < 8; ++kk) qb[cb][kk] = row_ok[cb] ? qp[kk * 2 + hf] : u4(0u);
   }
   const int wave_i_max = min(C - 1, (min(row0 + wave * kRowsPerWave + kRowsPerWave, rows_total) - 1) / gqa);
+  const int wave_i_min = min(C - 1, (row0 + wave * kRowsPerWave) / gqa);
 
-  // DMA of this wave's quarter (key rows 16w..16w+15) of tile t into ring slot s
+  // DMA of this wave's share (key rows kDmaRows*w .. kDmaRows*(w+1)-1) of tile
+  // t into ring slot s
   const uint32_t ring_lds = lds_address(&ring[0][0][0]);
   const int rl = lane >> 4;   // row within a 4-row DMA instruction
   const int pos = lane & 15;  // chunk position within the row
+  const int rb0 = (wave * kDmaRows) % kPage;   // first row of the share within its page
   auto issue = [&](int t, int s) {
-    const uint32_t dst = ring_lds + (uint32_t)s * kTileBytes + (uint32_t)wave * (16 * kChunks * 16);
+    const uint32_t dst = ring_lds + (uint32_t)s * kTileBytes + (uint32_t)wave * (kDmaRows * kChunks * 16);
     if (t < n_hist_tiles) {
-      const int pg = min(t * 4 + wave, npages - 1);   // past the history: any valid page, masked later
+      // past the history: any valid page, masked later
+      const int pg = min(t * (kTile / kPage) + wave * kDmaRows / kPage, npages - 1);
       const int64_t id = pt_pages[tbase + pg];
       const u4* kb = p.pool + ((id * 2 + 0) * p.heads_per_group + slot) * (kPage * kChunks);
       const u4* vb = p.pool + ((id * 2 + 1) * p.heads_per_group + slot) * (kPage * kChunks);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int r = j * 4 + rl;   // key row within the page (== tile row mod 16)
+      for (int j = 0; j < kDmaInst; ++j) {
+        const int r = rb0 + j * 4 + rl;   // key row within the page (== tile row mod 16)
         lds_dma16(kb + r * kChunks + (pos ^ r), dst + j * 1024);
         lds_dma16(vb + r * kChunks + (pos ^ (4 * (r & 3))), dst + kTile * kChunks * 16 + j * 1024);
       }
     } else {
-      const int c0 = (t - n_hist_tiles) * kTile + wave * 16;   // first chunk key of the quarter
+      const int c0 = (t - n_hist_tiles) * kTile + wave * kDmaRows;   // first chunk key of the share
       const u4* kb = p.k_new + h * kChunks;
       const u4* vb = p.v_new + h * kChunks;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < kDmaInst; ++j) {
         const int r = j * 4 + rl;
         const int c = min(c0 + r, C - 1);   // rows past the chunk repeat its last key (masked later)
+        const int rr = rb0 + r;             // tile row mod 16
         const int64_t roff = ((int64_t)b * C + c) * p.num_kv_heads * kChunks;
-        lds_dma16(kb + roff + (pos ^ r), dst + j * 1024);
-        lds_dma16(vb + roff + (pos ^ (4 * (r & 3))), dst + kTile * kChunks * 16 + j * 1024);
+        lds_dma16(kb + roff + (pos ^ rr), dst + j * 1024);
+        lds_dma16(vb + roff + (pos ^ (4 * (rr & 3))), dst + kTile * kChunks * 16 + j * 1024);
       }
     }
   };
 
-  f32x16 acc[2][4];
+  f32x16 acc[kCB][4];
+  float m[kCB], l[kCB];
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb)
+  for (int cb = 0; cb < kCB; ++cb) {
 #pragma unroll
     for (int d = 0; d < 4; ++d) acc[cb][d] = f32x16(0.f);
-  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.f, 0.f};
+    m[cb] = -INFINITY;
+    l[cb] = 0.f;
+  }
   const float cs = p.scale_log2;
 
   // lane-constant parts of the LDS operand addresses
@@ -230,6 +252,15 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
       wait_vmcnt<kDmaPerTile>();
     else
       wait_vmcnt<0>();
+    if (t < n_hist_tiles && t * kTile + wave * kDmaRows + kDmaRows > hist) {
+      // this wave's share holds V rows past the retained history: they may
+      // hold anything (NaN included) and p = 0 does not cancel NaN, so zero them
+      u4* vq = &ring[t % kRing][1][wave * kDmaRows * kChunks];
+#pragma unroll
+      for (int j = 0; j < kDmaInst; ++j)
+        if (t * kTile + wave * kDmaRows + j * 4 + rl >= hist) vq[j * 64 + lane] = u4(0u);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    }
     barrier();   // tile t complete in LDS; every wave is done with tile t-1
     if (t + 2 < n_tiles) issue(t + 2, (t + 2) % kRing);
 
@@ -240,33 +271,42 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
     const int key0 = is_chunk ? (t - n_hist_tiles) * kTile : t * kTile;   // first key of the tile
     const int key_end = is_chunk ? C : hist;                                 // keys >= this are invalid
     if (is_chunk && key0 > wave_i_max) continue;   // tile entirely in the future of this wave's rows
-    const bool edge_hist = !is_chunk && key0 + kTile > hist;
 
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       const int kbase = key0 + kb * 32;
       if (is_chunk && kbase > wave_i_max) break;
       // S^T for both column blocks; the K operand is read once
-      f32x16 sc[2] = {f32x16(0.f), f32x16(0.f)};
+      f32x16 sc[kCB];
+#pragma unroll
+      for (int cb = 0; cb < kCB; ++cb) sc[cb] = f32x16(0.f);
       const int krow = kb * 32 + k_row;
 #pragma unroll
       for (int kk = 0; kk < 8; ++kk) {
         const u4 a = *reinterpret_cast<const u4*>(kt + krow * 256 + (((kk * 2 + hf) ^ (krow & 15)) << 4));
-        sc[0] = mfma(a, qb[0][kk], sc[0]);
-        sc[1] = mfma(a, qb[1][kk], sc[1]);
-      }
-      u4 pb[2][2];
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb) {
-        // lane holds keys n(r) = 8*(r/4) + 4*hf + r%4 of its row
+        for (int cb = 0; cb < kCB; ++cb) sc[cb] = mfma(a, qb[cb][kk], sc[cb]);
+      }
+      // only the block holding the end of the history and the chunk blocks
+      // that reach past the wave's first row need a mask
+      const bool masked = is_chunk ? kbase + 31 > wave_i_min : kbase + 32 > hist;
+      if (masked) {
+#pragma unroll
+        for (int cb = 0; cb < kCB; ++cb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            // lane holds keys n(r) = 8*(r/4) + 4*hf + r%4 of its row
+            const int key = kbase + 8 * (r >> 2) + 4 * hf + (r & 3);
+            const bool ok = key < key_end && (!is_chunk || key <= my_i[cb]);
+            sc[cb][r] = ok ? sc[cb][r] : -INFINITY;
+          }
+      }
+      u4 pb[kCB][2];
+#pragma unroll
+      for (int cb = 0; cb < kCB; ++cb) {
         float mx = -INFINITY;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kbase + 8 * (r >> 2) + 4 * hf + (r & 3);
-          const bool ok = key < key_end && (!is_chunk || key <= my_i[cb]);
-          sc[cb][r] = ok ? sc[cb][r] : -INFINITY;
-          mx = fmaxf(mx, sc[cb][r]);
-        }
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[cb][r]);
         mx = swap32_max(mx);
         const bool raise = (mx - m[cb]) * cs > kSlack;
         if (__any(raise)) {   // raise the running max (rare after the first block)
@@ -284,7 +324,7 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
           const float p0 = fast_exp2(fmaf(sc[cb][r], cs, -mcs));
           const float p1 = fast_exp2(fmaf(sc[cb][r + 1], cs, -mcs));
           l[cb] += p0 + p1;
-          pw[r >> 1] = uint32_t(f32_to_bf16(p0)) | (uint32_t(f32_to_bf16(p1)) << 16);
+          pw[r >> 1] = pack_bf16(p0, p1);
         }
         pb[cb][0] = u4{pw[0], pw[1], pw[2], pw[3]};
         pb[cb][1] = u4{pw[4], pw[5], pw[6], pw[7]};
@@ -297,22 +337,11 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
 #pragma unroll
         for (int db = 0; db < 4; ++db) {
           const int c = 4 * db + tr_chunk;
-          u2v lo = lds_read_tr16(vt + r0 * 256 + ((c ^ (4 * (r0 & 3))) << 4) + tr_half * 8);
-          u2v hi = lds_read_tr16(vt + r1 * 256 + ((c ^ (4 * (r1 & 3))) << 4) + tr_half * 8);
-          if (edge_hist) {   // history rows past the retained length may hold anything
-            const int kl = key0 + g0, kh = key0 + g0 + 8;
-            if (kl + 0 >= hist) lo.x &= 0xffff0000u;
-            if (kl + 1 >= hist) lo.x &= 0x0000ffffu;
-            if (kl + 2 >= hist) lo.y &= 0xffff0000u;
-            if (kl + 3 >= hist) lo.y &= 0x0000ffffu;
-            if (kh + 0 >= hist) hi.x &= 0xffff0000u;
-            if (kh + 1 >= hist) hi.x &= 0x0000ffffu;
-            if (kh + 2 >= hist) hi.y &= 0xffff0000u;
-            if (kh + 3 >= hist) hi.y &= 0x0000ffffu;
-          }
+          const u2v lo = lds_read_tr16(vt + r0 * 256 + ((c ^ (4 * (r0 & 3))) << 4) + tr_half * 8);
+          const u2v hi = lds_read_tr16(vt + r1 * 256 + ((c ^ (4 * (r1 & 3))) << 4) + tr_half * 8);
           const u4 a = u4{lo.x, lo.y, hi.x, hi.y};
-          acc[0][db] = mfma(a, pb[0][q16], acc[0][db]);
-          acc[1][db] = mfma(a, pb[1][q16], acc[1][db]);
+#pragma unroll
+          for (int cb = 0; cb < kCB; ++cb) acc[cb][db] = mfma(a, pb[cb][q16], acc[cb][db]);
         }
       }
     }
@@ -320,7 +349,7 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
   wait_vmcnt<0>();
   // row sum over both halves of the row, then O = O^T / l
 #pragma unroll
-  for (int cb = 0; cb < 2; ++cb) {
+  for (int cb = 0; cb < kCB; ++cb) {
     const float lt = swap32_sum(l[cb]);
     if (!row_ok[cb]) continue;
     const int r = row0 + wave * kRowsPerWave + cb * 32 + (lane & 31);
@@ -332,10 +361,8 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const int dv = db * 32 + 8 * r4 + 4 * hf;
-        const uint32_t w0 = uint32_t(f32_to_bf16(acc[cb][db][r4 * 4 + 0] * inv)) |
-                            (uint32_t(f32_to_bf16(acc[cb][db][r4 * 4 + 1] * inv)) << 16);
-        const uint32_t w1 = uint32_t(f32_to_bf16(acc[cb][db][r4 * 4 + 2] * inv)) |
-                            (uint32_t(f32_to_bf16(acc[cb][db][r4 * 4 + 3] * inv)) << 16);
+        const uint32_t w0 = pack_bf16(acc[cb][db][r4 * 4 + 0] * inv, acc[cb][db][r4 * 4 + 1] * inv);
+        const uint32_t w1 = pack_bf16(acc[cb][db][r4 * 4 + 2] * inv, acc[cb][db][r4 * 4 + 3] * inv);
         *reinterpret_cast<uint2*>(orow + dv) = make_uint2(w0, w1);
       }
   }
