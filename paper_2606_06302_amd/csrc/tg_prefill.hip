@@ -17,7 +17,7 @@
 // read into one L2; the host schedule (tg_prefill_schedule) balances the units
 // over the XCDs by their tile counts and starts the longest blocks first.
 //
-// Data movement.  Tiles stream into a 3-deep LDS ring with gfx950's
+// Data movement.  Tiles stream into a 4-deep LDS ring with gfx950's
 // global_load_lds_dwordx4 (no staging registers); wave w fetches key rows
 // 8w..8w+7 of a tile (half a page of history).  The DMA is issued from inline
 // assembly (invisible to the compiler's wait-count pass), every wave waits for
@@ -73,7 +73,8 @@ constexpr int kRowsPerWave = 32 * kCB;
 constexpr int kRows = kRowsPerWave * kWaves;   // query rows per workgroup
 constexpr int kTile = 64;                      // keys per tile = 4 pages
 static_assert(kRows == TG_PREFILL_ROWS && kTile == TG_PREFILL_TILE, "tg_prefill_schedule costs these tiles");
-constexpr int kRing = 3;                       // LDS tile buffers
+constexpr int kRing = 4;                       // LDS tile buffers
+static_assert(kRing >= 2 && kRing <= 4, "the wait below covers up to two tiles in flight after the current one");
 constexpr int kTileBytes = 2 * kTile * kD * 2; // K + V
 constexpr int kDmaRows = kTile / kWaves;       // key rows each wave fetches per tile
 constexpr int kDmaInst = kDmaRows / 4;         // 1 KiB instructions per K or V slab and wave
@@ -243,12 +244,17 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
   const int tr_dim = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);   // dims within a 32-dim block
   const int tr_chunk = tr_dim >> 3, tr_half = (tr_dim >> 2) & 1;
 
-  // prologue: tiles 0 and 1 in flight
-  issue(0, 0);
-  if (n_tiles > 1) issue(1, 1);
+  // prologue: tiles 0 .. kRing-2 in flight
+#pragma unroll
+  for (int r = 0; r < kRing - 1; ++r)
+    if (r < n_tiles) issue(r, r);
 
   for (int t = 0; t < n_tiles; ++t) {
-    if (t + 1 < n_tiles)
+    // tile t has landed once at most the DMAs of the tiles after it are pending
+    const int after = min(kRing - 2, n_tiles - 1 - t);
+    if (after >= 2)
+      wait_vmcnt<2 * kDmaPerTile>();
+    else if (after == 1)
       wait_vmcnt<kDmaPerTile>();
     else
       wait_vmcnt<0>();
@@ -262,7 +268,7 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     }
     barrier();   // tile t complete in LDS; every wave is done with tile t-1
-    if (t + 2 < n_tiles) issue(t + 2, (t + 2) % kRing);
+    if (t + kRing - 1 < n_tiles) issue(t + kRing - 1, (t + kRing - 1) % kRing);
 
     const int s = t % kRing;
     const unsigned char* kt = reinterpret_cast<const unsigned char*>(&ring[s][0][0]);
