@@ -69,8 +69,9 @@ def measured_traffic(workload, mode, n_bins):
     return rec.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(session, seconds, seed=7):
-    """The fp64 oracle on a bounded sample of the same workload, timed on the host."""
+def cpu_baseline(session, seconds, threads=1, seed=7):
+    """The fp64 oracle on a bounded sample of the same workload, timed on the host with BLAS
+    limited to `threads` threads."""
     sys.path.insert(0, ROOT)
     from threadpoolctl import threadpool_limits
 
@@ -82,7 +83,7 @@ def cpu_baseline(session, seconds, seed=7):
     order = [(int(b), int(l)) for b, l in zip(rng.integers(0, wl.batch, 10**4), rng.choice(session.layers, 10**4))]
     done_bytes, spent, pairs, max_abs = 0, 0.0, 0, 0.0
     P, G, L = g.page_size, g.num_groups, g.num_layers
-    with threadpool_limits(limits=1):
+    with threadpool_limits(limits=threads):
         for b, l in order:
             if spent >= seconds:
                 break
@@ -106,9 +107,10 @@ def cpu_baseline(session, seconds, seed=7):
             pairs += 1
             got = session.out[l, b].float().cpu().numpy().astype(np.float64)
             max_abs = max(max_abs, float(np.abs(got - O[b]).max()))
-    return {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+    return {"value": done_bytes / spent / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
             "sample": f"{pairs} (request, layer) pairs x all {g.num_kv_heads} KV heads of the same workload, "
-                      f"{done_bytes / 1e9:.3f} GB of retained KV, {spent:.1f} s, BLAS pinned to 1 thread",
+                      f"{done_bytes / 1e9:.3f} GB of retained KV, {spent:.1f} s, BLAS limited to {threads} "
+                      f"thread{'s' if threads > 1 else ''}",
             "gpu_vs_oracle_max_abs": max_abs}
 
 
@@ -232,10 +234,12 @@ def main():
             torch.cuda.synchronize()
             lay_ms += np.array([a.elapsed_time(b) for a, b in evs])
         lay_ms /= nrep
+        busy = s.worker_busy(stream)   # an extra untimed step with per-worker stamps
     launch_bytes = np.array([s.t.kv_bytes(l) for l in s.layers], dtype=np.float64)
     achieved = float(launch_bytes.sum() / (lay_ms.sum() * 1e-3) / 1e9)
     imb = [s.bin_load_stats(l) for l in s.layers]
     planned_imbalance = float(np.mean([mx / mean for mx, mean in imb]))
+    measured_imbalance = float(np.mean([mx / mean for mx, mean in busy]))
     value = kv_bytes_step / (ms_per_step * 1e-3) / 1e9
     traffic = measured_traffic(wl.name, args.mode, s.n_bins)
     res = {
@@ -252,6 +256,7 @@ def main():
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),
         "plan_build_us": round(s.plan_build_us, 1),
         "load_imbalance_planned": round(planned_imbalance, 4),
+        "load_imbalance_measured": round(measured_imbalance, 4),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic,
@@ -262,7 +267,11 @@ def main():
     }
     if not args.no_cpu_baseline:
         log(f"[bench] cpu_baseline: oracle on a bounded sample (~{args.cpu_seconds:.0f} s)")
-        res["cpu_baseline"] = cpu_baseline(s, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(s, args.cpu_seconds, threads=1)
+        # the machine's CPU share: OMP_NUM_THREADS when the environment sets it
+        cores = min(len(os.sched_getaffinity(0)), int(os.environ.get("OMP_NUM_THREADS", "0")) or 10**6)
+        if cores > 1:
+            res["cpu_baseline_all_cores"] = cpu_baseline(s, args.cpu_seconds * 2 / 3, threads=cores, seed=8)
     print(json.dumps(res), flush=True)
 
 

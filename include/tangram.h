@@ -199,8 +199,9 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
  * ragged cache of Section 4.2): for every request b and query head qh with
  * KV head h = qh / gqa,
  *   O[b][qh] = softmax(K_h q * sm_scale) V_h   over the retained rows of h,
- * executed as the work items of a tg_build_plan partition: workgroup k of
- * the decode launch runs the items of bin k; an item with out_idx >= 0
+ * executed as the work items of a tg_build_plan partition: worker k of the
+ * decode launch (one wave in the bf16 head_dim-128 kernel, one workgroup
+ * otherwise) runs the items of bin k; an item with out_idx >= 0
  * writes an fp32 partial (o, lse) to the workspace, and a second launch on the
  * same stream (only when num_partials > 0) merges the partials of every split
  * unit with a log-sum-exp merge.
@@ -216,6 +217,11 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
  *            (fp32 partials; no initialisation needed).  Calls that share a
  *            workspace must not overlap in time.
  *   sm_scale: 0 means 1/sqrt(d).
+ *   timestamps [n_bins][2] uint64, or NULL: worker k writes the GPU's
+ *            constant-rate real-time counter (s_memrealtime, 100 MHz on
+ *            MI355X) when it starts bin k and when it has finished it, for
+ *            measuring the load imbalance across workers.  Empty bins write
+ *            equal stamps.
  * Supported: dtype TG_F32 or TG_BF16, head_dim 64 or 128, page_size 16,
  * gqa 1..16 (else TG_ERR_UNSUPPORTED).  hip_stream is a hipStream_t (NULL =
  * default stream).  Returns TG_ERR_HIP if a launch fails. */
@@ -238,6 +244,7 @@ typedef struct {
   float sm_scale;
   void* workspace;
   size_t workspace_bytes;
+  uint64_t* timestamps;
 } tg_decode_args;
 
 size_t  tg_decode_workspace_bytes(const tg_geometry* geom, int32_t batch, int32_t num_partials);

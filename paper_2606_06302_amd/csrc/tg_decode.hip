@@ -110,6 +110,7 @@ struct DecodeParams {
   int32_t num_kv_heads;
   int32_t n_bins;
   int32_t gqa;               // query heads per KV head
+  uint64_t* timestamps;      // [n_bins][2] start / end stamps, or NULL
   float scale_log2;          // sm_scale * log2(e)
   float scale;               // sm_scale
 };
@@ -185,6 +186,7 @@ __global__ void __launch_bounds__(kBlock) tg_decode_kernel(DecodeParams p, const
   const int r = lane / CPR;
   const int it_begin = bin_offsets[blockIdx.x], it_end = bin_offsets[blockIdx.x + 1];
   const float cs = p.scale_log2;
+  const uint64_t t_start = __builtin_amdgcn_s_memrealtime();
 
   for (int it = it_begin; it < it_end; ++it) {
     const tg_work_item item = items[it];
@@ -291,6 +293,10 @@ __global__ void __launch_bounds__(kBlock) tg_decode_kernel(DecodeParams p, const
     __syncthreads();
     finish_item<T, GQA, D>(p, item, sm_m, sm_l, &sm_acc[0][0][0], GQA * D);
     __syncthreads();
+  }
+  if (p.timestamps && threadIdx.x == 0) {   // one lane, vector stores
+    p.timestamps[2 * blockIdx.x] = t_start;
+    p.timestamps[2 * blockIdx.x + 1] = __builtin_amdgcn_s_memrealtime();
   }
 }
 
@@ -416,8 +422,15 @@ __global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, 
   const int wave = wave_id();
   const int bin = blockIdx.x * kFastWorkers + wave;
   if (bin >= p.n_bins) return;
+  const uint64_t t_start = __builtin_amdgcn_s_memrealtime();
   const int it_begin = bin_offsets[bin], it_end = bin_offsets[bin + 1];
-  if (it_begin >= it_end) return;
+  if (it_begin >= it_end) {
+    if (p.timestamps && lane == 0) {   // one lane, vector stores
+      p.timestamps[2 * bin] = t_start;
+      p.timestamps[2 * bin + 1] = t_start;
+    }
+    return;
+  }
   const int G = p.gqa;
   const int col = lane & 15;            // head column of the MFMA tiles
   const int rb = lane >> 4;             // row block: tokens / dims 4rb..4rb+3
@@ -604,6 +617,10 @@ __global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, 
     if (++it == it_end) break;
   }
   wait_vmcnt<0>();
+  if (p.timestamps && lane == 0) {   // one lane, vector stores
+    p.timestamps[2 * bin] = t_start;
+    p.timestamps[2 * bin + 1] = __builtin_amdgcn_s_memrealtime();
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -760,6 +777,7 @@ int32_t tg_decode(const tg_decode_args* a, void* hip_stream) {
   p.num_kv_heads = g.num_kv_heads;
   p.n_bins = a->n_bins;
   p.gqa = gqa;
+  p.timestamps = a->timestamps;
   p.scale = a->sm_scale != 0.f ? a->sm_scale : 1.0f / std::sqrt((float)g.head_dim);
   p.scale_log2 = p.scale * kLog2e;
   if (a->num_items == 0) return TG_OK;

@@ -106,6 +106,23 @@ class DecodeSession:
         for l in self.layers:
             tg.tg_decode(self.dplans[l].args, stream)
 
+    def worker_busy(self, stream=None):
+        """Runs one step with per-worker start/end stamps (s_memrealtime ticks) and returns, per
+        layer, (max, mean) of the busy time over the workers that had work, in microseconds."""
+        res = []
+        for l in self.layers:
+            dp = self.dplans[l]
+            ts = torch.zeros(2 * dp.host["num_bins"], dtype=torch.int64, device=self.device)
+            args = tg.tg_decode_args.from_buffer_copy(dp.args)
+            args.timestamps = ts.data_ptr()
+            tg.tg_decode(args, stream)
+            torch.cuda.synchronize()
+            t = ts.view(-1, 2).cpu().numpy()
+            busy = (t[:, 1] - t[:, 0]).astype(np.float64) / REALTIME_HZ * 1e6
+            busy = busy[np.diff(self.plans[l]["bin_offsets"]) > 0]
+            res.append((float(busy.max()), float(busy.mean())))
+        return res
+
     def bin_load_stats(self, l):
         """Planned token load per bin: (max, mean)."""
         p = self.plans[l]
@@ -115,6 +132,10 @@ class DecodeSession:
         loads = np.zeros(len(bo) - 1, dtype=np.int64)
         np.add.at(loads, np.repeat(np.arange(len(bo) - 1), np.diff(bo)), lens)
         return float(loads.max()), float(loads.mean())
+
+
+# s_memrealtime runs at a constant 100 MHz on MI300-class GPUs
+REALTIME_HZ = 100e6
 
 
 class PrefillSession:

@@ -43,7 +43,8 @@ class tg_decode_args(C.Structure):
                 ("items", C.c_void_p), ("bin_offsets", C.c_void_p), ("n_bins", C.c_int32),
                 ("num_items", C.c_int32), ("unit_splits", C.c_void_p), ("unit_partial_base", C.c_void_p),
                 ("num_partials", C.c_int32), ("out", C.c_void_p), ("lse", C.c_void_p),
-                ("sm_scale", C.c_float), ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t)]
+                ("sm_scale", C.c_float), ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t),
+                ("timestamps", C.c_void_p)]
 
 
 class tg_prefill_args(C.Structure):
@@ -226,12 +227,14 @@ def _stream(stream):
 
 def make_decode_args(geom, batch, dtype, q, kv_pool, pt_pages, items, bin_offsets, n_bins, num_items,
                      unit_splits, unit_partial_base, num_partials, out, lse=None, sm_scale=0.0,
-                     workspace=None) -> tg_decode_args:
-    """Packs a tg_decode_args from device tensors (kept alive by the caller)."""
+                     workspace=None, timestamps=None) -> tg_decode_args:
+    """Packs a tg_decode_args from device tensors (kept alive by the caller); timestamps is an
+    int64 device tensor of 2*n_bins entries, or None."""
     return tg_decode_args(_geom(geom), int(batch), int(dtype), _dptr(q), _dptr(kv_pool), _dptr(pt_pages),
                           _dptr(items), _dptr(bin_offsets), int(n_bins), int(num_items), _dptr(unit_splits),
                           _dptr(unit_partial_base), int(num_partials), _dptr(out), _dptr(lse), float(sm_scale),
-                          _dptr(workspace), 0 if workspace is None else workspace.numel() * workspace.element_size())
+                          _dptr(workspace), 0 if workspace is None else workspace.numel() * workspace.element_size(),
+                          _dptr(timestamps))
 
 
 def tg_decode(args: tg_decode_args, stream=None):

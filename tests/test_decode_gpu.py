@@ -188,3 +188,30 @@ def test_full_size_config3_sampled():
         compare_layer(s, layer, pairs=sample_pairs(wl, 10, seed=layer), what=f"config 3 layer {layer}")
     del s
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("dtype,d,gqa", [("bf16", 128, 8), ("f32", 64, 2)])
+def test_worker_timestamps(dtype, d, gqa):
+    """The optional per-worker stamps: ordered, present for every bin (empty bins
+    stamp start == end), and the outputs stay bitwise identical."""
+    _gpu()
+    from paper_2606_06302_amd import tangram as tg
+    g = Geometry(1, 4, 4 * gqa, d, 16, 2)
+    wl = custom(880 + d, g, 3, dtype, (40, 2000), kv_scale=0.5)
+    s = _small_session(wl, mode=0, n_bins=50, split_target=60)
+    ref = s.out.clone()
+    dp = s.dplans[0]
+    nb = dp.host["num_bins"]
+    ts = torch.full((2 * nb,), -1, dtype=torch.int64, device="cuda")
+    args = tg.tg_decode_args.from_buffer_copy(dp.args)
+    args.timestamps = ts.data_ptr()
+    s.out.zero_()
+    tg.tg_decode(args)
+    torch.cuda.synchronize()
+    assert torch.equal(s.out, ref)
+    t = ts.view(-1, 2).cpu().numpy()
+    assert (t >= 0).all() and (t[:, 1] >= t[:, 0]).all()
+    empty = np.diff(s.plans[0]["bin_offsets"]) == 0
+    assert (t[empty, 1] == t[empty, 0]).all()
+    busy = s.worker_busy()
+    assert len(busy) == 1 and busy[0][0] >= busy[0][1] > 0
