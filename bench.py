@@ -166,6 +166,7 @@ def main():
     ap.add_argument("--n-bins", type=int, default=0)
     ap.add_argument("--split-target", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of a HIP graph replay")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0)
     ap.add_argument("--free-order", default="shuffled", choices=["shuffled", "sequential"],
@@ -212,12 +213,19 @@ def main():
             s.run_step(stream)
         stream.synchronize()
         log(f"[bench] warmup {args.warmup} steps done")
-        # whole-step timing
+        # whole-step timing: the 64 layers' launches captured once in a HIP graph (or eager)
+        graph = None if args.no_graph else s.capture_step(stream)
+        if graph is not None:
+            graph.replay()
+            stream.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         e0.record(stream)
         for _ in range(args.steps):
-            s.run_step(stream)
+            if graph is not None:
+                graph.replay()
+            else:
+                s.run_step(stream)
         e1.record(stream)
         torch.cuda.synchronize()
         ms_per_step = e0.elapsed_time(e1) / args.steps
@@ -250,7 +258,7 @@ def main():
                    "kv_heads": g.num_kv_heads, "head_dim": g.head_dim, "page_size": g.page_size,
                    "heads_per_group": g.heads_per_group, "plan": args.mode, "n_bins": s.n_bins,
                    "split_target": s.split_target, "kv_bytes_per_step": kv_bytes_step,
-                   "free_order": args.free_order,
+                   "free_order": args.free_order, "launch": "eager" if args.no_graph else "hip graph",
                    "parallelism": "single GPU"},
         "us_per_step": round(ms_per_step * 1e3, 1),
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),

@@ -106,6 +106,15 @@ class DecodeSession:
         for l in self.layers:
             tg.tg_decode(self.dplans[l].args, stream)
 
+    def capture_step(self, stream):
+        """Captures one step (every layer's decode and merge launches) into a HIP graph on
+        `stream`; replaying it re-runs the step with the same buffers."""
+        graph = torch.cuda.CUDAGraph()
+        stream.synchronize()
+        with torch.cuda.graph(graph, stream=stream):
+            self.run_step(stream)
+        return graph
+
     def worker_busy(self, stream=None):
         """Runs one step with per-worker start/end stamps (s_memrealtime ticks) and returns, per
         layer, (max, mean) of the busy time over the workers that had work, in microseconds."""

@@ -215,3 +215,26 @@ def test_worker_timestamps(dtype, d, gqa):
     assert (t[empty, 1] == t[empty, 0]).all()
     busy = s.worker_busy()
     assert len(busy) == 1 and busy[0][0] >= busy[0][1] > 0
+
+
+def test_graph_replay_matches_eager_bitwise():
+    """A captured step replayed several times, with eager work and synchronisation
+    in between, reproduces the eager outputs bit for bit on every replay."""
+    _gpu()
+    g = Geometry(3, 8, 64, 128, 16, 2)
+    wl = custom(1357, g, 4, "bf16", (200, 4000), kv_scale=0.5)
+    s = _small_session(wl, mode=3, n_bins=64)
+    ref_out, ref_lse = s.out.clone(), s.lse.clone()
+    st = torch.cuda.Stream()
+    graph = s.capture_step(st)
+    for rep in range(4):
+        s.out.zero_()
+        s.lse.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(s.out, ref_out), rep
+        assert torch.equal(s.lse, ref_lse), rep
+        s.run_step()          # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.equal(s.out, ref_out), rep
