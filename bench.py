@@ -167,6 +167,8 @@ def main():
     ap.add_argument("--split-target", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of a HIP graph replay")
+    ap.add_argument("--calibrate-xcd", action="store_true",
+                    help="rebuild the fill plans with per-XCD bin weights measured in one stamped step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0)
     ap.add_argument("--free-order", default="shuffled", choices=["shuffled", "sequential"],
@@ -212,6 +214,14 @@ def main():
         for _ in range(args.warmup):
             s.run_step(stream)
         stream.synchronize()
+        xcd_speed = None
+        if mode == tg.TG_PLAN_AOT_FILL and args.calibrate_xcd:
+            # ahead-of-time calibration (untimed): one stamped step measures each XCD's pages per
+            # microsecond, and the fill plans are rebuilt with bin weights in proportion
+            xcd_speed = s.calibrate_xcd_weights(stream)
+            log(f"[bench] per-XCD relative speed {np.round(xcd_speed, 3).tolist()}; plans rebuilt")
+            s.run_step(stream)
+            stream.synchronize()
         log(f"[bench] warmup {args.warmup} steps done")
         # whole-step timing: the 64 layers' launches captured once in a HIP graph (or eager)
         graph = None if args.no_graph else s.capture_step(stream)
@@ -259,6 +269,8 @@ def main():
                    "heads_per_group": g.heads_per_group, "plan": args.mode, "n_bins": s.n_bins,
                    "split_target": s.split_target, "kv_bytes_per_step": kv_bytes_step,
                    "free_order": args.free_order, "launch": "eager" if args.no_graph else "hip graph",
+                   "bin_weights": None if xcd_speed is None else "per-XCD speed from one stamped step "
+                                  + str(np.round(xcd_speed, 3).tolist()),
                    "parallelism": "single GPU"},
         "us_per_step": round(ms_per_step * 1e3, 1),
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),

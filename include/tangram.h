@@ -155,10 +155,15 @@ int32_t tg_decode_max_ctas(const tg_geometry* geom, int32_t dtype, int32_t devic
  *   NAIVE:   s_u = 1, and one bin per unit (n_bins ignored: B*H bins)
  *   UNIFORM: s_u = min(n_u, max(1, ceil(n_bins / (B*H)))), one bin per chunk
  *   AOT_FILL: the units' pages laid end to end in unit order are cut into
- *            n_bins ranges [k*NP/n_bins, (k+1)*NP/n_bins) (NP = sum n_u); bin k
- *            gets the pieces of the units its range covers (in unit order), so
- *            every bin holds an equal share of the pages and every unit gets
- *            bins in proportion to its length; s_u = number of pieces of u.
+ *            n_bins ranges [cut_k, cut_{k+1}), cut_k = floor(NP * W_k / W)
+ *            (NP = sum n_u, W_k = sum of bin_weights[j] over j < k, W = the
+ *            sum of all weights; every weight is 1 when bin_weights is NULL,
+ *            giving [k*NP/n_bins, (k+1)*NP/n_bins)); bin k gets the pieces of
+ *            the units its range covers (in unit order), so bins hold page
+ *            shares in proportion to their weights and every unit gets bins
+ *            in proportion to its length; s_u = number of pieces of u.
+ *            Weights let a plan give less work to workers that run slower
+ *            (e.g. measured per-XCD throughput differences).
  *   chunk c < s_u of unit u covers pages [c*n_u/s_u, (c+1)*n_u/s_u) and tokens
  *   [p0*P, min(p1*P, kv_len)).  out_idx = -1 when s_u == 1, else
  *   unit_partial_base[u] + c (partials numbered over units in order).
@@ -168,7 +173,8 @@ int32_t tg_decode_max_ctas(const tg_geometry* geom, int32_t dtype, int32_t devic
  *   items[bin_offsets[k] .. bin_offsets[k+1]).
  * Arguments (host): kv_len [B][L][H] and pt_offsets [B*L*G+1] from tg_reserve;
  *   group_of, slot_of [L][H]; 0 <= layer < L; n_bins >= 1 (AOT, AOT_FILL, UNIFORM);
- *   split_target >= 1 (AOT); items [item_capacity] out, or NULL for a size
+ *   split_target >= 1 (AOT); bin_weights [n_bins] in 1..65535, or NULL
+ *   (AOT_FILL only; NULL otherwise); items [item_capacity] out, or NULL for a size
  *   query (num_items, num_partials and the bin count are still written);
  *   bin_offsets [bins+1] out, where bins = n_bins (AOT, AOT_FILL), B*H (NAIVE) or the
  *   number of chunks (UNIFORM) - its capacity is bin_capacity entries;
@@ -188,7 +194,7 @@ typedef struct {
 
 int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, const int32_t* kv_len,
                       const int64_t* pt_offsets, const int32_t* group_of, const int32_t* slot_of,
-                      int32_t mode, int32_t n_bins, int32_t split_target,
+                      int32_t mode, int32_t n_bins, int32_t split_target, const int32_t* bin_weights,
                       tg_work_item* items, int32_t item_capacity,
                       int32_t* bin_offsets, int32_t bin_capacity,
                       int32_t* unit_splits, int32_t* unit_partial_base,

@@ -216,7 +216,7 @@ def split_map(budget, perm, heads_per_group, n_cta):
 # ------------------------------------------- executed partition for one layer
 
 def partition_plan(kv_len, offsets, group_of, slot_of, layer, *, num_layers, num_groups, page_size,
-                   mode=MODE_AOT, n_bins=1, split_target=1):
+                   mode=MODE_AOT, n_bins=1, split_target=1, bin_weights=None):
     """Balanced split-KV partition of one layer of one batch.
 
     Work unit u = (request b, KV head h), in order b, h.  In AOT mode unit u is
@@ -230,9 +230,11 @@ def partition_plan(kv_len, offsets, group_of, slot_of, layer, *, num_layers, num
     one bin per chunk.
 
     FILL: the units' pages are laid end to end in (b, h) order and cut into
-    n_bins equal page ranges, one per bin; a unit is split wherever a range
-    boundary falls inside it, so every bin gets floor/ceil of total/n_bins
-    pages and every unit gets bins in proportion to its length.
+    n_bins page ranges, one per bin, whose sizes follow bin_weights (all equal
+    when None): range k starts at floor(total * (w_0 + ... + w_{k-1}) / sum w).
+    A unit is split wherever a range boundary falls inside it, so with equal
+    weights every bin gets floor/ceil of total/n_bins pages, and every unit gets
+    bins in proportion to its length.
 
     Returns dict(items=[(pt_base, b, h, slot, t0, t1, out_idx)], bin_offsets,
     unit_splits [B][H], unit_partial_base [B][H], num_partials, bin_load).
@@ -241,7 +243,8 @@ def partition_plan(kv_len, offsets, group_of, slot_of, layer, *, num_layers, num
     P = page_size
     lens = [[int(kv_len[b, layer, h]) for h in range(H)] for b in range(Bn)]
     if mode == MODE_FILL:
-        return _fill_plan(lens, offsets, group_of, slot_of, layer, num_layers, num_groups, P, n_bins)
+        return _fill_plan(lens, offsets, group_of, slot_of, layer, num_layers, num_groups, P, n_bins,
+                          bin_weights)
     W = sum(sum(r) for r in lens)
     n_units = Bn * H
     splits = np.zeros((Bn, H), dtype=np.int64)
@@ -298,7 +301,7 @@ def partition_plan(kv_len, offsets, group_of, slot_of, layer, *, num_layers, num
                 bin_load=np.array(bin_load, dtype=np.int64))
 
 
-def _fill_plan(lens, offsets, group_of, slot_of, layer, num_layers, num_groups, P, n_bins):
+def _fill_plan(lens, offsets, group_of, slot_of, layer, num_layers, num_groups, P, n_bins, bin_weights=None):
     Bn, H = len(lens), len(lens[0])
     units = [(b, h) for b in range(Bn) for h in range(H)]
     npages = [-(-lens[b][h] // P) for b, h in units]
@@ -306,9 +309,13 @@ def _fill_plan(lens, offsets, group_of, slot_of, layer, num_layers, num_groups, 
     for n in npages:
         start.append(start[-1] + n)
     total = start[-1]
+    weights = [1] * n_bins if bin_weights is None else [int(w) for w in bin_weights]
+    before = [0]
+    for w in weights:
+        before.append(before[-1] + w)
     pieces = []                               # (bin, unit index, first page, end page)
     for k in range(n_bins):
-        lo, hi = k * total // n_bins, (k + 1) * total // n_bins
+        lo, hi = total * before[k] // before[-1], total * before[k + 1] // before[-1]
         for u in range(len(units)):
             a, z = max(lo, start[u]), min(hi, start[u + 1])
             if a < z:

@@ -53,20 +53,28 @@ using tg::fail;
 // into n_bins equal page ranges; a unit is split wherever a boundary falls in it.
 static int32_t fill_plan(int L, int G, int H, int64_t P, int batch, int layer, const std::vector<int64_t>& len,
                          const std::vector<int64_t>& base, const int32_t* slot_of, int32_t n_bins,
-                         tg_work_item* items, int32_t item_capacity, int32_t* bin_offsets, int32_t bin_capacity,
-                         int32_t* unit_splits, int32_t* unit_partial_base, int32_t* num_items, int32_t* num_bins,
-                         int32_t* num_partials) {
+                         const int32_t* bin_weights, tg_work_item* items, int32_t item_capacity,
+                         int32_t* bin_offsets, int32_t bin_capacity, int32_t* unit_splits, int32_t* unit_partial_base,
+                         int32_t* num_items, int32_t* num_bins, int32_t* num_partials) {
   (void)L;
   (void)G;
   const int64_t n_units = (int64_t)batch * H;
   std::vector<int64_t> start(n_units + 1, 0);
   for (int64_t u = 0; u < n_units; ++u) start[u + 1] = start[u] + ceil_div(len[u], P);
   const int64_t total = start[n_units];
+  // bin k covers pages [cut[k], cut[k+1]): cut[k] = floor(total * W_k / W), W_k the
+  // weight of the bins before k (every weight 1 when bin_weights is NULL)
+  std::vector<int64_t> cut(n_bins + 1);
+  {
+    std::vector<int64_t> wsum(n_bins + 1, 0);
+    for (int32_t k = 0; k < n_bins; ++k) wsum[k + 1] = wsum[k] + (bin_weights ? bin_weights[k] : 1);
+    for (int32_t k = 0; k <= n_bins; ++k) cut[k] = (int64_t)((__int128)total * wsum[k] / wsum[n_bins]);
+  }
   // pass 1: count pieces per unit (bins walk the units monotonically)
   std::vector<int64_t> pieces(n_units, 0);
   int64_t n_items = 0;
   for (int64_t k = 0, u = 0; k < n_bins; ++k) {
-    const int64_t lo = k * total / n_bins, hi = (k + 1) * total / n_bins;
+    const int64_t lo = cut[k], hi = cut[k + 1];
     while (u < n_units && start[u + 1] <= lo) ++u;
     for (int64_t v = u; v < n_units && start[v] < hi; ++v)
       if (std::max(lo, start[v]) < std::min(hi, start[v + 1])) {
@@ -93,7 +101,7 @@ static int32_t fill_plan(int L, int G, int H, int64_t P, int batch, int layer, c
   int64_t it = 0;
   bin_offsets[0] = 0;
   for (int64_t k = 0, u = 0; k < n_bins; ++k) {
-    const int64_t lo = k * total / n_bins, hi = (k + 1) * total / n_bins;
+    const int64_t lo = cut[k], hi = cut[k + 1];
     while (u < n_units && start[u + 1] <= lo) ++u;
     for (int64_t v = u; v < n_units && start[v] < hi; ++v) {
       const int64_t a = std::max(lo, start[v]), z = std::min(hi, start[v + 1]);
@@ -259,7 +267,8 @@ int32_t tg_split_map(const tg_geometry* geom, const double* budget, const int32_
 // Balanced split-KV partition of one layer (Algorithm 1's rule on the batch).
 int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, const int32_t* kv_len,
                       const int64_t* pt_offsets, const int32_t* group_of, const int32_t* slot_of, int32_t mode,
-                      int32_t n_bins, int32_t split_target, tg_work_item* items, int32_t item_capacity,
+                      int32_t n_bins, int32_t split_target, const int32_t* bin_weights, tg_work_item* items,
+                      int32_t item_capacity,
                       int32_t* bin_offsets, int32_t bin_capacity, int32_t* unit_splits, int32_t* unit_partial_base,
                       int32_t* num_items, int32_t* num_bins, int32_t* num_partials) {
   if (int32_t rc = tg::check_geometry(geom)) return rc;
@@ -274,6 +283,12 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
     return fail(TG_ERR_INVALID_ARG, "unknown plan mode %d", mode);
   if (mode != TG_PLAN_NAIVE && n_bins < 1) return fail(TG_ERR_INVALID_ARG, "n_bins must be >= 1");
   if (mode == TG_PLAN_AOT && split_target < 1) return fail(TG_ERR_INVALID_ARG, "split_target must be >= 1");
+  if (bin_weights && mode != TG_PLAN_AOT_FILL)
+    return fail(TG_ERR_INVALID_ARG, "bin_weights apply to TG_PLAN_AOT_FILL only");
+  if (bin_weights)
+    for (int32_t k = 0; k < n_bins; ++k)
+      if (bin_weights[k] < 1 || bin_weights[k] > 65535)
+        return fail(TG_ERR_INVALID_ARG, "bin_weights[%d] = %d outside [1, 65535]", k, bin_weights[k]);
   const int64_t n_units = (int64_t)batch * H;
   // lengths of this layer, checked against the capacity of their table
   std::vector<int64_t> len(n_units), base(n_units);
@@ -294,8 +309,8 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
       W += len[u];
     }
   if (mode == TG_PLAN_AOT_FILL)
-    return fill_plan(L, G, H, P, batch, layer, len, base, slot_of, n_bins, items, item_capacity, bin_offsets,
-                     bin_capacity, unit_splits, unit_partial_base, num_items, num_bins, num_partials);
+    return fill_plan(L, G, H, P, batch, layer, len, base, slot_of, n_bins, bin_weights, items, item_capacity,
+                     bin_offsets, bin_capacity, unit_splits, unit_partial_base, num_items, num_bins, num_partials);
   // split counts
   std::vector<int64_t> splits(n_units);
   int64_t total = 0, nparts = 0;

@@ -68,14 +68,10 @@ class DecodeSession:
         if split_target is None:
             split_target = 2 * n_bins   # measured best on the 64-layer step (bins x {1,2,4,8})
         self.mode, self.n_bins, self.split_target = mode, n_bins, split_target
+        self.bin_weights = None
         L, B = g.num_layers, wl.batch
         self.layers = list(range(L)) if layers is None else list(layers)
-        # plans (timed: this is the host planning cost the paper's Table 1 measures for a runtime planner)
-        t0 = time.perf_counter()
-        self.plans = {l: tg.tg_build_plan(g, B, l, self.t.kv_len, self.t.pt_offsets, self.t.group_of,
-                                          self.t.slot_of, mode, n_bins, split_target) for l in self.layers}
-        self.plan_build_us = (time.perf_counter() - t0) * 1e6
-        self.dplans = {l: upload_plan(g, B, p, device) for l, p in self.plans.items()}
+        self._build_plans()
         # pool
         if pool is not None:
             self.pool = pool
@@ -95,9 +91,55 @@ class DecodeSession:
             device_normal_(self.q, wl, S_Q, wl.q_scale)
         self.out = torch.zeros(L, B, g.num_q_heads, g.head_dim, dtype=self.dtype, device=device)
         self.lse = torch.zeros(L, B, g.num_q_heads, dtype=torch.float32, device=device) if want_lse else None
+        self._bind()
+
+    def _build_plans(self):
+        g, B = self.wl.geom, self.wl.batch
+        # timed: this is the host planning cost the paper's Table 1 measures for a runtime planner
+        t0 = time.perf_counter()
+        self.plans = {l: tg.tg_build_plan(g, B, l, self.t.kv_len, self.t.pt_offsets, self.t.group_of,
+                                          self.t.slot_of, self.mode, self.n_bins, self.split_target,
+                                          bin_weights=self.bin_weights) for l in self.layers}
+        self.plan_build_us = (time.perf_counter() - t0) * 1e6
+        self.dplans = {l: upload_plan(g, B, p, self.device) for l, p in self.plans.items()}
+
+    def _bind(self):
+        g, B = self.wl.geom, self.wl.batch
         for l in self.layers:
             bind_decode(self.dplans[l], g, B, self.tg_dtype, self.q[l], self.pool, self.t.d_pt_pages, self.out[l],
                         None if self.lse is None else self.lse[l])
+
+    def calibrate_xcd_weights(self, stream=None, classes=8):
+        """Measures every worker's pages per microsecond over one stamped step and rebuilds the
+        sequential-fill plans with bin weights in proportion to the speed of the worker's class.
+        Worker k runs in workgroup k // 4; workgroups are dispatched round-robin over the
+        `classes` XCDs, so class = (k // 4) % classes.  Returns the per-class relative speeds."""
+        assert self.mode == tg.TG_PLAN_AOT_FILL, "bin weights apply to the sequential-fill plan"
+        pages = np.zeros(classes)
+        busy = np.zeros(classes)
+        for l in self.layers:
+            dp = self.dplans[l]
+            nb = dp.host["num_bins"]
+            ts = torch.zeros(2 * nb, dtype=torch.int64, device=self.device)
+            args = tg.tg_decode_args.from_buffer_copy(dp.args)
+            args.timestamps = ts.data_ptr()
+            tg.tg_decode(args, stream)
+            torch.cuda.synchronize()
+            t = ts.view(-1, 2).cpu().numpy()
+            items = self.plans[l]["items"]
+            npages = -(-(items["tok_end"] - items["tok_begin"]).astype(np.int64) // self.wl.geom.page_size)
+            bo = self.plans[l]["bin_offsets"]
+            per_bin = np.add.reduceat(npages, bo[:-1]) if len(npages) else np.zeros(nb)
+            per_bin[np.diff(bo) == 0] = 0
+            cls = (np.arange(nb) // 4) % classes
+            np.add.at(pages, cls, per_bin)
+            np.add.at(busy, cls, (t[:, 1] - t[:, 0]).astype(np.float64))
+        speed = pages / np.maximum(busy, 1)
+        speed = speed / speed.mean()
+        self.bin_weights = np.round(1000 * speed[(np.arange(self.n_bins) // 4) % classes]).astype(np.int32)
+        self._build_plans()
+        self._bind()
+        return speed
 
     def run_layer(self, l, stream=None):
         tg.tg_decode(self.dplans[l].args, stream)

@@ -83,7 +83,7 @@ _SIGS = {
     "tg_reserve": (_i32, [_G, _i32, _P, _P, _P, _P, _P, _i64, _i64, _P, _P, _P, _P, _i64, _P]),
     "tg_split_map": (_i32, [_G, _P, _P, _i32, _P]),
     "tg_decode_max_ctas": (_i32, [_G, _i32, _i32, _P]),
-    "tg_build_plan": (_i32, [_G, _i32, _i32, _P, _P, _P, _P, _i32, _i32, _i32, _P, _i32, _P, _i32, _P, _P,
+    "tg_build_plan": (_i32, [_G, _i32, _i32, _P, _P, _P, _P, _i32, _i32, _i32, _P, _P, _i32, _P, _i32, _P, _P,
                              _P, _P, _P]),
     "tg_decode_workspace_bytes": (_sz, [_G, _i32, _i32]),
     "tg_decode": (_i32, [C.POINTER(tg_decode_args), _P]),
@@ -188,7 +188,7 @@ def tg_decode_max_ctas(geom, dtype, device=0) -> int:
 
 
 def tg_build_plan(geom, batch, layer, kv_len, pt_offsets, group_of, slot_of, mode=TG_PLAN_AOT, n_bins=1,
-                  split_target=1):
+                  split_target=1, bin_weights=None):
     """-> dict(items (WORK_ITEM_DTYPE), bin_offsets, unit_splits, unit_partial_base, num_items, num_bins,
     num_partials)."""
     g = _geom(geom)
@@ -200,8 +200,9 @@ def tg_build_plan(geom, batch, layer, kv_len, pt_offsets, group_of, slot_of, mod
     splits = np.zeros((batch, H), np.int32)
     base = np.zeros((batch, H), np.int32)
     ni, nb, npart = C.c_int32(0), C.c_int32(0), C.c_int32(0)
+    w = None if bin_weights is None else _host(bin_weights, np.int32)
     head = (C.byref(g), int(batch), int(layer), _ptr(kv), _ptr(off), _ptr(gof), _ptr(sof), int(mode), int(n_bins),
-            int(split_target))
+            int(split_target), _ptr(w))
     tail = (_ptr(splits), _ptr(base), C.byref(ni), C.byref(nb), C.byref(npart))
     _check(_lib.tg_build_plan(*head, None, 0, None, 0, *tail), "tg_build_plan")
     items = np.zeros(max(1, ni.value), WORK_ITEM_DTYPE)

@@ -24,7 +24,7 @@ def _items_as_tuples(items):
 
 
 def _full_compare(geom, batch, ctx, ratio, budget, free, pool, grouping=0, mode=0, n_bins=7, split_target=33,
-                  layers=None):
+                  layers=None, bin_weights=None):
     L, H, Hp = geom.num_layers, geom.num_kv_heads, geom.heads_per_group
     G = H // Hp
     perm, gof, sof = tg.tg_cluster_heads(geom, budget, grouping)
@@ -42,9 +42,10 @@ def _full_compare(geom, batch, ctx, ratio, budget, free, pool, grouping=0, mode=
         assert np.array_equal(tg.tg_split_map(geom, budget, perm, n_cta), oracle.split_map(budget, operm, Hp, n_cta))
     for layer in (range(L) if layers is None else layers):
         pl = tg.tg_build_plan(geom, batch, layer, res["kv_len"], res["pt_offsets"], gof, sof, mode, n_bins,
-                              split_target)
+                              split_target, bin_weights=bin_weights)
         opl = oracle.partition_plan(ores["kv_len"], ores["offsets"], ogof, osof, layer, num_layers=L, num_groups=G,
-                                    page_size=geom.page_size, mode=mode, n_bins=n_bins, split_target=split_target)
+                                    page_size=geom.page_size, mode=mode, n_bins=n_bins, split_target=split_target,
+                                    bin_weights=bin_weights)
         assert _items_as_tuples(pl["items"]) == opl["items"]
         assert pl["bin_offsets"].tolist() == opl["bin_offsets"].tolist()
         assert np.array_equal(pl["unit_splits"], opl["unit_splits"])
@@ -115,8 +116,12 @@ def test_random_geometries_bit_exact(data):
     pool = need + int(rng.integers(0, 30))
     free = rng.permutation(pool).astype(np.int32)
     mode = data.draw(st.sampled_from([0, 1, 2, 3]))
+    n_bins = data.draw(st.integers(1, 64))
+    weights = None
+    if mode == 3 and data.draw(st.booleans()):
+        weights = rng.integers(1, data.draw(st.sampled_from([2, 1000, 65536])), size=n_bins).astype(np.int32)
     _full_compare(geom, B, ctx, ratio, budget, free, pool, grouping=grouping, mode=mode,
-                  n_bins=data.draw(st.integers(1, 64)), split_target=data.draw(st.integers(1, 300)))
+                  n_bins=n_bins, split_target=data.draw(st.integers(1, 300)), bin_weights=weights)
 
 
 def test_fp64_ceil_pitfalls_match_oracle():
@@ -227,3 +232,20 @@ def test_prefill_schedule_errors():
         tg.tg_prefill_schedule(geom, 1, 0, 0, kv)
     with pytest.raises(tg.TangramError):
         tg.tg_prefill_schedule(geom, 1, 8, 1, kv)
+
+
+def test_weighted_fill_config3_layer_bit_exact_and_errors():
+    wl = config(3)
+    gof = tg.tg_cluster_heads(wl.geom, wl.budget)[1]
+    need = tg.tg_reserve(wl.geom, wl.ctx_len, wl.ratio, None, gof, np.zeros(0, np.int32), 0, size_query=True)
+    pool = pool_pages_for(need["pages_needed"])
+    w = np.where((np.arange(1024) // 4) % 8 % 2 == 1, 955, 1044).astype(np.int32)
+    _full_compare(wl.geom, wl.batch, wl.ctx_len, wl.ratio, wl.budget, free_list(wl, pool), pool, mode=3,
+                  n_bins=1024, split_target=1, layers=[5], bin_weights=w)
+    geom = Geometry(1, 2, 4, 128, 16, 1)
+    kv = np.full((1, 1, 2), 40, np.int32)
+    off = np.array([0, 3, 6], np.int64)
+    gof1, sof1 = np.array([[0, 1]], np.int32), np.zeros((1, 2), np.int32)
+    for bad, mode in [([0, 1], 3), ([1, 65536], 3), ([1, 1], 0)]:
+        with pytest.raises(tg.TangramError):
+            tg.tg_build_plan(geom, 1, 0, kv, off, gof1, sof1, mode, 2, 4, bin_weights=np.array(bad, np.int32))

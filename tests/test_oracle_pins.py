@@ -192,14 +192,25 @@ def test_split_map_proportional():
 
 # ------------------------------------------------------------ partition
 
-def _cfg1_plan(mode=oracle.MODE_AOT, n_bins=8, split_target=16, free=None):
+def _cfg1_plan(mode=oracle.MODE_AOT, n_bins=8, split_target=16, free=None, bin_weights=None):
     budget, ratio, ctx = cfg1_arrays()
     _, group_of, slot_of = oracle.cluster_heads(budget, 2)
     res = oracle.reserve(ratio, ctx, group_of, 2, 16, np.arange(100) if free is None else free)
     plan = oracle.partition_plan(res["kv_len"], res["offsets"], group_of, slot_of, 0, num_layers=1,
                                  num_groups=2, page_size=16, mode=mode, n_bins=n_bins,
-                                 split_target=split_target)
+                                 split_target=split_target, bin_weights=bin_weights)
     return res, group_of, slot_of, plan
+
+
+def _random_case(rng):
+    H, Hp, L, Bn, P = 8, int(rng.choice([1, 2, 4])), 2, int(rng.integers(1, 6)), int(rng.choice([1, 4, 16]))
+    budget = rng.uniform(0.01, 1.0, size=(L, H))
+    ratio = np.clip(budget[None] + rng.uniform(-.03, .03, size=(Bn, L, H)), 0.02, 1.0)
+    ctx = rng.integers(1, 700, size=Bn)
+    _, group_of, slot_of = oracle.cluster_heads(budget, Hp)
+    G = H // Hp
+    res = oracle.reserve(ratio, ctx, group_of, G, P, np.arange(100000))
+    return dict(res=res, L=L, G=G, P=P, group_of=group_of, slot_of=slot_of)
 
 
 def test_plan_config1_hand():
@@ -518,3 +529,44 @@ def test_prefill_schedule_invariants(seed):
         seq = [cost(c) for c in order.tolist()[x::n_xcd] if c >= 0]
         assert seq == sorted(seq, reverse=True)
         assert all(c == -1 for c in order.tolist()[x::n_xcd][len(seq):])
+
+
+def test_weighted_fill_plan_config1_hand():
+    """Config 1 (units of 32, 16, 8, 4 pages per request, 120 pages), two bins
+    weighted 1:2: cuts at 0, floor(120/3) = 40, 120.  Bin 0 = unit (0,0) whole
+    and the first 8 pages of (0,1); bin 1 = the rest of (0,1) and every later
+    unit.  (0,1) is the only split unit (partials 0 and 1)."""
+    _, _, _, plan = _cfg1_plan(mode=oracle.MODE_FILL, n_bins=2, bin_weights=[1, 2])
+    assert [list(it) for it in plan["items"]] == [
+        [8, 0, 0, 1, 0, 512, -1], [8, 0, 1, 0, 0, 128, 0],
+        [8, 0, 1, 0, 128, 256, 1], [0, 0, 2, 1, 0, 128, -1], [0, 0, 3, 0, 0, 64, -1],
+        [48, 1, 0, 1, 0, 512, -1], [48, 1, 1, 0, 0, 256, -1], [40, 1, 2, 1, 0, 128, -1], [40, 1, 3, 0, 0, 64, -1]]
+    assert plan["bin_offsets"].tolist() == [0, 2, 9]
+    assert plan["num_partials"] == 2
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_weighted_fill_shares(seed):
+    """Every bin holds floor/ceil of its weighted share of the pages, equal
+    weights reproduce the unweighted plan, and the pieces tile every unit."""
+    rng = np.random.default_rng(seed)
+    c = _random_case(rng)
+    res, L, G, P = c["res"], c["L"], c["G"], c["P"]
+    n_bins = int(rng.integers(1, 60))
+    w = rng.integers(1, 1000, size=n_bins)
+    for layer in range(L):
+        kw = dict(num_layers=L, num_groups=G, page_size=P, mode=oracle.MODE_FILL, n_bins=n_bins)
+        plan = oracle.partition_plan(res["kv_len"], res["offsets"], c["group_of"], c["slot_of"], layer,
+                                     bin_weights=w, **kw)
+        pages = np.zeros(n_bins, dtype=np.int64)
+        for k in range(n_bins):
+            for it in plan["items"][plan["bin_offsets"][k]:plan["bin_offsets"][k + 1]]:
+                pages[k] += -(-(it[5] - it[4]) // P)
+        total = pages.sum()
+        share = total * w / w.sum()
+        assert np.all(np.abs(pages - share) < 1)
+        assert total == sum(-(-int(x) // P) for x in res["kv_len"][:, layer, :].ravel())
+        eq = oracle.partition_plan(res["kv_len"], res["offsets"], c["group_of"], c["slot_of"], layer,
+                                   bin_weights=np.ones(n_bins, dtype=np.int64), **kw)
+        base = oracle.partition_plan(res["kv_len"], res["offsets"], c["group_of"], c["slot_of"], layer, **kw)
+        assert eq["items"] == base["items"] and eq["bin_offsets"].tolist() == base["bin_offsets"].tolist()
