@@ -31,6 +31,11 @@ in the paper's order and notation:
                         workgroups: the same idea as the decode partition
                         (cost known from the retained lengths before the step,
                         Section 4.3), longest-processing-time onto the XCDs.
+  * chunk_keep_range  - compression fused into chunked prefill (Section 4.1):
+  * top_entries         Eq. 4's per-head Top(ceil(B*N), s) applied to each
+  * compress_chunk      chunk as its KV is produced, the kept entries appended
+  * compress_plan       to the head's reserved pages, never past the
+                        reservation (the overflow rule of Section 4.1).
 
 Readings of points the paper leaves open (each also listed in the design doc):
   - ceil(B*N) is the IEEE fp64 product followed by ceil, with no epsilon.
@@ -45,6 +50,13 @@ Readings of points the paper leaves open (each also listed in the design doc):
   - Softmax scale 1/sqrt(d) unless given.
   - A prefill chunk sees all of its head's compressed history and, causally
     and inclusively, its own (uncompressed) keys.
+  - Chunk-wise compression keeps, after the first x context tokens, ceil(r*x)
+    entries of a head (Eq. 4 on the prefix), capped by the head's reserved
+    length; a chunk keeps the difference, so the counts of all chunks of a
+    context add up to exactly ceil(r*N).
+  - Top() ranks by descending score; equal scores favour the lower token
+    index, -0 equals +0, and NaN ranks below every number.  The kept entries
+    are stored in ascending token order.
 """
 from __future__ import annotations
 
@@ -504,3 +516,98 @@ def prefill_schedule(kv_len, layer, chunk_len, gqa, n_xcd, rows_per_block=256, k
         v, j = lists[k % n_xcd], k // n_xcd
         order.append(v[j][0] * row_tiles + v[j][1] if j < len(v) else -1)
     return np.array(order, dtype=np.int64), load
+
+
+# ------------------------------------ compression fused into chunked prefill
+
+def chunk_keep_range(r, capacity, chunk_start, n_tokens):
+    """Entries a prefill chunk keeps for one head (Section 4.1, Eq. 4).
+
+    Once the first x tokens of a context have been compressed, a head with
+    ratio r holds ceil(r*x) entries (Eq. 4 applied to the prefix, one fp64
+    multiply then ceil), but never more than the `capacity` reserved for it at
+    admission: an input that asks for more keeps only its highest-scoring
+    entries within the reservation (the overflow rule of Section 4.1).  A chunk
+    covering context tokens [c0, c0 + n) finds `cursor` entries already stored
+    and keeps `count` more.  Returns (cursor, count).
+    """
+    _check_ratio(float(r))
+    if chunk_start < 0 or n_tokens < 0 or capacity < 0:
+        raise OracleError("negative chunk start, token count or capacity")
+    cursor = min(math.ceil(float(r) * chunk_start), capacity)
+    end = min(math.ceil(float(r) * (chunk_start + n_tokens)), capacity)
+    return cursor, end - cursor
+
+
+def top_entries(scores, k):
+    """Top(k, s) of Eq. 4 over one head's chunk: the k highest scores.
+
+    Equal scores favour the lower index, -0.0 equals +0.0 and NaN ranks below
+    every number.  Returns the chosen indices in ascending order.
+    """
+    n = len(scores)
+    if not 0 <= k <= n:
+        raise OracleError(f"cannot keep {k} of {n} entries")
+
+    def rank_key(t):
+        s = float(scores[t])
+        return (1, 0.0, t) if math.isnan(s) else (0, -s, t)
+
+    return sorted(sorted(range(n), key=rank_key)[:k])
+
+
+def compress_chunk(k_new, v_new, scores, pool, layer, *, geom, ratio, capacity, chunk_start, chunk_tokens,
+                   offsets, pages, group_of, slot_of):
+    """Compress one prefill chunk into the ragged cache (Section 4.1).
+
+    k_new, v_new [B][C][H][d]; scores [B][H][C] (importance of every chunk
+    entry, from the compression method's scoring function); ratio [B][L][H];
+    capacity [B][L][H] (the reserved retained lengths); chunk_start [B] (context
+    tokens before the chunk); chunk_tokens [B] (valid tokens of the chunk).
+    For each (b, h) the chunk keeps Top(count, s) of its first chunk_tokens[b]
+    entries (chunk_keep_range), written in ascending token order as retained
+    entries cursor, cursor+1, ... of the head (page layout of Section 4.2.1).
+    Returns (new pool, kept [B][H] lists of chunk indices, cursor [B][H],
+    count [B][H]).  `pool` is not modified.
+    """
+    Bn, C, H, d = k_new.shape
+    out = pool.copy()
+    cursor = np.zeros((Bn, H), dtype=np.int64)
+    count = np.zeros((Bn, H), dtype=np.int64)
+    kept = [[None] * H for _ in range(Bn)]
+    for b in range(Bn):
+        n = int(chunk_tokens[b])
+        if not 0 <= n <= C:
+            raise OracleError("chunk_tokens outside [0, C]")
+        for h in range(H):
+            c0, cnt = chunk_keep_range(ratio[b, layer, h], int(capacity[b, layer, h]), int(chunk_start[b]), n)
+            idx = top_entries(scores[b, h, :n], cnt)
+            for j, t in enumerate(idx):
+                p, s, r = token_location(b, layer, h, c0 + j, num_layers=geom.num_layers,
+                                         num_groups=geom.num_groups, page_size=geom.page_size, offsets=offsets,
+                                         pages=pages, group_of=group_of, slot_of=slot_of)
+                out[p, 0, s, r] = k_new[b, t, h]
+                out[p, 1, s, r] = v_new[b, t, h]
+            cursor[b, h], count[b, h], kept[b][h] = c0, cnt, idx
+    return out, kept, cursor, count
+
+
+def compress_plan(ratio, capacity, chunk_start, chunk_tokens, offsets, group_of, slot_of, layer, *,
+                  num_layers, num_groups, rows_per_item):
+    """Work items of one chunk's compression: each (b, h) with count > 0, in
+    order b, h, is cut into pieces of at most rows_per_item kept entries (by
+    rank in ascending token order).  Item = (pt_base, b, h, slot, n_valid,
+    cursor, count, rank_begin, rank_end).  Returns (items, cursor, count)."""
+    Bn, L, H = np.asarray(ratio).shape
+    items = []
+    cursor = np.zeros((Bn, H), dtype=np.int64)
+    count = np.zeros((Bn, H), dtype=np.int64)
+    for b in range(Bn):
+        n = int(chunk_tokens[b])
+        for h in range(H):
+            c0, cnt = chunk_keep_range(ratio[b, layer, h], int(capacity[b, layer, h]), int(chunk_start[b]), n)
+            cursor[b, h], count[b, h] = c0, cnt
+            base = int(offsets[(b * num_layers + layer) * num_groups + int(group_of[layer, h])])
+            for r0 in range(0, cnt, rows_per_item):
+                items.append((base, b, h, int(slot_of[layer, h]), n, c0, cnt, r0, min(cnt, r0 + rows_per_item)))
+    return items, cursor, count

@@ -570,3 +570,216 @@ def test_weighted_fill_shares(seed):
                                    bin_weights=np.ones(n_bins, dtype=np.int64), **kw)
         base = oracle.partition_plan(res["kv_len"], res["offsets"], c["group_of"], c["slot_of"], layer, **kw)
         assert eq["items"] == base["items"] and eq["bin_offsets"].tolist() == base["bin_offsets"].tolist()
+
+
+# ------------------------------------------- compression fused into prefill
+
+COMP = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "compress_hand.json")))
+
+
+def _scores(rows):
+    return np.array([float(x) for x in rows], dtype=np.float32)
+
+
+def _hand_cache(ratio):
+    """Runs the two hand chunks through compress_chunk on a tiny paged cache whose entries store their
+    context position, and returns (per-chunk kept, per-chunk count, cache positions of each head)."""
+    g = Geometry(1, 2, 2, 2, 2, 2)
+    cap = np.array(COMP["capacity"]).reshape(1, 1, 2)
+    r = np.array(ratio, dtype=np.float64).reshape(1, 1, 2)
+    budget = np.array([COMP["ratio"]], dtype=np.float64)
+    perm, gof, sof = oracle.cluster_heads(budget, 2)
+    gl = oracle.group_lengths(cap, gof, 1)
+    npages = -(-int(gl[0, 0, 0]) // g.page_size)
+    offsets, pages = np.array([0, npages]), np.arange(npages)
+    pool = np.full((npages, 2, 2, g.page_size, g.head_dim), -1.0)
+    C = COMP["chunk_len"]
+    kept_all, counts = [], []
+    for c in range(2):
+        pos = np.arange(c * C, (c + 1) * C, dtype=np.float64)
+        k_new = np.broadcast_to(pos[None, :, None, None], (1, C, 2, 2)).copy()
+        scores = np.stack([_scores(s) for s in COMP["scores"][c]])[None]
+        pool, kept, cur, cnt = oracle.compress_chunk(k_new, -k_new, scores, pool, 0, geom=g, ratio=r, capacity=cap,
+                                                     chunk_start=[c * C], chunk_tokens=[C], offsets=offsets,
+                                                     pages=pages, group_of=gof, slot_of=sof)
+        kept_all.append(kept[0])
+        counts.append(cnt[0].tolist())
+    cache = []
+    for h in range(2):
+        n = sum(cnt[h] for cnt in counts)
+        K, V = oracle.gather_head(pool, 0, 0, h, 0, n, geom=g, offsets=offsets, pages=pages, group_of=gof,
+                                  slot_of=sof)
+        assert np.array_equal(V, -K)
+        cache.append(K[:, 0].astype(int).tolist())
+    return kept_all, counts, cache
+
+
+def test_compress_hand():
+    kept, counts, cache = _hand_cache(COMP["ratio"])
+    assert kept == COMP["kept"]
+    assert counts == COMP["count"]
+    assert cache == COMP["cache_positions"]
+    for c in range(2):
+        for h in range(2):
+            cur, cnt = oracle.chunk_keep_range(COMP["ratio"][h], COMP["capacity"][h], c * 4, 4)
+            assert [cur, cnt] == [COMP["cursor"][c][h], COMP["count"][c][h]]
+
+
+def test_compress_hand_overflow_keeps_top_within_reservation():
+    kept, counts, cache = _hand_cache(COMP["overflow_ratio"])
+    assert counts == COMP["overflow_count"]
+    assert kept == COMP["overflow_kept"]
+    assert [len(x) for x in cache] == COMP["capacity"]
+
+
+def _tiny_scores(rng, n):
+    """Scores with many ties, signed zeros, infinities and NaNs."""
+    s = rng.integers(-3, 4, size=n).astype(np.float32) / 2
+    s[rng.random(n) < 0.1] = np.nan
+    s[rng.random(n) < 0.1] = -0.0
+    s[rng.random(n) < 0.05] = np.inf
+    s[rng.random(n) < 0.05] = -np.inf
+    return s
+
+
+def _beats(s, t, u):
+    """Does entry t rank above entry u (descending score, NaN lowest, lower index on ties)?"""
+    a, b = float(s[t]), float(s[u])
+    if math.isnan(a) or math.isnan(b):
+        return (not math.isnan(a)) or (math.isnan(b) and t < u)
+    return a > b or (a == b and t < u)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_top_entries_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    for _ in range(40):
+        n = int(rng.integers(0, 12))
+        s = _tiny_scores(rng, n)
+        for k in range(n + 1):
+            kept = oracle.top_entries(s, k)
+            assert kept == sorted(set(kept)) and len(kept) == k
+            drop = [u for u in range(n) if u not in kept]
+            assert all(_beats(s, t, u) for t in kept for u in drop)
+
+
+def test_top_entries_matches_library_selection():
+    import heapq
+    rng = np.random.default_rng(3)
+    for _ in range(50):
+        n = int(rng.integers(1, 300))
+        s = (rng.integers(-20, 20, size=n) / 4).astype(np.float32)   # NaN-free, many ties
+        k = int(rng.integers(0, n + 1))
+        lib = sorted(heapq.nlargest(k, range(n), key=lambda t: (float(s[t]), -t)))
+        assert oracle.top_entries(s, k) == lib
+        assert oracle.top_entries(s, k) == sorted(np.argsort(-s, kind="stable")[:k].tolist())
+
+
+def test_chunk_counts_fp64_pitfall():
+    # 0.07*50 is 3.5000000000000004 and 0.07*100 is 7.000000000000001 in fp64
+    assert oracle.chunk_keep_range(0.07, 8, 0, 100) == (0, 8)
+    assert [oracle.chunk_keep_range(0.07, 8, c0, 50) for c0 in (0, 50)] == [(0, 4), (4, 4)]
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_chunk_counts_telescope_to_eq4(seed):
+    """Whatever the chunking, the chunks of a context keep exactly ceil(r*N) entries in all, each
+    chunk appends right after the previous one and keeps at most its own length."""
+    rng = np.random.default_rng(seed)
+    for _ in range(300):
+        N = int(rng.integers(1, 5000))
+        r = float(rng.choice([rng.uniform(0.001, 1.0), 1.0, 0.07, 0.29, 1 / 3]))
+        cap = int(oracle.retained_lengths(np.array([[[r]]]), [N])[0, 0, 0])
+        cuts = np.unique(np.concatenate([[0, N], rng.integers(0, N + 1, size=int(rng.integers(0, 6)))]))
+        nxt = 0
+        for c0, c1 in zip(cuts[:-1], cuts[1:]):
+            cur, cnt = oracle.chunk_keep_range(r, cap, int(c0), int(c1 - c0))
+            assert cur == nxt and 0 <= cnt <= c1 - c0
+            nxt = cur + cnt
+        assert nxt == cap == math.ceil(r * N)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_overflow_caps_at_reservation_and_keeps_a_subset(seed):
+    """A selection ratio above the reserved one fills the reservation exactly; a chunk that hits the
+    cap keeps a subset of what it would keep uncapped (Top(k1) within Top(k2) for k1 <= k2)."""
+    rng = np.random.default_rng(100 + seed)
+    for _ in range(100):
+        N = int(rng.integers(2, 400))
+        r_res = float(rng.uniform(0.02, 0.9))
+        r_sel = min(1.0, r_res + float(rng.uniform(0.01, 0.5)))
+        cap = math.ceil(r_res * N)
+        C = int(rng.integers(1, N + 1))
+        total = 0
+        for c0 in range(0, N, C):
+            n = min(C, N - c0)
+            s = _tiny_scores(rng, n)
+            _, cnt = oracle.chunk_keep_range(r_sel, cap, c0, n)
+            _, free_cnt = oracle.chunk_keep_range(r_sel, 10**9, c0, n)
+            assert cnt <= free_cnt
+            assert set(oracle.top_entries(s, cnt)) <= set(oracle.top_entries(s, free_cnt))
+            total += cnt
+        assert total == cap
+
+
+def test_compress_one_chunk_is_eq4_and_lands_in_pages():
+    """A single chunk holding the whole context keeps Top(ceil(r*N), s) (Eq. 4 itself), stored in
+    ascending token order at the head's retained entries 0..count-1 (page layout of Section 4.2.1)."""
+    rng = np.random.default_rng(11)
+    g = Geometry(1, 4, 8, 8, 4, 2)
+    B, C = 3, 37
+    budget = rng.uniform(0.05, 1.0, size=(1, 4))
+    ratio = np.broadcast_to(budget, (B, 1, 4)).copy()
+    perm, gof, sof = oracle.cluster_heads(budget, 2)
+    res = oracle.reserve(ratio, [C] * B, gof, 2, g.page_size, rng.permutation(200))
+    pool = rng.standard_normal((200, 2, 2, g.page_size, g.head_dim))
+    k_new = rng.standard_normal((B, C, 4, g.head_dim))
+    v_new = rng.standard_normal((B, C, 4, g.head_dim))
+    scores = _tiny_scores(rng, B * 4 * C).reshape(B, 4, C)
+    out, kept, cur, cnt = oracle.compress_chunk(k_new, v_new, scores, pool, 0, geom=g, ratio=ratio,
+                                                capacity=res["kv_len"], chunk_start=[0] * B, chunk_tokens=[C] * B,
+                                                offsets=res["offsets"], pages=res["pages"], group_of=gof,
+                                                slot_of=sof)
+    for b in range(B):
+        for h in range(4):
+            n = math.ceil(float(budget[0, h]) * C)
+            assert cur[b, h] == 0 and cnt[b, h] == n
+            assert kept[b][h] == oracle.top_entries(scores[b, h], n)
+            K, V = oracle.gather_head(out, b, 0, h, 0, n, geom=g, offsets=res["offsets"], pages=res["pages"],
+                                      group_of=gof, slot_of=sof)
+            assert np.array_equal(K, k_new[b, kept[b][h], h]) and np.array_equal(V, v_new[b, kept[b][h], h])
+    # nothing outside the written entries changed
+    touched = np.zeros(out.shape[:4], dtype=bool)
+    for b in range(B):
+        for h in range(4):
+            for i in range(int(cnt[b, h])):
+                p, s, r = oracle.token_location(b, 0, h, i, num_layers=1, num_groups=2, page_size=g.page_size,
+                                                offsets=res["offsets"], pages=res["pages"], group_of=gof,
+                                                slot_of=sof)
+                touched[p, :, s, r] = True
+    assert np.array_equal(out[~touched], pool[~touched])
+
+
+def test_compress_plan_pieces_cover_every_kept_entry():
+    rng = np.random.default_rng(5)
+    B, L, H = 4, 2, 4
+    ratio = rng.uniform(0.02, 1.0, size=(B, L, H))
+    cap = oracle.retained_lengths(ratio, [900] * B)
+    gof = np.array([[0, 0, 1, 1]] * L)
+    sof = np.array([[0, 1, 0, 1]] * L)
+    offsets = np.arange(B * L * 2 + 1) * 100
+    starts, toks = [0, 300, 600, 850], [300, 300, 300, 50]
+    for R in (1, 7, 64):
+        items, cur, cnt = oracle.compress_plan(ratio, cap, starts, toks, offsets, gof, sof, 1, num_layers=L,
+                                               num_groups=2, rows_per_item=R)
+        seen = {}
+        for base, b, h, slot, n, c0, c, r0, r1 in items:
+            assert base == offsets[(b * L + 1) * 2 + gof[1, h]] and slot == sof[1, h] and n == toks[b]
+            assert (c0, c) == (cur[b, h], cnt[b, h]) and 0 <= r0 < r1 <= c and r1 - r0 <= R
+            seen.setdefault((b, h), []).append((r0, r1))
+        assert [k for k in seen] == sorted(seen)
+        for b in range(B):
+            for h in range(H):
+                spans = seen.get((b, h), [])
+                assert sum(r1 - r0 for r0, r1 in spans) == cnt[b, h]
+                assert all(s[1] == t[0] for s, t in zip(spans, spans[1:]))
