@@ -12,6 +12,8 @@
  *   4. ragged paged split-KV decode attention plus a log-sum-exp merge, and a
  *      ragged chunked-prefill attention (Section 2.2, chunked prefill and
  *      KV-dimension parallelism).
+ *   5. compression of each prefill chunk into the reserved pages as soon as
+ *      its K and V exist (Section 4.1, Eq. 4 per head).
  *
  * Conventions
  *   - Every function returns int32_t: TG_OK (0) or a negative TG_ERR_* code.
@@ -322,6 +324,99 @@ int32_t tg_prefill_schedule(const tg_geometry* geom, int32_t batch, int32_t chun
 
 size_t  tg_prefill_workspace_bytes(const tg_prefill_args* args);
 int32_t tg_prefill(const tg_prefill_args* args, void* hip_stream);
+
+/* ------------------------- 5. compression fused into chunked prefill
+ * Section 4.1 (compression fused into chunked prefill, Eq. 4, overflow
+ * handling).  Each prefill chunk is compressed as soon as its K and V exist.
+ * For request b and KV head h with selection ratio r = ratio[b][layer][h] (or
+ * budget[layer][h] when ratio is NULL) and reserved length
+ * cap = kv_len[b][layer][h] (tg_reserve's output for the whole context), a
+ * chunk that covers context tokens [c0, c0 + n) (c0 = chunk_start[b],
+ * n = chunk_tokens[b]) finds
+ *   cursor = min(ceil(r * c0), cap)
+ * entries already stored and keeps
+ *   count  = min(ceil(r * (c0 + n)), cap) - cursor
+ * more (each product one fp64 multiply, then ceil, as in Eq. 4).  Over all
+ * chunks of a context the counts add up to ceil(r * N); a selection ratio
+ * above the reserved one keeps only the top entries that still fit, the
+ * overflow rule.  The kept entries are Top(count) of the chunk's scores:
+ * descending score, equal scores favour the lower token index, -0.0 equals
+ * +0.0 and NaN ranks below every number.  They are stored in ascending token
+ * order as the head's retained entries cursor .. cursor + count - 1 (page
+ * layout in the file header).
+ *
+ * 5a. tg_compress_plan (host, integer): counts and work items of one chunk of
+ * one layer.  Units (b, h) with count > 0, in order b, h, are cut into items
+ * of at most rows_per_item kept entries, by rank in token order.
+ *   chunk_start [B] int32 >= 0; chunk_tokens [B] int32 in [0, chunk_len];
+ *   ratio [B][L][H] float64 in (0, 1], or NULL; budget [L][H] float64 (read
+ *   when ratio is NULL); kv_len [B][L][H] and pt_offsets from tg_reserve;
+ *   group_of, slot_of [L][H]; 0 <= layer < L;
+ *   chunk_len in 1..TG_COMPRESS_MAX_CHUNK; rows_per_item in 1..TG_COMPRESS_MAX_ROWS;
+ *   items [item_capacity] out, or NULL for a size query;
+ *   keep_count [B][H] out (count); write_begin [B][H] out (cursor);
+ *   num_items out.  All host memory.
+ * Errors: TG_ERR_INVALID_ARG (also when a head's page table holds fewer than
+ * kv_len entries, or c0 + n overflows int32); TG_ERR_BUFFER_TOO_SMALL when
+ * item_capacity < num_items (keep_count, write_begin and num_items are still
+ * written). */
+typedef struct {
+  int64_t pt_base;    /* pt_offsets[(b*L+layer)*G + group_of[layer][h]] */
+  int32_t b;          /* request */
+  int32_t kv_head;    /* h */
+  int32_t slot;       /* slot_of[layer][h] */
+  int32_t n_valid;    /* chunk_tokens[b]: scores past it are not read */
+  int32_t cursor;     /* entries of the head stored before this chunk */
+  int32_t count;      /* entries this chunk keeps, >= 1 */
+  int32_t rank_begin; /* this item writes kept entries [rank_begin, rank_end) */
+  int32_t rank_end;
+} tg_compress_item;   /* 40 bytes */
+
+enum { TG_COMPRESS_MAX_CHUNK = 16384, TG_COMPRESS_MAX_ROWS = 256 };
+
+int32_t tg_compress_plan(const tg_geometry* geom, int32_t batch, int32_t layer, int32_t chunk_len,
+                         const int32_t* chunk_start, const int32_t* chunk_tokens, const double* ratio,
+                         const double* budget, const int32_t* kv_len, const int64_t* pt_offsets,
+                         const int32_t* group_of, const int32_t* slot_of, int32_t rows_per_item,
+                         tg_compress_item* items, int32_t item_capacity, int32_t* keep_count,
+                         int32_t* write_begin, int32_t* num_items);
+
+/* 5b. tg_compress (device): runs a tg_compress_plan.  Workgroup i takes item
+ * i: it selects Top(count) of its unit's scores, ranks the kept entries in
+ * token order and copies the K and V rows of ranks [rank_begin, rank_end)
+ * into their pages.
+ * DEVICE pointers:
+ *   k_new, v_new [B][C][H][d] dtype: the chunk's K and V before compression
+ *   scores  [B][H][C] float32: importance of every chunk entry (from the
+ *           compression method's scoring function); entries at or past
+ *           chunk_tokens[b] are not read
+ *   kv_pool [pool_pages][2][H_p][P][d] dtype: only the kept rows are written
+ *   pt_pages device copy of tg_reserve's output; items [num_items]
+ *   kept    [B][H][C] int32, or NULL: kept[(b*H + h)*C + j] = chunk index of
+ *           the j-th kept entry (ascending), for j < count; the rest untouched
+ * Items must come from tg_compress_plan for the same geometry, layer,
+ * chunk_len, chunk_tokens and tables: the kernel trusts them.  The items of one
+ * call write disjoint rows; calls that write the same pages must be ordered.
+ * Supported: dtype TG_F32 or TG_BF16, head_dim 64 or 128, chunk_len in
+ * 1..TG_COMPRESS_MAX_CHUNK (else TG_ERR_UNSUPPORTED / TG_ERR_INVALID_ARG).
+ * No workspace.  num_items == 0 enqueues nothing.  Returns TG_ERR_HIP if the
+ * launch fails. */
+typedef struct {
+  tg_geometry geom;
+  int32_t batch;
+  int32_t chunk_len;
+  int32_t dtype;
+  const void* k_new;
+  const void* v_new;
+  const float* scores;
+  void* kv_pool;
+  const int32_t* pt_pages;
+  const tg_compress_item* items;
+  int32_t num_items;
+  int32_t* kept;
+} tg_compress_args;
+
+int32_t tg_compress(const tg_compress_args* args, void* hip_stream);
 
 #ifdef __cplusplus
 }

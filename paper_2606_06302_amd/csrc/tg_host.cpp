@@ -138,7 +138,7 @@ const char* tg_status_string(int32_t code) {
 
 const char* tg_last_error(void) { return tg::g_last_error; }
 
-int32_t tg_version(void) { return (1 << 16) | 0; }
+int32_t tg_version(void) { return (1 << 16) | 1; }
 
 // Section 4.2.2: sort each layer's heads by ascending budget (stable, so
 // equal budgets keep ascending head index) and cut into groups of H_p.
@@ -462,3 +462,89 @@ int32_t tg_prefill_schedule(const tg_geometry* geom, int32_t batch, int32_t chun
 }
 
 }  // extern "C"
+
+// Compression fused into chunked prefill (Section 4.1): after x context tokens
+// a head holds ceil(r*x) entries (Eq. 4 on the prefix, one fp64 multiply and
+// ceil), never more than its reservation; a chunk keeps the difference.
+extern "C" int32_t tg_compress_plan(const tg_geometry* geom, int32_t batch, int32_t layer, int32_t chunk_len,
+                                    const int32_t* chunk_start, const int32_t* chunk_tokens, const double* ratio,
+                                    const double* budget, const int32_t* kv_len, const int64_t* pt_offsets,
+                                    const int32_t* group_of, const int32_t* slot_of, int32_t rows_per_item,
+                                    tg_compress_item* items, int32_t item_capacity, int32_t* keep_count,
+                                    int32_t* write_begin, int32_t* num_items) {
+  if (int32_t rc = tg::check_geometry(geom)) return rc;
+  if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
+  const int L = geom->num_layers, H = geom->num_kv_heads, Hp = geom->heads_per_group, G = H / Hp;
+  const int64_t P = geom->page_size;
+  if (layer < 0 || layer >= L) return fail(TG_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, L);
+  if (chunk_len < 1 || chunk_len > TG_COMPRESS_MAX_CHUNK)
+    return fail(TG_ERR_INVALID_ARG, "chunk_len %d outside [1, %d]", chunk_len, (int)TG_COMPRESS_MAX_CHUNK);
+  if (rows_per_item < 1 || rows_per_item > TG_COMPRESS_MAX_ROWS)
+    return fail(TG_ERR_INVALID_ARG, "rows_per_item %d outside [1, %d]", rows_per_item, (int)TG_COMPRESS_MAX_ROWS);
+  if (!chunk_start || !chunk_tokens || !kv_len || !pt_offsets || !group_of || !slot_of || !keep_count ||
+      !write_begin || !num_items)
+    return fail(TG_ERR_INVALID_ARG, "NULL array");
+  if (!ratio && !budget) return fail(TG_ERR_INVALID_ARG, "ratio and budget are both NULL");
+  if (item_capacity < 0) return fail(TG_ERR_INVALID_ARG, "negative item_capacity");
+  for (int h = 0; h < H; ++h) {
+    const int64_t i = (int64_t)layer * H + h;
+    if (group_of[i] < 0 || group_of[i] >= G || slot_of[i] < 0 || slot_of[i] >= Hp)
+      return fail(TG_ERR_INVALID_ARG, "group_of / slot_of of head %d out of range", h);
+  }
+  // validate everything before writing anything
+  for (int b = 0; b < batch; ++b) {
+    if (chunk_start[b] < 0) return fail(TG_ERR_INVALID_ARG, "chunk_start[%d] < 0", b);
+    if (chunk_tokens[b] < 0 || chunk_tokens[b] > chunk_len)
+      return fail(TG_ERR_INVALID_ARG, "chunk_tokens[%d] = %d outside [0, %d]", b, chunk_tokens[b], chunk_len);
+    if ((int64_t)chunk_start[b] + chunk_tokens[b] > INT32_MAX)
+      return fail(TG_ERR_INVALID_ARG, "chunk_start + chunk_tokens of request %d overflows int32", b);
+    for (int h = 0; h < H; ++h) {
+      const int64_t i = ((int64_t)b * L + layer) * H + h;
+      const double r = ratio ? ratio[i] : budget[(int64_t)layer * H + h];
+      if (!tg::ratio_ok(r)) return fail(TG_ERR_INVALID_ARG, "ratio of request %d head %d outside (0,1]", b, h);
+      if (kv_len[i] < 0) return fail(TG_ERR_INVALID_ARG, "kv_len of request %d head %d < 0", b, h);
+      const int64_t t = ((int64_t)b * L + layer) * G + group_of[(int64_t)layer * H + h];
+      if ((pt_offsets[t + 1] - pt_offsets[t]) * P < kv_len[i])
+        return fail(TG_ERR_INVALID_ARG, "page table of request %d head %d holds fewer than kv_len entries", b, h);
+    }
+  }
+  int64_t n_items = 0;
+  for (int b = 0; b < batch; ++b) {
+    const double c0 = (double)chunk_start[b], c1 = (double)chunk_start[b] + (double)chunk_tokens[b];
+    for (int h = 0; h < H; ++h) {
+      const int64_t i = ((int64_t)b * L + layer) * H + h;
+      const double r = ratio ? ratio[i] : budget[(int64_t)layer * H + h];
+      const int64_t cap = kv_len[i];
+      const int64_t cursor = std::min((int64_t)std::ceil(r * c0), cap);
+      const int64_t end = std::min((int64_t)std::ceil(r * c1), cap);
+      keep_count[(int64_t)b * H + h] = (int32_t)(end - cursor);
+      write_begin[(int64_t)b * H + h] = (int32_t)cursor;
+      n_items += ceil_div(end - cursor, rows_per_item);
+    }
+  }
+  if (n_items > INT32_MAX) return fail(TG_ERR_INVALID_ARG, "too many work items");
+  *num_items = (int32_t)n_items;
+  if (!items) return TG_OK;
+  if (item_capacity < n_items)
+    return fail(TG_ERR_BUFFER_TOO_SMALL, "items holds %d, need %lld", item_capacity, (long long)n_items);
+  int64_t k = 0;
+  for (int b = 0; b < batch; ++b)
+    for (int h = 0; h < H; ++h) {
+      const int32_t cnt = keep_count[(int64_t)b * H + h];
+      const int64_t lh = (int64_t)layer * H + h;
+      const int64_t base = pt_offsets[((int64_t)b * L + layer) * G + group_of[lh]];
+      for (int32_t r0 = 0; r0 < cnt; r0 += rows_per_item) {
+        tg_compress_item& it = items[k++];
+        it.pt_base = base;
+        it.b = b;
+        it.kv_head = h;
+        it.slot = slot_of[lh];
+        it.n_valid = chunk_tokens[b];
+        it.cursor = write_begin[(int64_t)b * H + h];
+        it.count = cnt;
+        it.rank_begin = r0;
+        it.rank_end = std::min(cnt, r0 + rows_per_item);
+      }
+    }
+  return TG_OK;
+}

@@ -240,3 +240,56 @@ class PrefillSession:
         hist = self.t.kv_len[:, self.layer, :].astype(np.int64)          # [B][H]
         per_row_keys = hist.sum() * C + wl.batch * g.num_kv_heads * C * (C + 1) // 2
         return int(4 * g.head_dim * g.gqa * per_row_keys)
+
+
+class CompressSession:
+    """One prefill chunk's compression into the ragged cache (one layer), on the GPU.
+
+    `tables` must reserve each request's whole context (the chunk included);
+    chunk_start[b] context tokens precede the chunk and chunk_tokens[b] of its
+    chunk_len rows are valid.  k_new, v_new [B][C][H][d] and scores [B][H][C]
+    are device tensors (drawn from the workload's seeded streams when None).
+    The counts and work items come from tg_compress_plan (host, before the
+    step); run() enqueues tg_compress."""
+
+    def __init__(self, wl, tables: Tables, pool, chunk_start, chunk_tokens, layer=0, sel_ratio="reserved",
+                 rows_per_item=64, k_new=None, v_new=None, scores=None, want_kept=True, device="cuda"):
+        from workloads import S_K, S_V, device_normal_, host_scores
+        g = wl.geom
+        B, C, H = wl.batch, wl.chunk_len, g.num_kv_heads
+        self.wl, self.t, self.layer, self.device = wl, tables, layer, device
+        self.pool = pool
+        self.dtype = TORCH_DTYPE[wl.dtype]
+        self.chunk_start = np.asarray(chunk_start, dtype=np.int32)
+        self.chunk_tokens = np.asarray(chunk_tokens, dtype=np.int32)
+        ratio = wl.ratio if isinstance(sel_ratio, str) and sel_ratio == "reserved" else sel_ratio
+        t0 = time.perf_counter()
+        self.plan = tg.tg_compress_plan(g, B, layer, C, self.chunk_start, self.chunk_tokens, ratio, wl.budget,
+                                        tables.kv_len, tables.pt_offsets, tables.group_of, tables.slot_of,
+                                        rows_per_item)
+        self.plan_us = (time.perf_counter() - t0) * 1e6
+        self.d_items = to_device(self.plan["items"] if self.plan["num_items"]
+                                 else np.zeros(1, tg.COMPRESS_ITEM_DTYPE), device)
+        if k_new is None:
+            k_new = torch.empty(B, C, H, g.head_dim, dtype=self.dtype, device=device)
+            v_new = torch.empty_like(k_new)
+            device_normal_(k_new, wl, S_K, wl.kv_scale)
+            device_normal_(v_new, wl, S_V, wl.kv_scale)
+        self.k_new, self.v_new = k_new, v_new
+        self.scores = scores if scores is not None else torch.from_numpy(host_scores(wl, (B, H, C))).to(device)
+        self.kept = torch.full((B, H, C), -1, dtype=torch.int32, device=device) if want_kept else None
+        self.args = tg.make_compress_args(g, B, C, TG_DTYPE[wl.dtype], self.k_new, self.v_new, self.scores,
+                                          self.pool, tables.d_pt_pages, self.d_items, self.plan["num_items"],
+                                          self.kept)
+
+    def run(self, stream=None):
+        tg.tg_compress(self.args, stream)
+
+    def traffic_bytes(self) -> int:
+        """Algorithmic HBM bytes of one call: the kept K and V rows read from the chunk and
+        written to the pages, the valid scores read once, and the kept indices written."""
+        g = self.wl.geom
+        esz = 4 if self.wl.dtype == "f32" else 2
+        kept = int(self.plan["keep_count"].sum())
+        scores = int(self.chunk_tokens.astype(np.int64).sum()) * g.num_kv_heads * 4
+        return kept * 2 * g.head_dim * esz * 2 + scores + (kept * 4 if self.kept is not None else 0)

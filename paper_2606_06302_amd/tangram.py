@@ -25,6 +25,13 @@ WORK_ITEM_DTYPE = np.dtype([("pt_base", "<i8"), ("b", "<i4"), ("kv_head", "<i4")
                             ("tok_begin", "<i4"), ("tok_end", "<i4"), ("out_idx", "<i4")])
 assert WORK_ITEM_DTYPE.itemsize == 32
 
+# the 40-byte tg_compress_item
+COMPRESS_ITEM_DTYPE = np.dtype([("pt_base", "<i8"), ("b", "<i4"), ("kv_head", "<i4"), ("slot", "<i4"),
+                                ("n_valid", "<i4"), ("cursor", "<i4"), ("count", "<i4"), ("rank_begin", "<i4"),
+                                ("rank_end", "<i4")])
+assert COMPRESS_ITEM_DTYPE.itemsize == 40
+TG_COMPRESS_MAX_CHUNK, TG_COMPRESS_MAX_ROWS = 16384, 256
+
 
 class TangramError(RuntimeError):
     def __init__(self, code, where, detail):
@@ -54,6 +61,12 @@ class tg_prefill_args(C.Structure):
                 ("kv_len", C.c_void_p), ("group_of", C.c_void_p), ("slot_of", C.c_void_p),
                 ("out", C.c_void_p), ("sm_scale", C.c_float), ("workspace", C.c_void_p),
                 ("workspace_bytes", C.c_size_t), ("block_order", C.c_void_p), ("num_blocks", C.c_int32)]
+
+
+class tg_compress_args(C.Structure):
+    _fields_ = [("geom", tg_geometry), ("batch", C.c_int32), ("chunk_len", C.c_int32), ("dtype", C.c_int32),
+                ("k_new", C.c_void_p), ("v_new", C.c_void_p), ("scores", C.c_void_p), ("kv_pool", C.c_void_p),
+                ("pt_pages", C.c_void_p), ("items", C.c_void_p), ("num_items", C.c_int32), ("kept", C.c_void_p)]
 
 
 # One HIP runtime per process: torch ships its own libamdhip64 (soname
@@ -90,6 +103,8 @@ _SIGS = {
     "tg_prefill_workspace_bytes": (_sz, [C.POINTER(tg_prefill_args)]),
     "tg_prefill": (_i32, [C.POINTER(tg_prefill_args), _P]),
     "tg_prefill_schedule": (_i32, [_G, _i32, _i32, _i32, _P, _i32, _P, _i32, _P]),
+    "tg_compress_plan": (_i32, [_G, _i32, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _i32, _P, _i32, _P, _P, _P]),
+    "tg_compress": (_i32, [C.POINTER(tg_compress_args), _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -272,3 +287,40 @@ def tg_prefill_workspace_bytes(args: tg_prefill_args) -> int:
 
 def tg_prefill(args: tg_prefill_args, stream=None):
     _check(_lib.tg_prefill(C.byref(args), _stream(stream)), "tg_prefill")
+
+
+def tg_compress_plan(geom, batch, layer, chunk_len, chunk_start, chunk_tokens, ratio, budget, kv_len, pt_offsets,
+                     group_of, slot_of, rows_per_item=64):
+    """-> dict(items (COMPRESS_ITEM_DTYPE), num_items, keep_count [B][H], write_begin [B][H])."""
+    g = _geom(geom)
+    H = g.num_kv_heads
+    cs = _host(chunk_start, np.int32)
+    ct = _host(chunk_tokens, np.int32)
+    r = None if ratio is None else _host(ratio, np.float64)
+    bud = None if budget is None else _host(budget, np.float64)
+    kv = _host(kv_len, np.int32)
+    off = _host(pt_offsets, np.int64)
+    gof = _host(group_of, np.int32)
+    sof = _host(slot_of, np.int32)
+    cnt = np.zeros((batch, H), np.int32)
+    wb = np.zeros((batch, H), np.int32)
+    ni = C.c_int32(0)
+    head = (C.byref(g), int(batch), int(layer), int(chunk_len), _ptr(cs), _ptr(ct), _ptr(r), _ptr(bud), _ptr(kv),
+            _ptr(off), _ptr(gof), _ptr(sof), int(rows_per_item))
+    _check(_lib.tg_compress_plan(*head, None, 0, _ptr(cnt), _ptr(wb), C.byref(ni)), "tg_compress_plan")
+    items = np.zeros(max(1, ni.value), COMPRESS_ITEM_DTYPE)
+    _check(_lib.tg_compress_plan(*head, _ptr(items), len(items), _ptr(cnt), _ptr(wb), C.byref(ni)),
+           "tg_compress_plan")
+    return dict(items=items[: ni.value], num_items=ni.value, keep_count=cnt, write_begin=wb)
+
+
+def make_compress_args(geom, batch, chunk_len, dtype, k_new, v_new, scores, kv_pool, pt_pages, items, num_items,
+                       kept=None) -> tg_compress_args:
+    """Packs a tg_compress_args from device tensors (kept alive by the caller)."""
+    return tg_compress_args(_geom(geom), int(batch), int(chunk_len), int(dtype), _dptr(k_new), _dptr(v_new),
+                            _dptr(scores), _dptr(kv_pool), _dptr(pt_pages), _dptr(items), int(num_items),
+                            _dptr(kept))
+
+
+def tg_compress(args: tg_compress_args, stream=None):
+    _check(_lib.tg_compress(C.byref(args), _stream(stream)), "tg_compress")

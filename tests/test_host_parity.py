@@ -249,3 +249,109 @@ def test_weighted_fill_config3_layer_bit_exact_and_errors():
     for bad, mode in [([0, 1], 3), ([1, 65536], 3), ([1, 1], 0)]:
         with pytest.raises(tg.TangramError):
             tg.tg_build_plan(geom, 1, 0, kv, off, gof1, sof1, mode, 2, 4, bin_weights=np.array(bad, np.int32))
+
+
+# ------------------------------------------- compression fused into prefill
+
+def _compress_compare(geom, batch, ctx, ratio, budget, sel_ratio, starts, toks, C, R, layers=None):
+    L, H, Hp = geom.num_layers, geom.num_kv_heads, geom.heads_per_group
+    G = H // Hp
+    perm, gof, sof = tg.tg_cluster_heads(geom, budget)
+    res = tg.tg_reserve(geom, ctx, ratio, budget, gof, np.arange(10**6, dtype=np.int32), 10**6)
+    for layer in (range(L) if layers is None else layers):
+        pl = tg.tg_compress_plan(geom, batch, layer, C, starts, toks, sel_ratio, budget, res["kv_len"],
+                                 res["pt_offsets"], gof, sof, R)
+        sr = sel_ratio if sel_ratio is not None else np.broadcast_to(budget, (batch, L, H))
+        items, cur, cnt = oracle.compress_plan(sr, res["kv_len"], starts, toks, res["pt_offsets"], gof, sof, layer,
+                                               num_layers=L, num_groups=G, rows_per_item=R)
+        assert _items_as_tuples(pl["items"]) == items
+        assert np.array_equal(pl["write_begin"], cur) and np.array_equal(pl["keep_count"], cnt)
+    return res
+
+
+def test_compress_plan_config5_chunk_after_history_bit_exact():
+    """Config 5's chunk (512 tokens after a 16384-token history), reserved for the whole 16896-token context."""
+    wl = config(5)
+    C = wl.chunk_len
+    starts = wl.ctx_len
+    _compress_compare(wl.geom, wl.batch, wl.ctx_len + C, wl.ratio, wl.budget, wl.ratio, starts,
+                      np.full(wl.batch, C), C, 64)
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.data())
+def test_compress_plan_random_bit_exact(data):
+    H = data.draw(st.sampled_from([1, 2, 4, 8]))
+    Hp = data.draw(st.sampled_from([h for h in (1, 2, 4, 8) if H % h == 0]))
+    L = data.draw(st.integers(1, 3))
+    P = data.draw(st.sampled_from([1, 3, 16]))
+    B = data.draw(st.integers(1, 5))
+    geom = Geometry(L, H, H, 64, P, Hp)
+    rng = np.random.default_rng(data.draw(st.integers(0, 2**31)))
+    budget = rng.uniform(0.01, 1.0, size=(L, H))
+    ratio = np.clip(budget[None] + rng.uniform(-0.05, 0.05, size=(B, L, H)), 0.01, 1.0)
+    ctx = rng.integers(1, 3000, size=B).astype(np.int32)
+    C = int(rng.integers(1, 700))
+    starts = np.array([int(rng.integers(0, c + 1)) for c in ctx], dtype=np.int32)
+    toks = np.minimum(C, np.maximum(0, ctx - starts + rng.integers(-3, 50, size=B))).astype(np.int32)
+    choice = data.draw(st.sampled_from(["same", "overflow", "budget"]))
+    sel = {"same": ratio, "overflow": np.minimum(1.0, ratio * 1.7), "budget": None}[choice]
+    R = data.draw(st.sampled_from([1, 5, 64, 256]))
+    _compress_compare(geom, B, ctx, ratio, budget, sel, starts, toks, C, R)
+
+
+def test_compress_plan_fp64_pitfall_and_size_query():
+    geom = Geometry(1, 1, 1, 64, 16, 1)
+    budget = np.array([[0.07]])
+    res = tg.tg_reserve(geom, [100], None, budget, [[0]], np.arange(10, dtype=np.int32), 10)
+    assert res["kv_len"][0, 0, 0] == 8
+    got = [tg.tg_compress_plan(geom, 1, 0, 50, [c0], [50], None, budget, res["kv_len"], res["pt_offsets"], [[0]],
+                               [[0]], 3) for c0 in (0, 50)]
+    assert [(int(p["write_begin"][0, 0]), int(p["keep_count"][0, 0])) for p in got] == [(0, 4), (4, 4)]
+    assert [p["num_items"] for p in got] == [2, 2]
+
+
+def test_compress_plan_errors():
+    geom = Geometry(1, 2, 2, 64, 16, 2)
+    budget = np.array([[0.5, 0.25]])
+    res = tg.tg_reserve(geom, [64], None, budget, [[0, 0]], np.arange(10, dtype=np.int32), 10)
+    kv, off = res["kv_len"], res["pt_offsets"]
+    ok = dict(chunk_start=[0], chunk_tokens=[32], ratio=None, budget=budget, kv_len=kv, pt_offsets=off,
+              group_of=[[0, 0]], slot_of=[[0, 1]])
+
+    def call(C=32, R=64, layer=0, **kw):
+        a = dict(ok, **kw)
+        return tg.tg_compress_plan(geom, 1, layer, C, a["chunk_start"], a["chunk_tokens"], a["ratio"], a["budget"],
+                                   a["kv_len"], a["pt_offsets"], a["group_of"], a["slot_of"], R)
+
+    assert call()["num_items"] == 2
+    for kw in (dict(C=0), dict(C=tg.TG_COMPRESS_MAX_CHUNK + 1), dict(R=0), dict(R=tg.TG_COMPRESS_MAX_ROWS + 1),
+               dict(layer=1), dict(chunk_start=[-1]), dict(chunk_tokens=[33]), dict(chunk_tokens=[-1]),
+               dict(chunk_start=[2**31 - 10]), dict(ratio=np.array([[[0.5, 1.5]]])), dict(ratio=np.array([[[0.0, 0.5]]])),
+               dict(slot_of=[[0, 2]]), dict(group_of=[[0, 1]]), dict(kv_len=kv + 100), dict(kv_len=kv * 0 - 1)):
+        with pytest.raises(tg.TangramError) as e:
+            call(**kw)
+        assert e.value.code == tg.TG_ERR_INVALID_ARG, kw
+
+
+def test_compress_launch_validation_on_host():
+    """tg_compress rejects unsupported shapes before touching the device; an empty plan enqueues nothing."""
+    g = Geometry(1, 2, 2, 128, 16, 2)
+
+    def args(**kw):
+        a = dict(geom=g, batch=1, chunk_len=8, dtype=tg.TG_BF16, num_items=0)
+        a.update(kw)
+        return tg.tg_compress_args(tg._geom(a["geom"]), a["batch"], a["chunk_len"], a["dtype"], None, None, None,
+                                   None, None, None, a["num_items"], None)
+
+    tg.tg_compress(args())                       # nothing to do: OK without a device
+    for kw, code in ((dict(dtype=7), tg.TG_ERR_UNSUPPORTED), (dict(geom=Geometry(1, 2, 2, 96, 16, 2)),
+                                                              tg.TG_ERR_UNSUPPORTED),
+                     (dict(chunk_len=0), tg.TG_ERR_INVALID_ARG), (dict(chunk_len=tg.TG_COMPRESS_MAX_CHUNK + 1),
+                                                                  tg.TG_ERR_INVALID_ARG),
+                     (dict(batch=0), tg.TG_ERR_INVALID_ARG), (dict(num_items=-1), tg.TG_ERR_INVALID_ARG),
+                     (dict(num_items=3), tg.TG_ERR_INVALID_ARG), (dict(geom=Geometry(1, 3, 3, 128, 16, 2)),
+                                                                 tg.TG_ERR_INVALID_ARG)):
+        with pytest.raises(tg.TangramError) as e:
+            tg.tg_compress(args(**kw))
+        assert e.value.code == code, kw

@@ -29,7 +29,12 @@ Section 3.2):
 
 "Top x % of heads" selects max(1, round(x*L*H)) (layer, head) pairs with a
 seeded permutation of all L*H pairs.  Random streams: SeedSequence(1000+cfg)
-spawned into (ratios, contexts, free list, q, k, v, kv-pool).
+spawned into (ratios, contexts, free list, q, k, v, kv-pool, importance scores).
+
+Compression of a prefill chunk (config 5's chunk, or scaled-down cases) takes
+importance scores per (request, KV head, chunk token) standing in for a
+compression method's scoring function: N(0,1) fp32, optionally with a share of
+exact ties, signed zeros, infinities and NaNs.
 """
 from __future__ import annotations
 
@@ -40,8 +45,8 @@ from typing import Optional
 import numpy as np
 
 # Stream indices of SeedSequence(1000 + cfg).spawn(N_STREAMS).
-S_RATIO, S_CTX, S_FREE, S_Q, S_K, S_V, S_POOL = range(7)
-N_STREAMS = 7
+S_RATIO, S_CTX, S_FREE, S_Q, S_K, S_V, S_POOL, S_SCORE = range(8)
+N_STREAMS = 8
 
 
 @dataclasses.dataclass(frozen=True)
@@ -210,6 +215,21 @@ def host_prefill_inputs(wl: Workload):
     k = host_normal(wl, S_K, (wl.batch, C, g.num_kv_heads, g.head_dim), wl.kv_scale)
     v = host_normal(wl, S_V, (wl.batch, C, g.num_kv_heads, g.head_dim), wl.kv_scale)
     return q, k, v
+
+
+def host_scores(wl: Workload, shape, special: bool = False) -> np.ndarray:
+    """Importance scores [B][H][C] float32: N(0,1); with `special`, 30 % are rounded to
+    multiples of 0.5 (exact ties), and some are -0.0, +-inf or NaN."""
+    rng = wl.rng(S_SCORE)
+    s = rng.standard_normal(size=shape, dtype=np.float32)
+    if special:
+        u = rng.random(size=shape)
+        s = np.where(u < 0.3, np.round(s * 2) / 2, s).astype(np.float32)
+        s[(u >= 0.30) & (u < 0.33)] = -0.0
+        s[(u >= 0.33) & (u < 0.35)] = np.nan
+        s[(u >= 0.35) & (u < 0.36)] = np.inf
+        s[(u >= 0.36) & (u < 0.37)] = -np.inf
+    return s
 
 
 # -------------------------------------------------------------- device tensors
