@@ -14,6 +14,8 @@ of a step (sum over requests, layers and KV heads of kv_len * 2 * d * 2 bytes)
 divided by the measured step time.
 
     python bench.py [--steps K] [--warmup W] [--config 3] [--mode aot|naive|uniform]
+    python bench.py --config 5             # chunked prefill + compression of the chunk
+    python bench.py --compress-chunk C     # chunk compression alone, chunk of C tokens
     python bench.py --copy-probe BYTES     # plain copy kernel, for counter calibration
 """
 from __future__ import annotations
@@ -117,43 +119,210 @@ def cpu_baseline(session, seconds, threads=1, seed=7):
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
-def bench_prefill(args):
-    """Ragged chunked prefill (bf16 MFMA), one layer: TFLOP/s of the algorithmic work."""
+def prefill_cpu_baseline(ps, seconds, seed=9):
+    """The fp64 oracle's chunked-prefill attention on sampled (request, query head) rows of the same
+    workload, timed on the host with one BLAS thread; TFLOP/s of those rows' algorithmic flops."""
+    sys.path.insert(0, ROOT)
+    from threadpoolctl import threadpool_limits
+
+    import oracle
     import torch
-    from paper_2606_06302_amd.runner import PrefillSession
+    wl, t, g = ps.wl, ps.t, ps.wl.geom
+    C, P, G, L = wl.chunk_len, g.page_size, g.num_groups, g.num_layers
+    rng = np.random.default_rng(seed)
+    f = lambda x: x.float().cpu().numpy().astype(np.float64)
+    q, k, v = f(ps.q), f(ps.k_new), f(ps.v_new)
+    got = f(ps.out)
+    spent, flops, rows, max_abs = 0.0, 0, 0, 0.0
+    with threadpool_limits(limits=1):
+        while spent < seconds and rows < 4096:
+            b, qh = int(rng.integers(0, wl.batch)), int(rng.integers(0, g.num_q_heads))
+            h = qh // g.gqa
+            n = int(ps.hist[b, ps.layer, h])
+            base = int(t.pt_offsets[(b * L + ps.layer) * G + t.group_of[ps.layer, h]])
+            idx = t.pt_pages[base: base + (n + P - 1) // P].astype(np.int64)
+            sub = ps.pool[torch.from_numpy(idx).cuda()].float().cpu().numpy().astype(np.float64)
+            remap = np.full(t.pool_pages, -1, dtype=np.int64)
+            remap[idx] = np.arange(len(idx))
+            t0 = time.perf_counter()
+            ref = oracle.prefill_attention(q, k, v, sub, ps.layer, geom=g, kv_len=ps.hist, offsets=t.pt_offsets,
+                                           pages=remap[t.pt_pages], group_of=t.group_of, slot_of=t.slot_of,
+                                           rows=[(b, qh)])
+            spent += time.perf_counter() - t0
+            flops += 4 * g.head_dim * (n * C + C * (C + 1) // 2)
+            rows += 1
+            max_abs = max(max_abs, float(np.abs(got[b, :, qh] - ref[b, :, qh]).max()))
+    return {"value": flops / spent / 1e12, "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
+            "sample": f"{rows} (request, query head) rows of the same chunk, all {C} query positions each, "
+                      f"{flops / 1e9:.2f} GFLOP, {spent:.1f} s, BLAS limited to 1 thread",
+            "gpu_vs_oracle_max_abs": max_abs}
+
+
+def bench_prefill(args):
+    """One layer of chunked prefill with its compression (bf16): ragged chunked-prefill attention
+    (MFMA) over the compressed history, then the chunk's K/V compressed into the reserved pages."""
+    import dataclasses
+
+    import torch
+    from paper_2606_06302_amd import tangram as tg
+    from paper_2606_06302_amd.runner import CompressSession, PrefillSession, Tables
     from workloads import config
-    wl = config(5)
+    wl5 = config(5)
+    C, B = wl5.chunk_len, wl5.batch
+    g = wl5.geom
+    # the reservation covers each request's whole context: history plus this chunk
+    wl = dataclasses.replace(wl5, ctx_len=wl5.ctx_len + C)
     log(f"[bench] workload {wl.name}: tables, pool, chunk inputs")
-    s = PrefillSession(wl)
+    tables = Tables(wl)
+    starts, toks = wl5.ctx_len, np.full(B, C, dtype=np.int32)
+    plan = tg.tg_compress_plan(g, B, 0, C, starts, toks, wl.ratio, wl.budget, tables.kv_len, tables.pt_offsets,
+                               tables.group_of, tables.slot_of, 32)
+    hist = plan["write_begin"].reshape(B, 1, g.num_kv_heads)     # ceil(r * 16384): Eq. 4 on the history
+    s = PrefillSession(wl, tables=tables, hist_len=hist)
+    cs = CompressSession(wl, tables, s.pool, starts, toks, k_new=s.k_new, v_new=s.v_new)
     torch.cuda.synchronize()
     flops = s.flops()
+    comp_bytes = cs.traffic_bytes()
     stream = torch.cuda.Stream()
     with torch.cuda.stream(stream):
         for _ in range(args.warmup):
             s.run(stream)
+            cs.run(stream)
         stream.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for _ in range(args.steps):
             s.run(stream)
+            cs.run(stream)
         e1.record(stream)
         torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / args.steps
+        ms = e0.elapsed_time(e1) / args.steps
+        # per-kernel times, events on the launch stream
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        pre_ms = comp_ms = 0.0
+        nrep = max(1, min(args.steps, 10))
+        for _ in range(nrep):
+            ev[0].record(stream)
+            s.run(stream)
+            ev[1].record(stream)
+            cs.run(stream)
+            ev[2].record(stream)
+            torch.cuda.synchronize()
+            pre_ms += ev[0].elapsed_time(ev[1]) / nrep
+            comp_ms += ev[1].elapsed_time(ev[2]) / nrep
     tflops = flops / (ms * 1e-3) / 1e12
-    g = wl.geom
+    pre_tflops = flops / (pre_ms * 1e-3) / 1e12
+    comp_gbs = comp_bytes / (comp_ms * 1e-3) / 1e9
     res = {
         "metric": "ragged chunked prefill attn: TFLOP/s (bf16 MFMA)", "value": round(tflops, 2), "unit": "TFLOP/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": wl.name, "batch": wl.batch, "chunk_len": wl.chunk_len, "q_heads": g.num_q_heads,
-                   "kv_heads": g.num_kv_heads, "head_dim": g.head_dim, "history_ctx": int(wl.ctx_len[0]),
-                   "flops_per_step": flops, "parallelism": "single GPU"},
-        "roofline": {"bound": "mfma", "achieved": round(tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": "tg_prefill_kernel",
-                     "avg_launch_us": round(ms * 1e3, 2), "algorithmic_flops_per_launch": flops},
+        "config": {"workload": wl.name, "batch": B, "chunk_len": C, "q_heads": g.num_q_heads,
+                   "kv_heads": g.num_kv_heads, "head_dim": g.head_dim, "history_ctx": int(wl5.ctx_len[0]),
+                   "flops_per_step": flops, "step": "chunk attention over the compressed history, then the "
+                   "chunk's K/V compressed into the reserved pages", "parallelism": "single GPU"},
+        "roofline": {"bound": "mfma", "achieved": round(pre_tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(pre_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "kernel": "tg_prefill_kernel", "avg_launch_us": round(pre_ms * 1e3, 2),
+                     "algorithmic_flops_per_launch": flops},
+        "compress": {"bound": "hbm", "achieved": round(comp_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(comp_gbs / HBM_PEAK_GBS, 4), "kernel": "tg_compress (select + copy launches)",
+                     "avg_launch_us": round(comp_ms * 1e3, 2), "algorithmic_bytes_per_launch": comp_bytes,
+                     "kept_rows": int(cs.plan["keep_count"].sum()), "work_items": cs.plan["num_items"]},
         "cpu_baseline": None,
     }
+    if not args.no_cpu_baseline:
+        log(f"[bench] cpu_baseline: oracle on sampled rows (~{args.cpu_seconds:.0f} s)")
+        res["cpu_baseline"] = prefill_cpu_baseline(s, args.cpu_seconds)
     print(json.dumps(res), flush=True)
+
+
+def bench_compress(args):
+    """Compression of one prefill chunk into the ragged cache, alone: config 5's requests and ratios
+    with a chunk of args.compress_chunk tokens after the 16384-token history."""
+    import dataclasses
+
+    import torch
+    from paper_2606_06302_amd.runner import CompressSession, Tables
+    from workloads import S_POOL, config, device_normal_, page_elems
+    wl5 = config(5)
+    C, B = args.compress_chunk, wl5.batch
+    wl = dataclasses.replace(wl5, ctx_len=wl5.ctx_len + C, chunk_len=C)
+    g = wl.geom
+    log(f"[bench] chunk compression, {B} requests x {g.num_kv_heads} KV heads, chunk {C}")
+    t = Tables(wl)
+    pool = torch.empty(t.pool_pages * page_elems(g), dtype=torch.bfloat16, device="cuda")
+    device_normal_(pool, wl, S_POOL, wl.kv_scale)
+    pool = pool.view(t.pool_pages, 2, g.heads_per_group, g.page_size, g.head_dim)
+    cs = CompressSession(wl, t, pool, wl5.ctx_len, np.full(B, C, dtype=np.int32),
+                         rows_per_item=args.rows_per_item or 32)
+    nbytes = cs.traffic_bytes()
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            cs.run(stream)
+        stream.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            cs.run(stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / args.steps * 1e3
+    gbs = nbytes / (us * 1e-6) / 1e9
+    res = {"metric": "chunk compression into ragged pages: GB/s of algorithmic HBM traffic", "value": round(gbs, 2),
+           "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "ms_per_step": round(us / 1e3, 5), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": f"chunk-compression-bf16-c{C}", "batch": B, "chunk_len": C,
+                      "kv_heads": g.num_kv_heads, "head_dim": g.head_dim, "history_ctx": int(wl5.ctx_len[0]),
+                      "rows_per_item": args.rows_per_item or 32, "kept_rows": int(cs.plan["keep_count"].sum()),
+                      "work_items": cs.plan["num_items"], "parallelism": "single GPU"},
+           "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                        "kernel": "tg_compress (select + copy launches)", "avg_launch_us": round(us, 2),
+                        "algorithmic_bytes_per_launch": nbytes},
+           "cpu_baseline": None}
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = compress_cpu_baseline(cs, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+def compress_cpu_baseline(cs, seconds, seed=10):
+    """The oracle's compress_chunk on whole sampled requests of the same chunk (host, one thread);
+    GB/s of the same algorithmic traffic."""
+    sys.path.insert(0, ROOT)
+    import oracle
+    import torch
+    wl, t, g = cs.wl, cs.t, cs.wl.geom
+    L, G, P, H = g.num_layers, g.num_groups, g.page_size, g.num_kv_heads
+    f = lambda x: x.float().cpu().numpy().astype(np.float64)
+    k, v, sc = f(cs.k_new), f(cs.v_new), cs.scores.cpu().numpy()
+    rng = np.random.default_rng(seed)
+    spent, done, reqs, ok = 0.0, 0, 0, True
+    sel = cs.wl.ratio
+    while spent < seconds and reqs < wl.batch:
+        b = int(rng.integers(0, wl.batch))
+        lo, hi = b * L * G, (b + 1) * L * G
+        idx = np.unique(t.pt_pages[t.pt_offsets[lo]: t.pt_offsets[hi]]).astype(np.int64)
+        sub = cs.pool[torch.from_numpy(idx).cuda()].float().cpu().numpy().astype(np.float64)
+        remap = np.full(t.pool_pages, -1, dtype=np.int64)
+        remap[idx] = np.arange(len(idx))
+        t0 = time.perf_counter()
+        out, kept, cur, cnt = oracle.compress_chunk(k[b:b + 1], v[b:b + 1], sc[b:b + 1], sub, 0, geom=g,
+                                                    ratio=sel[b:b + 1], capacity=t.kv_len[b:b + 1],
+                                                    chunk_start=cs.chunk_start[b:b + 1],
+                                                    chunk_tokens=cs.chunk_tokens[b:b + 1],
+                                                    offsets=t.pt_offsets[lo: hi + 1], pages=remap[t.pt_pages],
+                                                    group_of=t.group_of, slot_of=t.slot_of)
+        spent += time.perf_counter() - t0
+        ok &= bool(np.array_equal(out, sub))   # the GPU already wrote these rows: nothing may change
+        n = int(cnt.sum())
+        done += n * 2 * g.head_dim * 2 * 2 + int(cs.chunk_tokens[b]) * H * 4 + n * 8
+        reqs += 1
+    return {"value": done / spent / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{reqs} whole requests (all {H} KV heads) of the same chunk, {spent:.1f} s",
+            "gpu_matches_oracle": ok}
 
 
 def main():
@@ -171,6 +340,9 @@ def main():
                     help="rebuild the fill plans with per-XCD bin weights measured in one stamped step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0)
+    ap.add_argument("--compress-chunk", type=int, default=0,
+                    help="time only the compression of a chunk of this many tokens (config 5's requests)")
+    ap.add_argument("--rows-per-item", type=int, default=0)
     ap.add_argument("--free-order", default="shuffled", choices=["shuffled", "sequential"],
                     help="order of the free page list (shuffled = seeded permutation of the pool)")
     args = ap.parse_args()
@@ -188,6 +360,8 @@ def main():
     from paper_2606_06302_amd.runner import DecodeSession
     from workloads import config
 
+    if args.compress_chunk:
+        return bench_compress(args)
     if args.config == 5:
         return bench_prefill(args)
     mode = {"aot": tg.TG_PLAN_AOT, "fill": tg.TG_PLAN_AOT_FILL, "naive": tg.TG_PLAN_NAIVE,

@@ -381,26 +381,31 @@ int32_t tg_compress_plan(const tg_geometry* geom, int32_t batch, int32_t layer, 
                          tg_compress_item* items, int32_t item_capacity, int32_t* keep_count,
                          int32_t* write_begin, int32_t* num_items);
 
-/* 5b. tg_compress (device): runs a tg_compress_plan.  Workgroup i takes item
- * i: it selects Top(count) of its unit's scores, ranks the kept entries in
- * token order and copies the K and V rows of ranks [rank_begin, rank_end)
- * into their pages.
+/* 5b. tg_compress (device): runs a tg_compress_plan as two launches on
+ * hip_stream.  The select launch takes one workgroup per (b, h): it ranks the
+ * chunk's entries and writes the indices of Top(keep_count[b][h]) to kept[].
+ * The copy launch takes one workgroup per item: it copies the K and V rows of
+ * ranks [rank_begin, rank_end) into their pages.
  * DEVICE pointers:
  *   k_new, v_new [B][C][H][d] dtype: the chunk's K and V before compression
  *   scores  [B][H][C] float32: importance of every chunk entry (from the
  *           compression method's scoring function); entries at or past
- *           chunk_tokens[b] are not read
+ *           chunk_tokens[b] are ignored (the buffer still holds all C)
  *   kv_pool [pool_pages][2][H_p][P][d] dtype: only the kept rows are written
- *   pt_pages device copy of tg_reserve's output; items [num_items]
- *   kept    [B][H][C] int32, or NULL: kept[(b*H + h)*C + j] = chunk index of
- *           the j-th kept entry (ascending), for j < count; the rest untouched
- * Items must come from tg_compress_plan for the same geometry, layer,
- * chunk_len, chunk_tokens and tables: the kernel trusts them.  The items of one
- * call write disjoint rows; calls that write the same pages must be ordered.
- * Supported: dtype TG_F32 or TG_BF16, head_dim 64 or 128, chunk_len in
- * 1..TG_COMPRESS_MAX_CHUNK (else TG_ERR_UNSUPPORTED / TG_ERR_INVALID_ARG).
- * No workspace.  num_items == 0 enqueues nothing.  Returns TG_ERR_HIP if the
- * launch fails. */
+ *   pt_pages device copy of tg_reserve's output
+ *   items [num_items], keep_count [B][H] int32, chunk_tokens [B] int32: device
+ *           copies of tg_compress_plan's items and counts and of its input
+ *   kept    [B][H][C] int32 (required; it also carries the selection to the
+ *           copy launch): kept[(b*H + h)*C + j] = chunk index of the j-th kept
+ *           entry in ascending order, for j < keep_count[b][h]; other entries
+ *           are left untouched
+ * Items and counts must come from one tg_compress_plan call for the same
+ * geometry, layer, chunk_len, chunk_tokens and tables; the kernels trust them.
+ * Items write disjoint rows; calls that write the same pages or the same kept
+ * buffer must be ordered.  Supported: dtype TG_F32 or TG_BF16, head_dim 64 or
+ * 128, chunk_len in 1..TG_COMPRESS_MAX_CHUNK (else TG_ERR_UNSUPPORTED /
+ * TG_ERR_INVALID_ARG).  No workspace.  num_items == 0 enqueues nothing.
+ * Returns TG_ERR_HIP if a launch fails. */
 typedef struct {
   tg_geometry geom;
   int32_t batch;
@@ -413,6 +418,8 @@ typedef struct {
   const int32_t* pt_pages;
   const tg_compress_item* items;
   int32_t num_items;
+  const int32_t* chunk_tokens;
+  const int32_t* keep_count;
   int32_t* kept;
 } tg_compress_args;
 

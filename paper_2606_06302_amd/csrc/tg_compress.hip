@@ -2,20 +2,20 @@
 // per-head Top(count) selection over a chunk's importance scores and the
 // scatter of the kept K and V rows into the head's reserved ragged pages.
 //
-// One workgroup of 256 threads per work item (at most TG_COMPRESS_MAX_ROWS
-// kept entries of one (request, KV head) unit):
-//   1. the unit's n scores become order-preserving 32-bit keys in LDS
-//      (larger score = larger key; -0 maps to +0; NaN maps to 0, below all);
-//   2. a most-significant-digit-first radix select (four 8-bit passes over
-//      LDS histograms) finds the count-th largest key T and how many entries
-//      equal to T are kept (the lowest-index ones);
-//   3. two workgroup prefix sums over contiguous token runs give every kept
-//      entry its rank in token order;
-//   4. the item's ranks are copied row by row with 16-byte loads from the
-//      chunk's K and V and 16-byte stores into page pt_pages[pt_base + pos/P],
-//      row pos % P, pos = cursor + rank.
-// Every item of a unit repeats the selection (it reads n scores, a few KB
-// from L2); the K/V rows are the HBM traffic, each read and written once.
+// Two launches on the caller's stream:
+//   select - one workgroup of 256 threads per (request, KV head) unit:
+//     1. the unit's n scores become order-preserving 32-bit keys in LDS
+//        (larger score = larger key; -0 maps to +0; NaN maps to 0, below all);
+//     2. a most-significant-digit-first radix select (four 8-bit passes, one
+//        LDS histogram per wave) finds the count-th largest key T and how many
+//        entries equal to T are kept (the lowest-index ones);
+//     3. each wave walks its quarter of the tokens 64 at a time; ballots of
+//        the "kept" and "equal to T" predicates and lane-prefix bit counts
+//        give every kept entry its rank in token order, written to kept[].
+//   copy - one workgroup per work item (at most TG_COMPRESS_MAX_ROWS ranks of
+//     one unit): 16-byte loads of the K and V rows named by kept[] from the
+//     chunk, 16-byte stores to page pt_pages[pt_base + pos / P], row pos % P,
+//     pos = cursor + rank.  These rows are the HBM traffic.
 #include <hip/hip_runtime.h>
 
 #include "tg_internal.h"
@@ -26,17 +26,26 @@ constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kBins = 256;           // one radix digit of 8 bits; == kThreads
 constexpr int kUnroll = 4;           // rows in flight per thread in the copy
+constexpr int kBatch = 8;            // score loads / LDS key reads in flight per thread
+constexpr int kGroups = 4;           // 64-token groups per batch of the ranking walk
 
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
-struct CompressParams {
+struct SelectParams {
+  const uint32_t* scores;            // float32 bit patterns [B][H][C]
+  const int32_t* chunk_tokens;       // [B]
+  const int32_t* keep_count;         // [B][H]
+  int32_t* kept;                     // [B][H][C]
+  int32_t H, C;
+};
+
+struct CopyParams {
   const u4* k_new;
   const u4* v_new;
-  const uint32_t* scores;            // float32 bit patterns
   u4* pool;
   const int32_t* pt_pages;
   const tg_compress_item* items;
-  int32_t* kept;
+  const int32_t* kept;
   int32_t H, C, Hp, P;
   int32_t row_u4;                    // 16-byte vectors per K or V row: 8, 16 or 32
 };
@@ -49,76 +58,128 @@ __device__ __forceinline__ uint32_t order_key(uint32_t u) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-__device__ __forceinline__ int wave_inclusive_sum(int x, int lane) {
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
+// Scalar (constant-cache) loads of values that are uniform across a workgroup.
+#define TG_CONST __attribute__((address_space(4)))
+
+__device__ __forceinline__ tg_compress_item load_item(const TG_CONST tg_compress_item* src) {
+  tg_compress_item r;
+  r.pt_base = src->pt_base;
+  r.b = src->b;
+  r.kv_head = src->kv_head;
+  r.slot = src->slot;
+  r.n_valid = src->n_valid;
+  r.cursor = src->cursor;
+  r.count = src->count;
+  r.rank_begin = src->rank_begin;
+  r.rank_end = src->rank_end;
+  return r;
+}
+
+// DPP lane movement with zero fill (row_mask selects the 16-lane rows updated).
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ int dpp_add_src(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, ROW_MASK, 0xF, true);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave: shifts by 1, 2, 4 and 8
+// inside each 16-lane row, then row 0's total into row 1 and row 2's into row
+// 3 (row_bcast:15), then rows 0-1's total into rows 2 and 3 (row_bcast:31).
+__device__ __forceinline__ int wave_inclusive_sum(int x) {
+  x += dpp_add_src<0x111, 0xF>(x);
+  x += dpp_add_src<0x112, 0xF>(x);
+  x += dpp_add_src<0x114, 0xF>(x);
+  x += dpp_add_src<0x118, 0xF>(x);
+  x += dpp_add_src<0x142, 0xA>(x);
+  x += dpp_add_src<0x143, 0xC>(x);
   return x;
 }
 
-// Exclusive prefix sum over the workgroup in thread order; *total gets the sum.
-__device__ __forceinline__ int block_exclusive_sum(int v, int* wave_tot, int* total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int inc = wave_inclusive_sum(v, lane);
-  if (lane == 63) wave_tot[wave] = inc;
-  __syncthreads();
-  int before = 0, all = 0;
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
-    const int t = wave_tot[w];
-    before += (w < wave) ? t : 0;
-    all += t;
-  }
-  __syncthreads();  // wave_tot is reused by the next sum
-  *total = all;
-  return before + inc - v;
+// Number of set bits of `mask` at lanes below the calling lane.
+__device__ __forceinline__ int lanes_below(uint64_t mask) {
+  return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-__global__ __launch_bounds__(kThreads) void tg_compress_kernel(CompressParams p) {
+__global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectParams p) {
   extern __shared__ uint32_t keys[];             // [n] keys of the unit's scores
-  __shared__ uint32_t hist[kBins];
-  __shared__ int32_t rows_src[TG_COMPRESS_MAX_ROWS];  // chunk index of each rank of the item
-  __shared__ int32_t wave_tot[kWaves];
+  __shared__ uint32_t hist[kWaves][kBins];
+  __shared__ int32_t wave_cnt[2][kWaves];
   __shared__ uint32_t pick[2];
 
-  const tg_compress_item it = p.items[blockIdx.x];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // the plan guarantees these bounds; clamping keeps a malformed item inside its buffers
-  const int n = min(max(it.n_valid, 0), p.C);
-  const int count = min(max(it.count, 0), n);
-  const int r0 = max(it.rank_begin, 0);
-  const int r1 = min(min(it.rank_end, count), r0 + TG_COMPRESS_MAX_ROWS);
-  const int64_t unit = (int64_t)it.b * p.H + it.kv_head;
-
+  const int64_t unit = blockIdx.x;
+  const int b = (int)(unit / p.H);
+  // the first batch of scores is requested before the counts arrive: it
+  // covers chunk entries that exist whatever chunk_tokens says
   const uint32_t* sc = p.scores + unit * p.C;
-  for (int t = tid; t < n; t += kThreads) keys[t] = order_key(sc[t]);
+  uint32_t v[kBatch];
+#pragma unroll
+  for (int u = 0; u < kBatch; ++u) {
+    const int t = tid + u * kThreads;
+    v[u] = t < p.C ? sc[t] : 0u;
+  }
+  const int n = min(max(((const TG_CONST int32_t*)p.chunk_tokens)[b], 0), p.C);
+  const int count = min(max(((const TG_CONST int32_t*)p.keep_count)[unit], 0), n);
+  if (count == 0) return;                        // the whole workgroup leaves together
+  const bool keep_all = count >= n;
+
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) hist[w][tid] = 0;
+  __syncthreads();
+  // keys into LDS, kBatch loads in flight per thread; the histogram of the
+  // top digit is taken on the way
+  for (int t0 = tid; t0 < n; t0 += kBatch * kThreads) {
+    if (t0 != tid) {
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const int t = t0 + u * kThreads;
+        v[u] = t < n ? sc[t] : 0u;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int t = t0 + u * kThreads;
+      if (t < n) {
+        const uint32_t key = order_key(v[u]);
+        keys[t] = key;
+        if (!keep_all) atomicAdd(&hist[wave][key >> 24], 1u);
+      }
+    }
+  }
   __syncthreads();
 
-  // 1-2. radix select: thr = the count-th largest key, need = entries equal to
-  // thr that are kept
-  const bool keep_all = count >= n;
+  // radix select: thr = the count-th largest key, need = entries equal to thr
+  // that are kept
   uint32_t thr = 0, mask = 0;
   int need = count;
   if (!keep_all) {
     for (int shift = 24; shift >= 0; shift -= 8) {
-      hist[tid] = 0;
-      __syncthreads();
-      for (int t = tid; t < n; t += kThreads) {
-        const uint32_t key = keys[t];
-        if ((key & mask) == thr) atomicAdd(&hist[(key >> shift) & 0xffu], 1u);
+      if (shift < 24) {
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) hist[w][tid] = 0;
+        __syncthreads();
+        for (int t0 = tid; t0 < n; t0 += kBatch * kThreads) {
+          uint32_t kk[kBatch];
+#pragma unroll
+          for (int u = 0; u < kBatch; ++u) {
+            const int t = t0 + u * kThreads;
+            kk[u] = t < n ? keys[t] : ~thr;    // ~thr never matches thr under mask (mask != 0 here)
+          }
+#pragma unroll
+          for (int u = 0; u < kBatch; ++u)
+            if ((kk[u] & mask) == thr) atomicAdd(&hist[wave][(kk[u] >> shift) & 0xffu], 1u);
+        }
+        __syncthreads();
       }
-      __syncthreads();
       if (wave == 0) {
         // lane i owns digits 255-4i .. 252-4i, in descending order
         int c[4], s = 0;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          c[j] = (int)hist[255 - 4 * lane - j];
+          const int d = 255 - 4 * lane - j;
+          c[j] = (int)(hist[0][d] + hist[1][d] + hist[2][d] + hist[3][d]);
           s += c[j];
         }
-        int run = wave_inclusive_sum(s, lane) - s;  // matching keys with a larger digit
+        int run = wave_inclusive_sum(s) - s;  // matching keys with a larger digit
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           if (run < need && run + c[j] >= need) {
@@ -135,44 +196,66 @@ __global__ __launch_bounds__(kThreads) void tg_compress_kernel(CompressParams p)
     }
   }
 
-  // 3. ranks in token order over contiguous runs of m tokens per thread
-  const int m = (n + kThreads - 1) / kThreads;
-  const int a = min(n, tid * m), e = min(n, a + m);
-  int gt = 0, eq = 0;
-  if (keep_all) {
-    gt = e - a;
-  } else {
-    for (int t = a; t < e; ++t) {
-      const uint32_t key = keys[t];
-      gt += key > thr;
-      eq += key == thr;
+  // ranks in token order: wave w owns tokens [w*span, (w+1)*span), walked in
+  // groups of 64, kGroups groups per batch of LDS reads
+  const int span = ((n + kThreads - 1) / kThreads) * 64;
+  const int t_begin = wave * span, t_end = min(n, t_begin + span);
+  int gt_w = 0, eq_w = 0;
+  for (int base = t_begin; base < t_end; base += 64 * kGroups) {
+    uint32_t kk[kGroups];
+#pragma unroll
+    for (int u = 0; u < kGroups; ++u) {
+      const int t = base + 64 * u + lane;
+      kk[u] = t < t_end ? keys[t] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kGroups; ++u) {
+      const bool valid = base + 64 * u + lane < t_end;
+      gt_w += __popcll(__ballot(valid && (keep_all || kk[u] > thr)));
+      eq_w += __popcll(__ballot(valid && !keep_all && kk[u] == thr));
     }
   }
-  int eq_total = 0, kept_total = 0;
-  const int eq_before = block_exclusive_sum(eq, wave_tot, &eq_total);
-  const int take_eq = min(eq, max(0, need - eq_before));
-  int rank = block_exclusive_sum(gt + take_eq, wave_tot, &kept_total);
-  int32_t* kept_out = p.kept ? p.kept + unit * p.C : nullptr;
-  int eq_seen = eq_before;
-  for (int t = a; t < e; ++t) {
-    bool keep = true;
-    if (!keep_all) {
-      const uint32_t key = keys[t];
-      keep = key > thr;
-      if (key == thr) keep = eq_seen++ < need;
-    }
-    if (keep) {
-      if (rank >= r0 && rank < r1) {
-        rows_src[rank - r0] = t;
-        if (kept_out) kept_out[rank] = t;
-      }
-      ++rank;
-    }
+  if (lane == 0) {
+    wave_cnt[0][wave] = gt_w;
+    wave_cnt[1][wave] = eq_w;
   }
   __syncthreads();
+  int gt_before = 0, eq_before = 0;
+  for (int w = 0; w < wave; ++w) {
+    gt_before += wave_cnt[0][w];
+    eq_before += wave_cnt[1][w];
+  }
+  int run_eq = eq_before, run_kept = gt_before + min(eq_before, need);
+  int32_t* out = p.kept + unit * p.C;
+  for (int base = t_begin; base < t_end; base += 64 * kGroups) {
+    uint32_t kk[kGroups];
+#pragma unroll
+    for (int u = 0; u < kGroups; ++u) {
+      const int t = base + 64 * u + lane;
+      kk[u] = t < t_end ? keys[t] : 0u;
+    }
+#pragma unroll
+    for (int u = 0; u < kGroups; ++u) {
+      const int t = base + 64 * u + lane;
+      const bool valid = t < t_end;
+      const bool eq = valid && !keep_all && kk[u] == thr;
+      const uint64_t eq_mask = __ballot(eq);
+      const bool keep = valid && (keep_all || kk[u] > thr || (eq && run_eq + lanes_below(eq_mask) < need));
+      const uint64_t keep_mask = __ballot(keep);
+      if (keep) out[run_kept + lanes_below(keep_mask)] = t;
+      run_eq += __popcll(eq_mask);
+      run_kept += __popcll(keep_mask);
+    }
+  }
+}
 
-  // 4. copy the item's kept rows into the pages
+__global__ __launch_bounds__(kThreads) void tg_compress_copy_kernel(CopyParams p) {
+  const tg_compress_item it = load_item((const TG_CONST tg_compress_item*)p.items + blockIdx.x);
+  const int tid = threadIdx.x;
+  const int r0 = max(it.rank_begin, 0);
+  const int r1 = min(min(it.rank_end, min(it.count, p.C)), r0 + TG_COMPRESS_MAX_ROWS);
   const int rows = r1 - r0;
+  const int32_t* src_tok = p.kept + ((int64_t)it.b * p.H + it.kv_head) * p.C + r0;
   const int lpr = p.row_u4;
   const int rpp = kThreads / lpr;               // rows per pass of the workgroup
   const int sub = tid % lpr, rsel = tid / lpr;
@@ -186,7 +269,8 @@ __global__ __launch_bounds__(kThreads) void tg_compress_kernel(CompressParams p)
     for (int u = 0; u < kUnroll; ++u) {
       const int j = base + u * rpp + rsel;
       if (j < rows) {
-        const int64_t src = src0 + rows_src[j] * tok_stride;
+        const int t = min(max(src_tok[j], 0), p.C - 1);   // in range by construction; clamped for safety
+        const int64_t src = src0 + t * tok_stride;
         kk[u] = p.k_new[src];
         vv[u] = p.v_new[src];
         const int pos = it.cursor + r0 + j;
@@ -219,31 +303,41 @@ extern "C" int32_t tg_compress(const tg_compress_args* a, void* hip_stream) {
     return tg::fail(TG_ERR_INVALID_ARG, "chunk_len %d outside [1, %d]", a->chunk_len, (int)TG_COMPRESS_MAX_CHUNK);
   if (a->num_items < 0) return tg::fail(TG_ERR_INVALID_ARG, "num_items < 0");
   if (a->num_items == 0) return TG_OK;
-  if (!a->k_new || !a->v_new || !a->scores || !a->kv_pool || !a->pt_pages || !a->items)
+  if (!a->k_new || !a->v_new || !a->scores || !a->kv_pool || !a->pt_pages || !a->items || !a->chunk_tokens ||
+      !a->keep_count || !a->kept)
     return tg::fail(TG_ERR_INVALID_ARG, "NULL device pointer");
-  CompressParams p;
-  p.k_new = static_cast<const u4*>(a->k_new);
-  p.v_new = static_cast<const u4*>(a->v_new);
-  p.scores = reinterpret_cast<const uint32_t*>(a->scores);
-  p.pool = static_cast<u4*>(a->kv_pool);
-  p.pt_pages = a->pt_pages;
-  p.items = a->items;
-  p.kept = a->kept;
-  p.H = g.num_kv_heads;
-  p.C = a->chunk_len;
-  p.Hp = g.heads_per_group;
-  p.P = g.page_size;
-  p.row_u4 = g.head_dim * (a->dtype == TG_F32 ? 4 : 2) / 16;
-  const size_t lds = (size_t)a->chunk_len * sizeof(uint32_t);
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
+  SelectParams s;
+  s.scores = reinterpret_cast<const uint32_t*>(a->scores);
+  s.chunk_tokens = a->chunk_tokens;
+  s.keep_count = a->keep_count;
+  s.kept = a->kept;
+  s.H = g.num_kv_heads;
+  s.C = a->chunk_len;
+  const size_t lds = (size_t)a->chunk_len * sizeof(uint32_t);
   static_assert(kBins == kThreads, "one histogram bin per thread");
   if (lds > 32768) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(tg_compress_kernel),
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(tg_compress_select_kernel),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress LDS attribute: %s", hipGetErrorString(e));
   }
-  hipLaunchKernelGGL(tg_compress_kernel, dim3(a->num_items), dim3(kThreads), lds, stream, p);
+  hipLaunchKernelGGL(tg_compress_select_kernel, dim3(a->batch * g.num_kv_heads), dim3(kThreads), lds, stream, s);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress launch failed: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress select launch failed: %s", hipGetErrorString(e));
+  CopyParams c;
+  c.k_new = static_cast<const u4*>(a->k_new);
+  c.v_new = static_cast<const u4*>(a->v_new);
+  c.pool = static_cast<u4*>(a->kv_pool);
+  c.pt_pages = a->pt_pages;
+  c.items = a->items;
+  c.kept = a->kept;
+  c.H = g.num_kv_heads;
+  c.C = a->chunk_len;
+  c.Hp = g.heads_per_group;
+  c.P = g.page_size;
+  c.row_u4 = g.head_dim * (a->dtype == TG_F32 ? 4 : 2) / 16;
+  hipLaunchKernelGGL(tg_compress_copy_kernel, dim3(a->num_items), dim3(kThreads), 0, stream, c);
+  e = hipGetLastError();
+  if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress copy launch failed: %s", hipGetErrorString(e));
   return TG_OK;
 }

@@ -192,12 +192,16 @@ REALTIME_HZ = 100e6
 class PrefillSession:
     """Pool, chunk inputs and output of one chunked-prefill workload (one layer)."""
 
-    def __init__(self, wl, tables: Tables = None, layer=0, fill="device", pool=None, device="cuda", schedule=True):
+    def __init__(self, wl, tables: Tables = None, layer=0, fill="device", pool=None, device="cuda", schedule=True,
+                 hist_len=None):
         from workloads import S_K, S_POOL, S_Q, S_V, device_normal_, host_pool, host_prefill_inputs, page_elems
         g = wl.geom
         assert wl.chunk_len >= 1, "prefill workloads need a chunk length"
         self.wl, self.layer, self.device = wl, layer, device
         self.t = tables if tables is not None else Tables(wl, device=device)
+        # retained history rows per (b, l, h): the reserved lengths, or fewer when the
+        # tables also reserve room for entries of this and later chunks
+        self.hist = self.t.kv_len if hist_len is None else np.ascontiguousarray(hist_len, dtype=np.int32)
         self.dtype = TORCH_DTYPE[wl.dtype]
         B, C = wl.batch, wl.chunk_len
         if pool is not None:
@@ -220,11 +224,11 @@ class PrefillSession:
             device_normal_(self.v_new, wl, S_V, wl.kv_scale)
         self.out = torch.zeros(B, C, g.num_q_heads, g.head_dim, dtype=self.dtype, device=device)
         self.d_offsets = to_device(self.t.pt_offsets, device)
-        self.d_kv_len = to_device(self.t.kv_len, device)
+        self.d_kv_len = to_device(self.hist, device)
         self.d_group_of = to_device(self.t.group_of, device)
         self.d_slot_of = to_device(self.t.slot_of, device)
         # ahead-of-time workgroup schedule from the retained lengths (host integer work)
-        self.order = tg.tg_prefill_schedule(g, B, C, layer, self.t.kv_len) if schedule else None
+        self.order = tg.tg_prefill_schedule(g, B, C, layer, self.hist) if schedule else None
         self.d_order = to_device(self.order, device) if schedule else None
         self.args = tg.make_prefill_args(g, B, C, layer, TG_DTYPE[wl.dtype], self.q, self.k_new, self.v_new,
                                          self.pool, self.t.d_pt_pages, self.d_offsets, self.d_kv_len,
@@ -237,7 +241,7 @@ class PrefillSession:
         """Algorithmic flops: 4*d per (query row, visible key) for q.k and p.v."""
         g, wl = self.wl.geom, self.wl
         C = wl.chunk_len
-        hist = self.t.kv_len[:, self.layer, :].astype(np.int64)          # [B][H]
+        hist = self.hist[:, self.layer, :].astype(np.int64)              # [B][H]
         per_row_keys = hist.sum() * C + wl.batch * g.num_kv_heads * C * (C + 1) // 2
         return int(4 * g.head_dim * g.gqa * per_row_keys)
 
@@ -253,7 +257,7 @@ class CompressSession:
     step); run() enqueues tg_compress."""
 
     def __init__(self, wl, tables: Tables, pool, chunk_start, chunk_tokens, layer=0, sel_ratio="reserved",
-                 rows_per_item=64, k_new=None, v_new=None, scores=None, want_kept=True, device="cuda"):
+                 rows_per_item=32, k_new=None, v_new=None, scores=None, device="cuda"):
         from workloads import S_K, S_V, device_normal_, host_scores
         g = wl.geom
         B, C, H = wl.batch, wl.chunk_len, g.num_kv_heads
@@ -277,19 +281,22 @@ class CompressSession:
             device_normal_(v_new, wl, S_V, wl.kv_scale)
         self.k_new, self.v_new = k_new, v_new
         self.scores = scores if scores is not None else torch.from_numpy(host_scores(wl, (B, H, C))).to(device)
-        self.kept = torch.full((B, H, C), -1, dtype=torch.int32, device=device) if want_kept else None
+        self.d_chunk_tokens = to_device(self.chunk_tokens, device)
+        self.d_keep_count = to_device(self.plan["keep_count"], device)
+        self.kept = torch.full((B, H, C), -1, dtype=torch.int32, device=device)
         self.args = tg.make_compress_args(g, B, C, TG_DTYPE[wl.dtype], self.k_new, self.v_new, self.scores,
                                           self.pool, tables.d_pt_pages, self.d_items, self.plan["num_items"],
-                                          self.kept)
+                                          self.d_chunk_tokens, self.d_keep_count, self.kept)
 
     def run(self, stream=None):
         tg.tg_compress(self.args, stream)
 
     def traffic_bytes(self) -> int:
         """Algorithmic HBM bytes of one call: the kept K and V rows read from the chunk and
-        written to the pages, the valid scores read once, and the kept indices written."""
+        written to the pages, the valid scores read once, and the kept indices written once
+        (and read back by the copy)."""
         g = self.wl.geom
         esz = 4 if self.wl.dtype == "f32" else 2
         kept = int(self.plan["keep_count"].sum())
         scores = int(self.chunk_tokens.astype(np.int64).sum()) * g.num_kv_heads * 4
-        return kept * 2 * g.head_dim * esz * 2 + scores + (kept * 4 if self.kept is not None else 0)
+        return kept * 2 * g.head_dim * esz * 2 + scores + kept * 4 * 2

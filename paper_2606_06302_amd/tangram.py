@@ -66,7 +66,8 @@ class tg_prefill_args(C.Structure):
 class tg_compress_args(C.Structure):
     _fields_ = [("geom", tg_geometry), ("batch", C.c_int32), ("chunk_len", C.c_int32), ("dtype", C.c_int32),
                 ("k_new", C.c_void_p), ("v_new", C.c_void_p), ("scores", C.c_void_p), ("kv_pool", C.c_void_p),
-                ("pt_pages", C.c_void_p), ("items", C.c_void_p), ("num_items", C.c_int32), ("kept", C.c_void_p)]
+                ("pt_pages", C.c_void_p), ("items", C.c_void_p), ("num_items", C.c_int32),
+                ("chunk_tokens", C.c_void_p), ("keep_count", C.c_void_p), ("kept", C.c_void_p)]
 
 
 # One HIP runtime per process: torch ships its own libamdhip64 (soname
@@ -315,11 +316,11 @@ def tg_compress_plan(geom, batch, layer, chunk_len, chunk_start, chunk_tokens, r
 
 
 def make_compress_args(geom, batch, chunk_len, dtype, k_new, v_new, scores, kv_pool, pt_pages, items, num_items,
-                       kept=None) -> tg_compress_args:
+                       chunk_tokens, keep_count, kept) -> tg_compress_args:
     """Packs a tg_compress_args from device tensors (kept alive by the caller)."""
     return tg_compress_args(_geom(geom), int(batch), int(chunk_len), int(dtype), _dptr(k_new), _dptr(v_new),
                             _dptr(scores), _dptr(kv_pool), _dptr(pt_pages), _dptr(items), int(num_items),
-                            _dptr(kept))
+                            _dptr(chunk_tokens), _dptr(keep_count), _dptr(kept))
 
 
 def tg_compress(args: tg_compress_args, stream=None):

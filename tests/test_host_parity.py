@@ -342,7 +342,7 @@ def test_compress_launch_validation_on_host():
         a = dict(geom=g, batch=1, chunk_len=8, dtype=tg.TG_BF16, num_items=0)
         a.update(kw)
         return tg.tg_compress_args(tg._geom(a["geom"]), a["batch"], a["chunk_len"], a["dtype"], None, None, None,
-                                   None, None, None, a["num_items"], None)
+                                   None, None, None, a["num_items"], None, None, None)
 
     tg.tg_compress(args())                       # nothing to do: OK without a device
     for kw, code in ((dict(dtype=7), tg.TG_ERR_UNSUPPORTED), (dict(geom=Geometry(1, 2, 2, 96, 16, 2)),
