@@ -31,6 +31,10 @@ in the paper's order and notation:
                         workgroups: the same idea as the decode partition
                         (cost known from the retained lengths before the step,
                         Section 4.3), longest-processing-time onto the XCDs.
+  * memory_footprint  - KV slots each paging scheme allocates for the same
+                        retained lengths: the uncompressed cache, a monolithic
+                        page table spanning all L x H heads (PagedAttention,
+                        Section 4.2.1), and ragged per-group tables.
   * chunk_keep_range  - compression fused into chunked prefill (Section 4.1):
   * top_entries         Eq. 4's per-head Top(ceil(B*N), s) applied to each
   * compress_chunk      chunk as its KV is produced, the kept entries appended
@@ -176,6 +180,41 @@ def reserve(ratio, ctx_len, group_of, num_groups, page_size, free_pages):
         raise OutOfPages(f"need {k} pages, {len(free_pages)} free")
     pages = free_pages[:k].astype(np.int64).copy()
     return dict(kv_len=kv_len, group_len=gl, offsets=offsets, pages=pages, pages_needed=k)
+
+
+def memory_footprint(ratio, ctx_len, group_of, num_groups, heads_per_group, page_size):
+    """KV slots (one slot = the K and V rows of one token of one head) that each
+    paging scheme allocates for the retained lengths of Eq. 4 (Section 4.2.1).
+
+    full:       every request's whole context, paged:  ceil(N/P)*P slots per head.
+    retained:   sum of kv_len, what compression keeps.
+    monolithic: PagedAttention's single page table spans all L x H heads, so a
+                request gets ceil(max_{l,h} kv_len / P) pages for every head.
+    ragged:     one table per (request, layer, group) sized by the group's
+                longest member: ceil(GL/P) pages of H_p heads.
+    Returns a dict of int slot counts plus ragged_pages and page_tables.
+    """
+    ratio = np.asarray(ratio, dtype=np.float64)
+    Bn, L, H = ratio.shape
+    P = page_size
+    kv_len = retained_lengths(ratio, ctx_len)
+    gl = group_lengths(kv_len, group_of, num_groups)
+    full = retained = mono = ragged = pages = 0
+    for b in range(Bn):
+        n = int(ctx_len[b])
+        full += -(-n // P) * P * L * H
+        longest = 0
+        for l in range(L):
+            for h in range(H):
+                retained += int(kv_len[b, l, h])
+                longest = max(longest, int(kv_len[b, l, h]))
+            for g in range(num_groups):
+                npg = -(-int(gl[b, l, g]) // P)
+                pages += npg
+                ragged += npg * P * heads_per_group
+        mono += -(-longest // P) * P * L * H
+    return dict(full_slots=full, retained_slots=retained, monolithic_slots=mono, ragged_slots=ragged,
+                ragged_pages=pages, page_tables=Bn * L * num_groups)
 
 
 def token_location(b, l, h, i, *, num_layers, num_groups, page_size, offsets, pages, group_of, slot_of):

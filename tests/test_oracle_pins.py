@@ -783,3 +783,98 @@ def test_compress_plan_pieces_cover_every_kept_entry():
                 spans = seen.get((b, h), [])
                 assert sum(r1 - r0 for r0, r1 in spans) == cnt[b, h]
                 assert all(s[1] == t[0] for s, t in zip(spans, spans[1:]))
+
+
+# ------------------------------------------------ memory footprint of paging
+
+FOOT = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "footprint_hand.json")))
+
+
+def _footprint(budget, ctx, Hp, grouping, ratio=None, P=16):
+    budget = np.asarray(budget, dtype=np.float64)
+    L, H = budget.shape
+    _, gof, _ = oracle.cluster_heads(budget, Hp, grouping)
+    r = np.broadcast_to(budget, (len(ctx), L, H)) if ratio is None else ratio
+    return oracle.memory_footprint(r, ctx, gof, H // Hp, Hp, P)
+
+
+def test_footprint_hand():
+    for key, slots in FOOT["ragged_slots"].items():
+        hp, grouping = key.split("-")
+        f = _footprint(FOOT["budget"], FOOT["ctx_len"], int(hp),
+                       oracle.GROUP_CLUSTERED if grouping == "clustered" else oracle.GROUP_ADJACENT)
+        assert f["ragged_slots"] == slots and f["ragged_pages"] == FOOT["ragged_pages"][key], key
+        assert f["full_slots"] == FOOT["full_slots"] and f["retained_slots"] == FOOT["retained_slots"]
+        assert f["monolithic_slots"] == FOOT["monolithic_slots"]
+
+
+def test_footprint_hand_partial_pages():
+    c = FOOT["case2"]
+    for key, slots in c["ragged_slots"].items():
+        hp, grouping = key.split("-")
+        f = _footprint(FOOT["budget"], c["ctx_len"], int(hp),
+                       oracle.GROUP_CLUSTERED if grouping == "clustered" else oracle.GROUP_ADJACENT)
+        assert f["ragged_slots"] == slots, key
+        assert (f["full_slots"], f["retained_slots"], f["monolithic_slots"]) == \
+            (c["full_slots"], c["retained_slots"], c["monolithic_slots"])
+
+
+def test_footprint_config1_hand():
+    # config 1: lengths {512, 256, 128, 64}; groups {3,2} (GL 128, 8 pages) and {1,0} (GL 512, 32 pages)
+    f = _footprint(GOLD["budget"], GOLD["ctx_len"], 2, oracle.GROUP_CLUSTERED, P=16)
+    assert f["ragged_pages"] == 80 and f["ragged_slots"] == 80 * 16 * 2
+    assert f["full_slots"] == f["monolithic_slots"] == 2 * 32 * 16 * 4     # head 0 keeps everything
+    assert f["retained_slots"] == 2 * (512 + 256 + 128 + 64)
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_clustering_minimises_ragged_slots_bruteforce(seed):
+    """Without per-request jitter, retained lengths follow the budget order, so the clustered groups take
+    the smallest possible group maxima: no equal-size partition of the heads allocates fewer slots."""
+    rng = np.random.default_rng(seed)
+    for _ in range(6):
+        H = int(rng.choice([4, 6, 8]))
+        Hp = int(rng.choice([h for h in (2, 3, 4) if H % h == 0]))
+        budget = rng.choice([0.02, 0.1, 0.3, 0.6, 1.0], size=(1, H))
+        ctx = rng.integers(1, 3000, size=3)
+        P = int(rng.choice([1, 16]))
+        best = _footprint(budget, ctx, Hp, oracle.GROUP_CLUSTERED, P=P)["ragged_slots"]
+        ratio = np.broadcast_to(budget, (3, 1, H))
+        kv = oracle.retained_lengths(ratio, ctx)
+
+        def partitions(items):
+            if not items:
+                yield []
+                return
+            first, rest = items[0], items[1:]
+            for others in itertools.combinations(rest, Hp - 1):
+                left = [x for x in rest if x not in others]
+                for tail in partitions(left):
+                    yield [(first,) + others] + tail
+
+        for part in partitions(list(range(H))):
+            slots = 0
+            for b in range(3):
+                for grp in part:
+                    slots += -(-max(int(kv[b, 0, h]) for h in grp) // P) * P * Hp
+            assert best <= slots
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_footprint_orderings(seed):
+    """retained <= ragged(H_p = 1) <= ragged(any H_p, any grouping) <= monolithic <= full."""
+    rng = np.random.default_rng(40 + seed)
+    L, H, B = 3, 8, 4
+    budget = rng.uniform(0.02, 1.0, size=(L, H))
+    ratio = np.clip(budget[None] + rng.uniform(-0.03, 0.03, size=(B, L, H)), 0.02, 1.0)
+    ctx = rng.integers(100, 5000, size=B)
+    one = _footprint(budget, ctx, 1, oracle.GROUP_CLUSTERED, ratio=ratio)
+    for Hp in (1, 2, 4, 8):
+        for grouping in (oracle.GROUP_CLUSTERED, oracle.GROUP_ADJACENT):
+            f = _footprint(budget, ctx, Hp, grouping, ratio=ratio)
+            assert f["retained_slots"] <= one["ragged_slots"] <= f["ragged_slots"] <= f["monolithic_slots"] \
+                <= f["full_slots"]
+            assert f["page_tables"] == B * L * H // Hp
+            res = oracle.reserve(ratio, ctx, oracle.cluster_heads(budget, Hp, grouping)[1], H // Hp, 16,
+                                 np.arange(10**6))
+            assert res["pages_needed"] == f["ragged_pages"]
