@@ -16,6 +16,7 @@ divided by the measured step time.
     python bench.py [--steps K] [--warmup W] [--config 3] [--mode aot|naive|uniform]
     python bench.py --config 5             # chunked prefill + compression of the chunk
     python bench.py --compress-chunk C     # chunk compression alone, chunk of C tokens
+    python bench.py --memory               # host only: memory reclaimed per paging scheme
     python bench.py --copy-probe BYTES     # plain copy kernel, for counter calibration
 """
 from __future__ import annotations
@@ -325,6 +326,46 @@ def compress_cpu_baseline(cs, seconds, seed=10):
             "gpu_matches_oracle": ok}
 
 
+def bench_memory(args):
+    """Memory reclaimed by ragged paging (host, integer; no GPU): KV slots each scheme allocates for the
+    same retained lengths, per heads-per-group and grouping, and the block-table build time."""
+    sys.path.insert(0, ROOT)
+    from paper_2606_06302_amd import tangram as tg
+    from workloads import Geometry, config
+    rows = []
+    for cfg in (2, 3, 4, 5):
+        wl = config(cfg)
+        g = wl.geom
+        esz = 4 if wl.dtype == "f32" else 2
+        for Hp in (1, 2, 4, 8):
+            geom = Geometry(g.num_layers, g.num_kv_heads, g.num_q_heads, g.head_dim, g.page_size, Hp)
+            for grouping, gname in ((tg.TG_GROUP_CLUSTERED, "clustered"), (tg.TG_GROUP_ADJACENT, "adjacent")):
+                _, gof, _ = tg.tg_cluster_heads(geom, wl.budget, grouping)
+                f = tg.tg_memory_footprint(geom, wl.ctx_len, wl.ratio, None, gof)
+                need = f["ragged_pages"]
+                free = np.arange(need, dtype=np.int32)
+                reps = 3
+                tg.tg_reserve(geom, wl.ctx_len, wl.ratio, None, gof, free, need)   # untimed: first touch
+                t0 = time.perf_counter()
+                for _ in range(reps):
+                    tg.tg_reserve(geom, wl.ctx_len, wl.ratio, None, gof, free, need)
+                us = (time.perf_counter() - t0) / reps * 1e6
+                full = f["full_slots"]
+                rows.append({"workload": wl.name, "heads_per_group": Hp, "grouping": gname,
+                             "full_GB": round(full * 2 * g.head_dim * esz / 1e9, 3),
+                             "retained_frac": round(f["retained_slots"] / full, 4),
+                             "monolithic_frac": round(f["monolithic_slots"] / full, 4),
+                             "ragged_frac": round(f["ragged_slots"] / full, 4),
+                             "reclaimed_vs_full": round(1 - f["ragged_slots"] / full, 4),
+                             "reclaimed_monolithic": round(1 - f["monolithic_slots"] / full, 4),
+                             "page_tables": f["page_tables"], "pages": need,
+                             "reserve_us": round(us, 1)})
+                log(f"[bench] {wl.name} H_p={Hp} {gname}: ragged {f['ragged_slots'] / full:.3f} of full, "
+                    f"monolithic {f['monolithic_slots'] / full:.3f}, reserve {us:.0f} us")
+    print(json.dumps({"metric": "KV slots allocated per paging scheme (fraction of the full cache)",
+                      "data": "synthetic", "rows": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -343,6 +384,8 @@ def main():
     ap.add_argument("--compress-chunk", type=int, default=0,
                     help="time only the compression of a chunk of this many tokens (config 5's requests)")
     ap.add_argument("--rows-per-item", type=int, default=0)
+    ap.add_argument("--memory", action="store_true",
+                    help="host-only: memory reclaimed by ragged paging for each heads-per-group and grouping")
     ap.add_argument("--free-order", default="shuffled", choices=["shuffled", "sequential"],
                     help="order of the free page list (shuffled = seeded permutation of the pool)")
     args = ap.parse_args()
@@ -353,6 +396,8 @@ def main():
     if args.copy_probe:
         copy_probe(args.copy_probe)
         return
+    if args.memory:
+        return bench_memory(args)
 
     import torch
     sys.path.insert(0, ROOT)

@@ -425,6 +425,35 @@ typedef struct {
 
 int32_t tg_compress(const tg_compress_args* args, void* hip_stream);
 
+/* ------------------------------------ 6. memory footprint of the paging
+ * Section 4.2.1 (a page table spans the heads of one group; PagedAttention is
+ * the single group of all L x H heads) and Section 4.2.2.  For the retained
+ * lengths kv_len[b][l][h] = ceil(r[b][l][h] * ctx_len[b]) (Eq. 4; r = ratio,
+ * or budget broadcast when ratio is NULL), counts KV slots - one slot holds
+ * the K and V rows of one token of one head, 2 * d * sizeof(dtype) bytes -
+ * that each paging scheme allocates:
+ *   full_slots       = sum_b ceil(N_b/P)*P * L*H      (uncompressed, paged)
+ *   retained_slots   = sum_{b,l,h} kv_len              (what compression keeps)
+ *   monolithic_slots = sum_b ceil(max_{l,h} kv_len/P)*P * L*H
+ *                      (one page table spanning every head of the request)
+ *   ragged_slots     = sum_{b,l,g} ceil(GL/P)*P * H_p  (one table per group,
+ *                      GL = max over the group's heads, groups from group_of)
+ *   ragged_pages     = sum_{b,l,g} ceil(GL/P)          (== tg_reserve's count)
+ *   page_tables      = B * L * G
+ * All host memory; ctx_len [B] >= 1, ratio [B][L][H] or budget [L][H] in
+ * (0, 1], group_of [L][H].  Errors: TG_ERR_INVALID_ARG (nothing written). */
+typedef struct {
+  int64_t full_slots;
+  int64_t retained_slots;
+  int64_t monolithic_slots;
+  int64_t ragged_slots;
+  int64_t ragged_pages;
+  int64_t page_tables;
+} tg_footprint;
+
+int32_t tg_memory_footprint(const tg_geometry* geom, int32_t batch, const int32_t* ctx_len, const double* ratio,
+                            const double* budget, const int32_t* group_of, tg_footprint* out);
+
 #ifdef __cplusplus
 }
 #endif

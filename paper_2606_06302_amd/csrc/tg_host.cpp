@@ -548,3 +548,51 @@ extern "C" int32_t tg_compress_plan(const tg_geometry* geom, int32_t batch, int3
     }
   return TG_OK;
 }
+
+// KV slots allocated by each paging scheme for the same retained lengths
+// (Section 4.2.1: a table spans one group; PagedAttention spans all L x H heads).
+extern "C" int32_t tg_memory_footprint(const tg_geometry* geom, int32_t batch, const int32_t* ctx_len,
+                                       const double* ratio, const double* budget, const int32_t* group_of,
+                                       tg_footprint* out) {
+  if (int32_t rc = tg::check_geometry(geom)) return rc;
+  if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
+  if (!ctx_len || !group_of || !out) return fail(TG_ERR_INVALID_ARG, "NULL array");
+  if (!ratio && !budget) return fail(TG_ERR_INVALID_ARG, "ratio and budget are both NULL");
+  const int L = geom->num_layers, H = geom->num_kv_heads, Hp = geom->heads_per_group, G = H / Hp;
+  const int64_t P = geom->page_size;
+  for (int64_t i = 0; i < (int64_t)L * H; ++i)
+    if (group_of[i] < 0 || group_of[i] >= G) return fail(TG_ERR_INVALID_ARG, "group_of[%lld] out of range", (long long)i);
+  for (int b = 0; b < batch; ++b) {
+    if (ctx_len[b] < 1) return fail(TG_ERR_INVALID_ARG, "ctx_len[%d] < 1", b);
+    for (int64_t i = 0; i < (int64_t)L * H; ++i) {
+      const double r = ratio ? ratio[(int64_t)b * L * H + i] : budget[i];
+      if (!tg::ratio_ok(r)) return fail(TG_ERR_INVALID_ARG, "ratio of request %d entry %lld outside (0,1]", b, (long long)i);
+    }
+  }
+  tg_footprint f = {0, 0, 0, 0, 0, (int64_t)batch * L * G};
+  std::vector<int64_t> gl(G);
+  for (int b = 0; b < batch; ++b) {
+    const double n = (double)ctx_len[b];
+    f.full_slots += ceil_div(ctx_len[b], P) * P * L * H;
+    int64_t longest = 0;
+    for (int l = 0; l < L; ++l) {
+      std::fill(gl.begin(), gl.end(), 0);
+      for (int h = 0; h < H; ++h) {
+        const int64_t i = (int64_t)l * H + h;
+        const double r = ratio ? ratio[(int64_t)b * L * H + i] : budget[i];
+        const int64_t len = (int64_t)std::ceil(r * n);
+        f.retained_slots += len;
+        longest = std::max(longest, len);
+        gl[group_of[i]] = std::max(gl[group_of[i]], len);
+      }
+      for (int g = 0; g < G; ++g) {
+        const int64_t pages = ceil_div(gl[g], P);
+        f.ragged_pages += pages;
+        f.ragged_slots += pages * P * Hp;
+      }
+    }
+    f.monolithic_slots += ceil_div(longest, P) * P * L * H;
+  }
+  *out = f;
+  return TG_OK;
+}

@@ -70,6 +70,11 @@ class tg_compress_args(C.Structure):
                 ("chunk_tokens", C.c_void_p), ("keep_count", C.c_void_p), ("kept", C.c_void_p)]
 
 
+class tg_footprint(C.Structure):
+    _fields_ = [("full_slots", C.c_int64), ("retained_slots", C.c_int64), ("monolithic_slots", C.c_int64),
+                ("ragged_slots", C.c_int64), ("ragged_pages", C.c_int64), ("page_tables", C.c_int64)]
+
+
 # One HIP runtime per process: torch ships its own libamdhip64 (soname
 # libamdhip64.so.7) and loads it by file name, so if libtangram.so were loaded
 # first (binding the system copy) torch would bring in a second runtime and
@@ -106,6 +111,7 @@ _SIGS = {
     "tg_prefill_schedule": (_i32, [_G, _i32, _i32, _i32, _P, _i32, _P, _i32, _P]),
     "tg_compress_plan": (_i32, [_G, _i32, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _i32, _P, _i32, _P, _P, _P]),
     "tg_compress": (_i32, [C.POINTER(tg_compress_args), _P]),
+    "tg_memory_footprint": (_i32, [_G, _i32, _P, _P, _P, _P, C.POINTER(tg_footprint)]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -325,3 +331,15 @@ def make_compress_args(geom, batch, chunk_len, dtype, k_new, v_new, scores, kv_p
 
 def tg_compress(args: tg_compress_args, stream=None):
     _check(_lib.tg_compress(C.byref(args), _stream(stream)), "tg_compress")
+
+
+def tg_memory_footprint(geom, ctx_len, ratio, budget, group_of) -> dict:
+    """-> dict of slot counts (full, retained, monolithic, ragged), ragged_pages and page_tables."""
+    g = _geom(geom)
+    ctx = _host(ctx_len, np.int32)
+    r = None if ratio is None else _host(ratio, np.float64)
+    bud = None if budget is None else _host(budget, np.float64)
+    out = tg_footprint()
+    _check(_lib.tg_memory_footprint(C.byref(g), len(ctx), _ptr(ctx), _ptr(r), _ptr(bud),
+                                    _ptr(_host(group_of, np.int32)), C.byref(out)), "tg_memory_footprint")
+    return {f[0]: int(getattr(out, f[0])) for f in tg_footprint._fields_}

@@ -355,3 +355,36 @@ def test_compress_launch_validation_on_host():
         with pytest.raises(tg.TangramError) as e:
             tg.tg_compress(args(**kw))
         assert e.value.code == code, kw
+
+
+# ------------------------------------------------ memory footprint of paging
+
+@pytest.mark.parametrize("cfg", [1, 2, 4, 5])
+def test_footprint_configs_bit_exact(cfg):
+    wl = config(cfg)
+    g = wl.geom
+    for Hp in (1, 2, 4, 8):
+        if g.num_kv_heads % Hp:
+            continue
+        geom = Geometry(g.num_layers, g.num_kv_heads, g.num_q_heads, g.head_dim, g.page_size, Hp)
+        for grouping in (tg.TG_GROUP_CLUSTERED, tg.TG_GROUP_ADJACENT):
+            _, gof, _ = tg.tg_cluster_heads(geom, wl.budget, grouping)
+            got = tg.tg_memory_footprint(geom, wl.ctx_len, wl.ratio, None, gof)
+            ref = oracle.memory_footprint(wl.ratio, wl.ctx_len, gof, g.num_kv_heads // Hp, Hp, g.page_size)
+            assert got == ref, (cfg, Hp, grouping)
+            need = tg.tg_reserve(geom, wl.ctx_len, wl.ratio, None, gof, np.zeros(0, np.int32), 0,
+                                 size_query=True)["pages_needed"]
+            assert got["ragged_pages"] == need
+
+
+def test_footprint_budget_broadcast_and_errors():
+    geom = Geometry(1, 4, 4, 64, 16, 2)
+    budget = np.array([[0.1, 1.0, 0.1, 1.0]])
+    _, gof, _ = tg.tg_cluster_heads(geom, budget)
+    f = tg.tg_memory_footprint(geom, [160], None, budget, gof)
+    assert (f["ragged_slots"], f["monolithic_slots"], f["full_slots"], f["retained_slots"]) == (352, 640, 640, 352)
+    for args in (([0], None, budget, gof), ([160], None, np.array([[0.1, 1.5, 0.1, 1.0]]), gof),
+                 ([160], None, budget, np.array([[0, 1, 2, 0]])), ([160], None, None, gof)):
+        with pytest.raises(tg.TangramError) as e:
+            tg.tg_memory_footprint(geom, *args)
+        assert e.value.code == tg.TG_ERR_INVALID_ARG
