@@ -19,6 +19,10 @@ in the paper's order and notation:
   * partition_plan    - Algorithm 1's proportional rule applied to one batch's
                         integer retained lengths, then greedy longest-first
                         assignment of the split chunks to persistent workgroups.
+  * append_token      - a decode step's new token appended to every head
+                        (after its retained entries, within the reservation);
+                        partition plans can leave each unit's last chunk open
+                        so that one plan serves every later step.
   * decode_attention  - softmax attention of one query token per request over
                         each KV head's retained rows (Eq. 1 with standard
                         scaled-dot-product attention; grouped-query heads share
@@ -156,13 +160,16 @@ def group_lengths(kv_len, group_of, num_groups):
     return gl
 
 
-def reserve(ratio, ctx_len, group_of, num_groups, page_size, free_pages):
+def reserve(ratio, ctx_len, group_of, num_groups, page_size, free_pages, headroom=None):
     """Precise Page Allocation (Section 4.1) into per-group page tables.
 
     Pages are taken from the front of free_pages in (b, l, g, page) order.  The
     per-(b, l, g) tables are concatenated (the Vectorized Block Table, Section
     4.2.3): table (b, l, g) is pages[offsets[(b*L+l)*G+g] : offsets[...+1]].
-    Raises OutOfPages, consuming nothing, when the list is too short.
+    headroom[b] (optional) reserves room for that many decode tokens more in
+    every table of request b: each decode step appends one token to every head,
+    so every group's length grows by one per step.  Raises OutOfPages,
+    consuming nothing, when the list is too short.
     """
     kv_len = retained_lengths(ratio, ctx_len)
     gl = group_lengths(kv_len, group_of, num_groups)
@@ -170,10 +177,13 @@ def reserve(ratio, ctx_len, group_of, num_groups, page_size, free_pages):
     offsets = np.zeros(Bn * L * G + 1, dtype=np.int64)
     k = 0
     for b in range(Bn):
+        extra = 0 if headroom is None else int(headroom[b])
+        if extra < 0:
+            raise OracleError("negative headroom")
         for l in range(L):
             for g in range(G):
                 offsets[(b * L + l) * G + g] = k
-                k += -(-int(gl[b, l, g]) // page_size)     # ceil(GL / P) pages
+                k += -(-(int(gl[b, l, g]) + extra) // page_size)     # ceil((GL + headroom) / P) pages
     offsets[-1] = k
     free_pages = np.asarray(free_pages)
     if k > len(free_pages):
@@ -267,7 +277,29 @@ def split_map(budget, perm, heads_per_group, n_cta):
 # ------------------------------------------- executed partition for one layer
 
 def partition_plan(kv_len, offsets, group_of, slot_of, layer, *, num_layers, num_groups, page_size,
-                   mode=MODE_AOT, n_bins=1, split_target=1, bin_weights=None):
+                   mode=MODE_AOT, n_bins=1, split_target=1, bin_weights=None, open_end=False):
+    """Balanced split-KV partition of one layer, optionally reusable while the
+    lengths grow: with open_end, the chunk that ends a unit (t1 == its length)
+    gets t1 = -(capacity of the unit's page table in tokens), meaning "up to
+    the head's current length", so the plan stays valid as decode steps append
+    tokens (the ahead-of-time plan of Section 4.3 needs no per-step planning).
+    """
+    plan = _partition_plan(kv_len, offsets, group_of, slot_of, layer, num_layers=num_layers,
+                           num_groups=num_groups, page_size=page_size, mode=mode, n_bins=n_bins,
+                           split_target=split_target, bin_weights=bin_weights)
+    if open_end:
+        items = []
+        for (pt_base, b, h, slot, t0, t1, out_idx) in plan["items"]:
+            if t1 == int(kv_len[b, layer, h]):
+                t = (b * num_layers + layer) * num_groups + int(group_of[layer, h])
+                t1 = -int(offsets[t + 1] - offsets[t]) * page_size
+            items.append((pt_base, b, h, slot, t0, t1, out_idx))
+        plan["items"] = items
+    return plan
+
+
+def _partition_plan(kv_len, offsets, group_of, slot_of, layer, *, num_layers, num_groups, page_size,
+                    mode=MODE_AOT, n_bins=1, split_target=1, bin_weights=None):
     """Balanced split-KV partition of one layer of one batch.
 
     Work unit u = (request b, KV head h), in order b, h.  In AOT mode unit u is
@@ -448,16 +480,21 @@ def merge_partials(outs, lses):
     return (w[..., None] * outs).sum(axis=0), tot
 
 
-def decode_by_plan(q, pool, layer, plan, *, geom, batch, offsets, pages, group_of, slot_of, sm_scale=0.0):
+def decode_by_plan(q, pool, layer, plan, *, geom, batch, offsets, pages, group_of, slot_of, sm_scale=0.0,
+                   live_len=None):
     """Evaluate decode attention chunk by chunk along a partition plan, then merge.
 
     Split-KV with a log-sum-exp merge is algebraically exact, so this must
-    reproduce decode_attention up to fp64 rounding.
+    reproduce decode_attention up to fp64 rounding.  An open-ended chunk
+    (t1 < 0) runs to the head's current length live_len[b, layer, h], kept
+    within [t0 + 1, -t1].
     """
     d, gqa = geom.head_dim, geom.gqa
     scale = sm_scale if sm_scale != 0.0 else 1.0 / math.sqrt(d)
     parts = {}
     for (pt_base, b, h, slot, t0, t1, out_idx) in plan["items"]:
+        if t1 < 0:
+            t1 = min(max(int(live_len[b, layer, h]), t0 + 1), -t1)
         K, V = gather_head(pool, b, layer, h, t0, t1, geom=geom, offsets=offsets, pages=pages,
                            group_of=group_of, slot_of=slot_of)
         qs = slice(h * gqa, (h + 1) * gqa)
@@ -469,6 +506,35 @@ def decode_by_plan(q, pool, layer, plan, *, geom, batch, offsets, pages, group_o
         qs = slice(h * gqa, (h + 1) * gqa)
         O[b, qs], lse[b, qs] = merge_partials([x[1] for x in lst], [x[2] for x in lst])
     return O, lse
+
+
+def append_token(k_tok, v_tok, pool, layer, *, geom, live_len, offsets, pages, group_of, slot_of):
+    """One decode step's new token, appended to every KV head of one layer.
+
+    k_tok, v_tok [B][H][d]: the token's K and V.  Head (b, layer, h) holding
+    n = live_len[b, layer, h] entries stores them as entry n (page layout of
+    Section 4.2.1) and then holds n + 1, provided its group's page table has
+    room; otherwise nothing is written for that head and it is reported.
+    Returns (new pool, new live_len, list of (b, h) that had no room).
+    """
+    out = pool.copy()
+    live = np.array(live_len, dtype=np.int64, copy=True)
+    Bn, H = k_tok.shape[0], k_tok.shape[1]
+    P, L, G = geom.page_size, geom.num_layers, geom.num_groups
+    full = []
+    for b in range(Bn):
+        for h in range(H):
+            n = int(live[b, layer, h])
+            t = (b * L + layer) * G + int(group_of[layer, h])
+            if n >= int(offsets[t + 1] - offsets[t]) * P:
+                full.append((b, h))
+                continue
+            p, s, r = token_location(b, layer, h, n, num_layers=L, num_groups=G, page_size=P, offsets=offsets,
+                                     pages=pages, group_of=group_of, slot_of=slot_of)
+            out[p, 0, s, r] = k_tok[b, h]
+            out[p, 1, s, r] = v_tok[b, h]
+            live[b, layer, h] = n + 1
+    return out, live, full
 
 
 def prefill_attention(q, k_new, v_new, pool, layer, *, geom, kv_len, offsets, pages, group_of, slot_of,

@@ -878,3 +878,97 @@ def test_footprint_orderings(seed):
             res = oracle.reserve(ratio, ctx, oracle.cluster_heads(budget, Hp, grouping)[1], H // Hp, 16,
                                  np.arange(10**6))
             assert res["pages_needed"] == f["ragged_pages"]
+
+
+# ----------------------------------------- decode steps: append and plan reuse
+
+def test_reserve_headroom_config1_hand():
+    """Config 1 with room for 20 decode tokens: group {3,2} (GL 128) takes ceil(148/16) = 10 pages and group
+    {1,0} (GL 512) ceil(532/16) = 34, so the tables start at 0, 10, 44, 54 and hold 88 pages."""
+    budget, ratio, ctx = cfg1_arrays()
+    _, gof, _ = oracle.cluster_heads(budget, 2)
+    res = oracle.reserve(ratio, ctx, gof, 2, 16, np.arange(100), headroom=[20, 20])
+    assert res["offsets"].tolist() == [0, 10, 44, 54, 88]
+    assert res["kv_len"].tolist() == GOLD["kv_len"]
+
+
+def _tiny_decode_case(seed, T, mode, Hp=2):
+    rng = np.random.default_rng(seed)
+    g = Geometry(2, 4, 8, 8, 4, Hp)
+    B = 3
+    budget = rng.uniform(0.05, 1.0, size=(2, 4))
+    ratio = np.clip(budget[None] + rng.uniform(-0.03, 0.03, size=(B, 2, 4)), 0.02, 1.0)
+    ctx = rng.integers(5, 60, size=B)
+    _, gof, sof = oracle.cluster_heads(budget, Hp)
+    res = oracle.reserve(ratio, ctx, gof, g.num_groups, g.page_size, rng.permutation(400), headroom=[T] * B)
+    pool = rng.standard_normal((400, 2, Hp, g.page_size, g.head_dim))
+    return rng, g, B, gof, sof, res, pool
+
+
+@pytest.mark.parametrize("mode", [oracle.MODE_AOT, oracle.MODE_NAIVE, oracle.MODE_UNIFORM, oracle.MODE_FILL])
+def test_open_plan_marks_exactly_the_last_chunk_of_each_unit(mode):
+    _, g, B, gof, sof, res, _ = _tiny_decode_case(3, 9, mode)
+    kw = dict(num_layers=2, num_groups=g.num_groups, page_size=g.page_size, mode=mode, n_bins=5, split_target=11)
+    closed = oracle.partition_plan(res["kv_len"], res["offsets"], gof, sof, 1, **kw)
+    opened = oracle.partition_plan(res["kv_len"], res["offsets"], gof, sof, 1, open_end=True, **kw)
+    assert len(closed["items"]) == len(opened["items"])
+    ends = {}
+    for c, o in zip(closed["items"], opened["items"]):
+        assert c[:5] == o[:5] and c[6] == o[6]
+        if o[5] < 0:
+            b, h = o[1], o[2]
+            t = (b * 2 + 1) * g.num_groups + gof[1, h]
+            assert c[5] == res["kv_len"][b, 1, h] and -o[5] == (res["offsets"][t + 1] - res["offsets"][t]) * 4
+            assert (b, h) not in ends
+            ends[(b, h)] = o
+        else:
+            assert o[5] == c[5] < res["kv_len"][o[1], 1, o[2]]
+    assert len(ends) == B * 4
+
+
+@pytest.mark.parametrize("mode", [oracle.MODE_AOT, oracle.MODE_NAIVE, oracle.MODE_UNIFORM, oracle.MODE_FILL])
+def test_plan_from_step_zero_serves_later_steps(mode):
+    """A plan built before the first decode step, with open ends, gives the plain attention over the grown
+    cache after T appended tokens (split-KV merge exact in fp64); the appended rows read back in order."""
+    T = 9
+    rng, g, B, gof, sof, res, pool = _tiny_decode_case(7, T, mode)
+    kw = dict(num_layers=2, num_groups=g.num_groups, page_size=g.page_size, mode=mode, n_bins=5, split_target=11)
+    plan = oracle.partition_plan(res["kv_len"], res["offsets"], gof, sof, 1, open_end=True, **kw)
+    live = res["kv_len"].copy()
+    toks = []
+    for _ in range(T):
+        kt, vt = rng.standard_normal((B, 4, g.head_dim)), rng.standard_normal((B, 4, g.head_dim))
+        pool, live, full = oracle.append_token(kt, vt, pool, 1, geom=g, live_len=live, offsets=res["offsets"],
+                                               pages=res["pages"], group_of=gof, slot_of=sof)
+        assert full == []
+        toks.append((kt, vt))
+    assert np.array_equal(live[:, 1], res["kv_len"][:, 1] + T) and np.array_equal(live[:, 0], res["kv_len"][:, 0])
+    for b in range(B):
+        for h in range(4):
+            n = int(res["kv_len"][b, 1, h])
+            K, V = oracle.gather_head(pool, b, 1, h, n, n + T, geom=g, offsets=res["offsets"], pages=res["pages"],
+                                      group_of=gof, slot_of=sof)
+            assert np.array_equal(K, np.stack([t[0][b, h] for t in toks]))
+            assert np.array_equal(V, np.stack([t[1][b, h] for t in toks]))
+    q = rng.standard_normal((B, 8, g.head_dim))
+    ref, ref_lse = oracle.decode_attention(q, pool, 1, geom=g, batch=B, kv_len=live, offsets=res["offsets"],
+                                           pages=res["pages"], group_of=gof, slot_of=sof)
+    got, got_lse = oracle.decode_by_plan(q, pool, 1, plan, geom=g, batch=B, offsets=res["offsets"],
+                                         pages=res["pages"], group_of=gof, slot_of=sof, live_len=live)
+    assert np.abs(got - ref).max() < 1e-12 and np.abs(got_lse - ref_lse).max() < 1e-12
+
+
+def test_append_without_room_writes_nothing():
+    """Config 1 reserved without headroom: heads 0 (512 of 512) and 2 (128 of 128) have no room for a decode
+    token, heads 1 and 3 do."""
+    budget, ratio, ctx = cfg1_arrays()
+    g = Geometry(1, 4, 8, 64, 16, 2)
+    _, gof, sof = oracle.cluster_heads(budget, 2)
+    res = oracle.reserve(ratio, ctx, gof, 2, 16, np.arange(100))
+    pool = np.zeros((100, 2, 2, 16, 64))
+    k = np.ones((2, 4, 64))
+    out, live, full = oracle.append_token(k, -k, pool, 0, geom=g, live_len=res["kv_len"], offsets=res["offsets"],
+                                          pages=res["pages"], group_of=gof, slot_of=sof)
+    assert full == [(0, 0), (0, 2), (1, 0), (1, 2)]
+    assert (live - res["kv_len"]).tolist() == [[[0, 1, 0, 1]], [[0, 1, 0, 1]]]
+    assert int((out != 0).sum()) == 2 * 2 * 2 * 64      # two heads of two requests, a K and a V row each
