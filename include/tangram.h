@@ -63,6 +63,9 @@ enum { TG_F32 = 0, TG_BF16 = 1 };
 enum { TG_GROUP_CLUSTERED = 0, TG_GROUP_ADJACENT = 1 };
 /* partition modes for tg_build_plan */
 enum { TG_PLAN_AOT = 0, TG_PLAN_NAIVE = 1, TG_PLAN_UNIFORM = 2, TG_PLAN_AOT_FILL = 3 };
+/* flag OR'ed into a tg_build_plan mode: plans that stay valid while decode
+ * steps append tokens (see tg_build_plan) */
+enum { TG_PLAN_OPEN_END = 0x100 };
 
 /* Model / cache geometry.  H = num_kv_heads (compression is per KV head,
  * Section 2.1), G = H / heads_per_group groups per layer (must divide),
@@ -100,13 +103,15 @@ int32_t tg_cluster_heads(const tg_geometry* geom, const double* budget, int32_t 
  *   kv_len[b][l][h]    = ceil(r[b][l][h] * ctx_len[b])   (one fp64 multiply,
  *                        then ceil; r = ratio, or budget broadcast if ratio is NULL)
  *   group_len[b][l][g] = max over heads h of group g of kv_len[b][l][h]
- *   table (b, l, g) holds ceil(group_len/P) pages; tables are concatenated in
+ *   table (b, l, g) holds ceil((group_len + headroom[b])/P) pages: headroom
+ *   reserves room for that many decode tokens, which every decode step appends
+ *   to every head (tg_append); tables are concatenated in
  *   (b, l, g) order into one CSR array (the Vectorized Block Table):
  *   table (b, l, g) = pt_pages[pt_offsets[(b*L+l)*G+g] .. pt_offsets[...+1]).
  *   Pages are taken from the front of free_pages in that order, so
  *   pt_pages[k] == free_pages[k] for every k < pages_needed.
  * Arguments (all host memory):
- *   batch >= 1; ctx_len [B] int32 >= 1;
+ *   batch >= 1; ctx_len [B] int32 >= 1; headroom [B] int32 >= 0, or NULL for none;
  *   ratio [B][L][H] float64 in (0, 1], or NULL to use budget for every request;
  *   budget [L][H] float64 in (0, 1] (read only when ratio is NULL);
  *   group_of [L][H] int32 from tg_cluster_heads;
@@ -124,7 +129,7 @@ int32_t tg_cluster_heads(const tg_geometry* geom, const double* budget, int32_t 
  * ids that repeat or fall outside the pool.  With pt_pages == NULL the call
  * writes kv_len, group_len, pt_offsets and pages_needed and consumes nothing.
  * On any error pt_pages is left untouched. */
-int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_len,
+int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_len, const int32_t* headroom,
                    const double* ratio, const double* budget, const int32_t* group_of,
                    const int32_t* free_pages, int64_t num_free, int64_t pool_pages,
                    int32_t* kv_len, int32_t* group_len, int64_t* pt_offsets,
@@ -173,6 +178,12 @@ int32_t tg_decode_max_ctas(const tg_geometry* geom, int32_t dtype, int32_t devic
  *   with the least token load so far (ties: lowest bin), kept in placement
  *   order within a bin.  Items are emitted bin by bin; bin k owns
  *   items[bin_offsets[k] .. bin_offsets[k+1]).
+ *   mode | TG_PLAN_OPEN_END: the same plan, except that the chunk that ends a
+ *   unit (tok_end == kv_len) gets tok_end = -(capacity of the unit's page
+ *   table in tokens).  tg_decode then runs it to the head's live length
+ *   (tg_decode_args.live_len), kept within [tok_begin + 1, capacity], so one
+ *   plan serves every decode step until the batch changes (Section 4.3: no
+ *   planning inside the step).
  * Arguments (host): kv_len [B][L][H] and pt_offsets [B*L*G+1] from tg_reserve;
  *   group_of, slot_of [L][H]; 0 <= layer < L; n_bins >= 1 (AOT, AOT_FILL, UNIFORM);
  *   split_target >= 1 (AOT); bin_weights [n_bins] in 1..65535, or NULL
@@ -230,6 +241,9 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
  *            MI355X) when it starts bin k and when it has finished it, for
  *            measuring the load imbalance across workers.  Empty bins write
  *            equal stamps.
+ *   live_len [B][L][H] int32 or NULL, with layer: current lengths for items
+ *            of a TG_PLAN_OPEN_END plan (an open item with live_len NULL runs
+ *            to its table's capacity).
  * Supported: dtype TG_F32 or TG_BF16, head_dim 64 or 128, page_size 16,
  * gqa 1..16 (else TG_ERR_UNSUPPORTED).  hip_stream is a hipStream_t (NULL =
  * default stream).  Returns TG_ERR_HIP if a launch fails. */
@@ -253,10 +267,42 @@ typedef struct {
   void* workspace;
   size_t workspace_bytes;
   uint64_t* timestamps;
+  const int32_t* live_len;
+  int32_t layer;
 } tg_decode_args;
 
 size_t  tg_decode_workspace_bytes(const tg_geometry* geom, int32_t batch, int32_t num_partials);
 int32_t tg_decode(const tg_decode_args* args, void* hip_stream);
+
+/* 3a. decode-token append (device): one decode step's new token of one layer,
+ * written after every KV head's current entries (the cache grows by one token
+ * per head per step; Section 2.2, decode, on the ragged layout of Section
+ * 4.2).  Head (b, layer, h) with n = live_len[b][layer][h] entries stores the
+ * token as entry n (page pt_pages[pt_offsets[t] + n / P], row n % P, t =
+ * (b*L + layer)*G + group_of[layer][h]) and live_len becomes n + 1, when its
+ * table holds more than n entries; otherwise nothing is written for that head
+ * and *full (if not NULL) is set to 1.
+ * DEVICE pointers: k_tok, v_tok [B][H][d] dtype; kv_pool; pt_pages,
+ * pt_offsets [B*L*G+1]; group_of, slot_of [L][H]; live_len [B][L][H] int32
+ * (read and written); full: one int32 the caller clears, or NULL.
+ * Supported: dtype TG_F32 or TG_BF16, head_dim 64 or 128.  No workspace. */
+typedef struct {
+  tg_geometry geom;
+  int32_t batch;
+  int32_t layer;
+  int32_t dtype;
+  const void* k_tok;
+  const void* v_tok;
+  void* kv_pool;
+  const int32_t* pt_pages;
+  const int64_t* pt_offsets;
+  const int32_t* group_of;
+  const int32_t* slot_of;
+  int32_t* live_len;
+  int32_t* full;
+} tg_append_args;
+
+int32_t tg_append(const tg_append_args* args, void* hip_stream);
 
 /* ------------------------------- 4. ragged chunked-prefill attention (MFMA)
  * Chunked prefill (Section 2.2.1) over the compressed history (Section 4.1):

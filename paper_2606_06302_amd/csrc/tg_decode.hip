@@ -111,9 +111,21 @@ struct DecodeParams {
   int32_t n_bins;
   int32_t gqa;               // query heads per KV head
   uint64_t* timestamps;      // [n_bins][2] start / end stamps, or NULL
+  const int32_t* live;       // live lengths of this layer: live[b * live_stride + h], or NULL
+  int32_t live_stride;
   float scale_log2;          // sm_scale * log2(e)
   float scale;               // sm_scale
 };
+
+// An open-ended item (tok_end = -capacity) runs to the head's live length,
+// kept within [tok_begin + 1, capacity]; without live lengths, to capacity.
+__device__ __forceinline__ int resolve_end(int tok_begin, int tok_end, int b, int h, const int32_t* live,
+                                           int live_stride) {
+  if (tok_end >= 0) return tok_end;
+  const int cap = -tok_end;
+  const int n = live ? live[(int64_t)b * live_stride + h] : cap;
+  return min(max(n, tok_begin + 1), cap);
+}
 
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
@@ -189,7 +201,8 @@ __global__ void __launch_bounds__(kBlock) tg_decode_kernel(DecodeParams p, const
   const uint64_t t_start = __builtin_amdgcn_s_memrealtime();
 
   for (int it = it_begin; it < it_end; ++it) {
-    const tg_work_item item = items[it];
+    tg_work_item item = items[it];
+    item.tok_end = resolve_end(item.tok_begin, item.tok_end, item.b, item.kv_head, p.live, p.live_stride);
     const int qh0 = item.kv_head * GQA;
     u4 qv[GQA];
     {
@@ -370,7 +383,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 __device__ __forceinline__ void wait_lgkmcnt0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 // field-wise copy: the implicit copy constructor cannot bind a constant-space object
-__device__ __forceinline__ tg_work_item load_item(const TG_CONST tg_work_item* src) {
+__device__ __forceinline__ tg_work_item load_item(const TG_CONST tg_work_item* src, const DecodeParams& p) {
   tg_work_item r;
   r.pt_base = src->pt_base;
   r.b = src->b;
@@ -379,6 +392,12 @@ __device__ __forceinline__ tg_work_item load_item(const TG_CONST tg_work_item* s
   r.tok_begin = src->tok_begin;
   r.tok_end = src->tok_end;
   r.out_idx = src->out_idx;
+  if (r.tok_end < 0) {
+    const TG_CONST int32_t* live = (const TG_CONST int32_t*)p.live;
+    const int cap = -r.tok_end;
+    const int n = live ? live[(int64_t)r.b * p.live_stride + r.kv_head] : cap;
+    r.tok_end = min(max(n, r.tok_begin + 1), cap);
+  }
   return r;
 }
 
@@ -448,7 +467,7 @@ __global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, 
     int64_t pbase, qoff;
   };
   auto enter = [&](Cursor& cu, int it) {
-    const tg_work_item im = load_item(items + it);
+    const tg_work_item im = load_item(items + it, p);
     cu.it = it;
     cu.pi = 0;
     cu.np = (im.tok_end - im.tok_begin + kPage - 1) / kPage;
@@ -520,7 +539,7 @@ __global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, 
   f32x4 acc[8];
   for (;;) {
     if (pi == 0) {   // item start: its queries were DMA'd just before its first page
-      item = load_item(items + it);
+      item = load_item(items + it, p);
       ntok = item.tok_end - item.tok_begin;
       np = (ntok + kPage - 1) / kPage;
       if (d_live)
@@ -778,6 +797,10 @@ int32_t tg_decode(const tg_decode_args* a, void* hip_stream) {
   p.n_bins = a->n_bins;
   p.gqa = gqa;
   p.timestamps = a->timestamps;
+  if (a->live_len && (a->layer < 0 || a->layer >= g.num_layers))
+    return tg::fail(TG_ERR_INVALID_ARG, "layer %d out of range", a->layer);
+  p.live = a->live_len ? a->live_len + (int64_t)a->layer * g.num_kv_heads : nullptr;
+  p.live_stride = g.num_layers * g.num_kv_heads;
   p.scale = a->sm_scale != 0.f ? a->sm_scale : 1.0f / std::sqrt((float)g.head_dim);
   p.scale_log2 = p.scale * kLog2e;
   if (a->num_items == 0) return TG_OK;

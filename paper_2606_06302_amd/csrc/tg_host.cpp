@@ -168,8 +168,9 @@ int32_t tg_cluster_heads(const tg_geometry* geom, const double* budget, int32_t 
 }
 
 // Eq. 4 + Section 4.1 (Precise Page Allocation) + Section 4.2.1/4.2.3.
-int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_len, const double* ratio,
-                   const double* budget, const int32_t* group_of, const int32_t* free_pages, int64_t num_free,
+int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_len, const int32_t* headroom,
+                   const double* ratio, const double* budget, const int32_t* group_of, const int32_t* free_pages,
+                   int64_t num_free,
                    int64_t pool_pages, int32_t* kv_len, int32_t* group_len, int64_t* pt_offsets,
                    int32_t* pt_pages, int64_t pt_capacity, int64_t* pages_needed) {
   if (int32_t rc = tg::check_geometry(geom)) return rc;
@@ -183,8 +184,10 @@ int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_le
   const int64_t P = geom->page_size;
   for (int64_t i = 0; i < (int64_t)L * H; ++i)
     if (group_of[i] < 0 || group_of[i] >= G) return fail(TG_ERR_INVALID_ARG, "group_of[%lld] out of range", (long long)i);
-  for (int b = 0; b < batch; ++b)
+  for (int b = 0; b < batch; ++b) {
     if (ctx_len[b] < 1) return fail(TG_ERR_INVALID_ARG, "ctx_len[%d] < 1", b);
+    if (headroom && headroom[b] < 0) return fail(TG_ERR_INVALID_ARG, "headroom[%d] < 0", b);
+  }
   // retained lengths first (validating every ratio before anything is written)
   for (int b = 0; b < batch; ++b)
     for (int64_t i = 0; i < (int64_t)L * H; ++i) {
@@ -209,7 +212,7 @@ int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_le
       for (int h = 0; h < H; ++h) gl[gof[h]] = std::max(gl[gof[h]], kl[h]);
       for (int g = 0; g < G; ++g) {
         pt_offsets[((int64_t)b * L + l) * G + g] = k;
-        k += ceil_div(gl[g], P);
+        k += ceil_div((int64_t)gl[g] + (headroom ? headroom[b] : 0), P);
       }
     }
   pt_offsets[(int64_t)batch * L * G] = k;
@@ -265,7 +268,7 @@ int32_t tg_split_map(const tg_geometry* geom, const double* budget, const int32_
 }
 
 // Balanced split-KV partition of one layer (Algorithm 1's rule on the batch).
-int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, const int32_t* kv_len,
+static int32_t build_plan_core(const tg_geometry* geom, int32_t batch, int32_t layer, const int32_t* kv_len,
                       const int64_t* pt_offsets, const int32_t* group_of, const int32_t* slot_of, int32_t mode,
                       int32_t n_bins, int32_t split_target, const int32_t* bin_weights, tg_work_item* items,
                       int32_t item_capacity,
@@ -391,6 +394,30 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
   for (int32_t k = 0; k < n_bins; ++k) bin_offsets[k + 1] = bin_offsets[k] + count[k];
   std::vector<int32_t> fill(bin_offsets, bin_offsets + n_bins);
   for (int64_t i = 0; i < total; ++i) items[fill[bin_of[i]]++] = chunks[order[i]];
+  return TG_OK;
+}
+
+int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, const int32_t* kv_len,
+                      const int64_t* pt_offsets, const int32_t* group_of, const int32_t* slot_of, int32_t mode,
+                      int32_t n_bins, int32_t split_target, const int32_t* bin_weights, tg_work_item* items,
+                      int32_t item_capacity, int32_t* bin_offsets, int32_t bin_capacity, int32_t* unit_splits,
+                      int32_t* unit_partial_base, int32_t* num_items, int32_t* num_bins, int32_t* num_partials) {
+  if ((mode & ~0x1ff) != 0) return fail(TG_ERR_INVALID_ARG, "unknown plan mode %d", mode);
+  const bool open_end = (mode & TG_PLAN_OPEN_END) != 0;
+  const int32_t rc = build_plan_core(geom, batch, layer, kv_len, pt_offsets, group_of, slot_of,
+                                     mode & ~TG_PLAN_OPEN_END, n_bins, split_target, bin_weights, items,
+                                     item_capacity, bin_offsets, bin_capacity, unit_splits, unit_partial_base,
+                                     num_items, num_bins, num_partials);
+  if (rc != TG_OK || !open_end || !items) return rc;
+  // the chunk that ends each unit runs to the live length, bounded by its table
+  const int64_t L = geom->num_layers, H = geom->num_kv_heads, G = H / geom->heads_per_group;
+  for (int32_t i = 0; i < *num_items; ++i) {
+    tg_work_item& it = items[i];
+    const int64_t lh = (int64_t)layer * H + it.kv_head;
+    if (it.tok_end != kv_len[((int64_t)it.b * L + layer) * H + it.kv_head]) continue;
+    const int64_t t = ((int64_t)it.b * L + layer) * G + group_of[lh];
+    it.tok_end = (int32_t)(-(pt_offsets[t + 1] - pt_offsets[t]) * geom->page_size);
+  }
   return TG_OK;
 }
 

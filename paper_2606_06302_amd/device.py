@@ -49,10 +49,11 @@ def upload_plan(geom, batch, plan: dict, device) -> DevicePlan:
     )
 
 
-def bind_decode(dp: DevicePlan, geom, batch, dtype, q, kv_pool, pt_pages, out, lse=None, sm_scale=0.0):
+def bind_decode(dp: DevicePlan, geom, batch, dtype, q, kv_pool, pt_pages, out, lse=None, sm_scale=0.0,
+                live_len=None, layer=0):
     """Packs (and stores on dp) the tg_decode_args for this layer."""
     dp.args = tg.make_decode_args(geom, batch, dtype, q, kv_pool, pt_pages, dp.items, dp.bin_offsets,
                                   dp.host["num_bins"], dp.host["num_items"], dp.unit_splits,
                                   dp.unit_partial_base, dp.host["num_partials"], out, lse, sm_scale,
-                                  dp.workspace)
+                                  dp.workspace, live_len=live_len, layer=layer)
     return dp.args

@@ -21,20 +21,23 @@ TG_DTYPE = {"f32": tg.TG_F32, "bf16": tg.TG_BF16}
 class Tables:
     """Clustering + reservation of one workload (host arrays and device copies)."""
 
-    def __init__(self, wl, free_pages=None, pool_pages=None, grouping=tg.TG_GROUP_CLUSTERED, device="cuda"):
+    def __init__(self, wl, free_pages=None, pool_pages=None, grouping=tg.TG_GROUP_CLUSTERED, device="cuda",
+                 headroom=None):
         from workloads import free_list, pool_pages_for   # seeded inputs only
         g = wl.geom
         self.wl = wl
         self.perm, self.group_of, self.slot_of = tg.tg_cluster_heads(g, wl.budget, grouping)
+        self.headroom = headroom
         if free_pages is None:
             need = tg.tg_reserve(g, wl.ctx_len, wl.ratio, None, self.group_of, np.zeros(0, np.int32), 0,
-                                 size_query=True)["pages_needed"]
+                                 size_query=True, headroom=headroom)["pages_needed"]
             pool_pages = pool_pages_for(need)
             free_pages = free_list(wl, pool_pages)
         self.pool_pages = int(pool_pages)
         self.free_pages = np.asarray(free_pages, dtype=np.int32)
         t0 = time.perf_counter()
-        res = tg.tg_reserve(g, wl.ctx_len, wl.ratio, None, self.group_of, self.free_pages, self.pool_pages)
+        res = tg.tg_reserve(g, wl.ctx_len, wl.ratio, None, self.group_of, self.free_pages, self.pool_pages,
+                            headroom=headroom)
         self.reserve_us = (time.perf_counter() - t0) * 1e6
         self.kv_len = res["kv_len"]
         self.group_len = res["group_len"]
@@ -56,7 +59,7 @@ class DecodeSession:
     """Pool, queries, outputs and per-layer plans of one decode workload."""
 
     def __init__(self, wl, tables: Tables = None, mode=tg.TG_PLAN_AOT, n_bins=None, split_target=None,
-                 fill="device", pool=None, q=None, want_lse=True, device="cuda", layers=None):
+                 fill="device", pool=None, q=None, want_lse=True, device="cuda", layers=None, open_end=False):
         from workloads import S_POOL, S_Q, device_normal_, host_pool, host_q_decode, page_elems
         g = wl.geom
         self.wl, self.device = wl, device
@@ -68,6 +71,10 @@ class DecodeSession:
         if split_target is None:
             split_target = 2 * n_bins   # measured best on the 64-layer step (bins x {1,2,4,8})
         self.mode, self.n_bins, self.split_target = mode, n_bins, split_target
+        # open-ended plans: every unit's last chunk runs to the live length, so that the
+        # plans built here serve every later decode step (tokens appended with append_layer)
+        self.open_end = open_end
+        self.live_len = to_device(self.t.kv_len, device) if open_end else None
         self.bin_weights = None
         L, B = g.num_layers, wl.batch
         self.layers = list(range(L)) if layers is None else list(layers)
@@ -97,8 +104,9 @@ class DecodeSession:
         g, B = self.wl.geom, self.wl.batch
         # timed: this is the host planning cost the paper's Table 1 measures for a runtime planner
         t0 = time.perf_counter()
+        mode = self.mode | (tg.TG_PLAN_OPEN_END if self.open_end else 0)
         self.plans = {l: tg.tg_build_plan(g, B, l, self.t.kv_len, self.t.pt_offsets, self.t.group_of,
-                                          self.t.slot_of, self.mode, self.n_bins, self.split_target,
+                                          self.t.slot_of, mode, self.n_bins, self.split_target,
                                           bin_weights=self.bin_weights) for l in self.layers}
         self.plan_build_us = (time.perf_counter() - t0) * 1e6
         self.dplans = {l: upload_plan(g, B, p, self.device) for l, p in self.plans.items()}
@@ -107,7 +115,16 @@ class DecodeSession:
         g, B = self.wl.geom, self.wl.batch
         for l in self.layers:
             bind_decode(self.dplans[l], g, B, self.tg_dtype, self.q[l], self.pool, self.t.d_pt_pages, self.out[l],
-                        None if self.lse is None else self.lse[l])
+                        None if self.lse is None else self.lse[l], live_len=self.live_len, layer=l)
+
+    def item_tokens(self, l):
+        """Tokens of every item of layer l's plan; open-ended items count up to the lengths the
+        plan was built for."""
+        items = self.plans[l]["items"]
+        end = items["tok_end"].astype(np.int64)
+        open_ = end < 0
+        end[open_] = self.t.kv_len[items["b"][open_], l, items["kv_head"][open_]]
+        return end - items["tok_begin"]
 
     def calibrate_xcd_weights(self, stream=None, classes=8):
         """Measures every worker's pages per microsecond over one stamped step and rebuilds the
@@ -126,8 +143,7 @@ class DecodeSession:
             tg.tg_decode(args, stream)
             torch.cuda.synchronize()
             t = ts.view(-1, 2).cpu().numpy()
-            items = self.plans[l]["items"]
-            npages = -(-(items["tok_end"] - items["tok_begin"]).astype(np.int64) // self.wl.geom.page_size)
+            npages = -(-self.item_tokens(l) // self.wl.geom.page_size)
             bo = self.plans[l]["bin_offsets"]
             per_bin = np.add.reduceat(npages, bo[:-1]) if len(npages) else np.zeros(nb)
             per_bin[np.diff(bo) == 0] = 0
@@ -140,6 +156,31 @@ class DecodeSession:
         self._build_plans()
         self._bind()
         return speed
+
+    def enable_append(self, k_tok=None, v_tok=None):
+        """Device buffers for one decode step's new token per layer ([L][B][H][d] K and V) and the
+        tg_append arguments of every layer; run_decode_step then appends before attending."""
+        assert self.open_end, "appending needs open-ended plans and live lengths"
+        g, B, dev = self.wl.geom, self.wl.batch, self.device
+        shape = (g.num_layers, B, g.num_kv_heads, g.head_dim)
+        self.k_tok = k_tok if k_tok is not None else torch.zeros(shape, dtype=self.dtype, device=dev)
+        self.v_tok = v_tok if v_tok is not None else torch.zeros(shape, dtype=self.dtype, device=dev)
+        self.full = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.d_offsets = to_device(self.t.pt_offsets, dev)
+        self.d_group_of = to_device(self.t.group_of, dev)
+        self.d_slot_of = to_device(self.t.slot_of, dev)
+        self.append_args = {l: tg.make_append_args(g, B, l, self.tg_dtype, self.k_tok[l], self.v_tok[l], self.pool,
+                                                   self.t.d_pt_pages, self.d_offsets, self.d_group_of,
+                                                   self.d_slot_of, self.live_len, self.full) for l in self.layers}
+
+    def append_layer(self, l, stream=None):
+        tg.tg_append(self.append_args[l], stream)
+
+    def run_decode_step(self, stream=None):
+        """One decode step: per layer, the new token's K/V appended, then attention over the cache."""
+        for l in self.layers:
+            tg.tg_append(self.append_args[l], stream)
+            tg.tg_decode(self.dplans[l].args, stream)
 
     def run_layer(self, l, stream=None):
         tg.tg_decode(self.dplans[l].args, stream)
@@ -177,8 +218,7 @@ class DecodeSession:
     def bin_load_stats(self, l):
         """Planned token load per bin: (max, mean)."""
         p = self.plans[l]
-        items = p["items"]
-        lens = (items["tok_end"] - items["tok_begin"]).astype(np.int64)
+        lens = self.item_tokens(l)
         bo = p["bin_offsets"]
         loads = np.zeros(len(bo) - 1, dtype=np.int64)
         np.add.at(loads, np.repeat(np.arange(len(bo) - 1), np.diff(bo)), lens)

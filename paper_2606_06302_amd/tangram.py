@@ -19,6 +19,7 @@ TG_OK, TG_ERR_INVALID_ARG, TG_ERR_OUT_OF_PAGES, TG_ERR_BUFFER_TOO_SMALL, TG_ERR_
 TG_F32, TG_BF16 = 0, 1
 TG_GROUP_CLUSTERED, TG_GROUP_ADJACENT = 0, 1
 TG_PLAN_AOT, TG_PLAN_NAIVE, TG_PLAN_UNIFORM, TG_PLAN_AOT_FILL = 0, 1, 2, 3
+TG_PLAN_OPEN_END = 0x100
 
 # the 32-byte tg_work_item
 WORK_ITEM_DTYPE = np.dtype([("pt_base", "<i8"), ("b", "<i4"), ("kv_head", "<i4"), ("slot", "<i4"),
@@ -51,7 +52,7 @@ class tg_decode_args(C.Structure):
                 ("num_items", C.c_int32), ("unit_splits", C.c_void_p), ("unit_partial_base", C.c_void_p),
                 ("num_partials", C.c_int32), ("out", C.c_void_p), ("lse", C.c_void_p),
                 ("sm_scale", C.c_float), ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t),
-                ("timestamps", C.c_void_p)]
+                ("timestamps", C.c_void_p), ("live_len", C.c_void_p), ("layer", C.c_int32)]
 
 
 class tg_prefill_args(C.Structure):
@@ -61,6 +62,13 @@ class tg_prefill_args(C.Structure):
                 ("kv_len", C.c_void_p), ("group_of", C.c_void_p), ("slot_of", C.c_void_p),
                 ("out", C.c_void_p), ("sm_scale", C.c_float), ("workspace", C.c_void_p),
                 ("workspace_bytes", C.c_size_t), ("block_order", C.c_void_p), ("num_blocks", C.c_int32)]
+
+
+class tg_append_args(C.Structure):
+    _fields_ = [("geom", tg_geometry), ("batch", C.c_int32), ("layer", C.c_int32), ("dtype", C.c_int32),
+                ("k_tok", C.c_void_p), ("v_tok", C.c_void_p), ("kv_pool", C.c_void_p), ("pt_pages", C.c_void_p),
+                ("pt_offsets", C.c_void_p), ("group_of", C.c_void_p), ("slot_of", C.c_void_p),
+                ("live_len", C.c_void_p), ("full", C.c_void_p)]
 
 
 class tg_compress_args(C.Structure):
@@ -99,13 +107,14 @@ _SIGS = {
     "tg_last_error": (C.c_char_p, []),
     "tg_version": (_i32, []),
     "tg_cluster_heads": (_i32, [_G, _P, _i32, _P, _P, _P]),
-    "tg_reserve": (_i32, [_G, _i32, _P, _P, _P, _P, _P, _i64, _i64, _P, _P, _P, _P, _i64, _P]),
+    "tg_reserve": (_i32, [_G, _i32, _P, _P, _P, _P, _P, _P, _i64, _i64, _P, _P, _P, _P, _i64, _P]),
     "tg_split_map": (_i32, [_G, _P, _P, _i32, _P]),
     "tg_decode_max_ctas": (_i32, [_G, _i32, _i32, _P]),
     "tg_build_plan": (_i32, [_G, _i32, _i32, _P, _P, _P, _P, _i32, _i32, _i32, _P, _P, _i32, _P, _i32, _P, _P,
                              _P, _P, _P]),
     "tg_decode_workspace_bytes": (_sz, [_G, _i32, _i32]),
     "tg_decode": (_i32, [C.POINTER(tg_decode_args), _P]),
+    "tg_append": (_i32, [C.POINTER(tg_append_args), _P]),
     "tg_prefill_workspace_bytes": (_sz, [C.POINTER(tg_prefill_args)]),
     "tg_prefill": (_i32, [C.POINTER(tg_prefill_args), _P]),
     "tg_prefill_schedule": (_i32, [_G, _i32, _i32, _i32, _P, _i32, _P, _i32, _P]),
@@ -166,8 +175,9 @@ def tg_cluster_heads(geom, budget, grouping=TG_GROUP_CLUSTERED):
     return perm, gof, sof
 
 
-def tg_reserve(geom, ctx_len, ratio, budget, group_of, free_pages, pool_pages, size_query=False):
-    """-> dict(kv_len [B][L][H], group_len [B][L][G], pt_offsets, pt_pages, pages_needed)."""
+def tg_reserve(geom, ctx_len, ratio, budget, group_of, free_pages, pool_pages, size_query=False, headroom=None):
+    """-> dict(kv_len [B][L][H], group_len [B][L][G], pt_offsets, pt_pages, pages_needed).  headroom [B]
+    reserves room for that many decode tokens per request (None: none)."""
     g = _geom(geom)
     L, H, G = g.num_layers, g.num_kv_heads, g.num_kv_heads // max(1, g.heads_per_group)
     ctx = _host(ctx_len, np.int32)
@@ -180,7 +190,8 @@ def tg_reserve(geom, ctx_len, ratio, budget, group_of, free_pages, pool_pages, s
     group_len = np.zeros((B, L, G), np.int32)
     offsets = np.zeros(B * L * G + 1, np.int64)
     need = C.c_int64(0)
-    args = (C.byref(g), B, _ptr(ctx), _ptr(r), _ptr(bud), _ptr(gof), _ptr(free), len(free), int(pool_pages),
+    hr = None if headroom is None else _host(np.broadcast_to(headroom, (B,)), np.int32)
+    args = (C.byref(g), B, _ptr(ctx), _ptr(hr), _ptr(r), _ptr(bud), _ptr(gof), _ptr(free), len(free), int(pool_pages),
             _ptr(kv_len), _ptr(group_len), _ptr(offsets))
     rc = _lib.tg_reserve(*args, None, 0, C.byref(need))
     _check(rc, "tg_reserve")
@@ -250,14 +261,15 @@ def _stream(stream):
 
 def make_decode_args(geom, batch, dtype, q, kv_pool, pt_pages, items, bin_offsets, n_bins, num_items,
                      unit_splits, unit_partial_base, num_partials, out, lse=None, sm_scale=0.0,
-                     workspace=None, timestamps=None) -> tg_decode_args:
+                     workspace=None, timestamps=None, live_len=None, layer=0) -> tg_decode_args:
     """Packs a tg_decode_args from device tensors (kept alive by the caller); timestamps is an
-    int64 device tensor of 2*n_bins entries, or None."""
+    int64 device tensor of 2*n_bins entries, or None; live_len an int32 [B][L][H] device tensor of
+    current lengths for open-ended plans, or None."""
     return tg_decode_args(_geom(geom), int(batch), int(dtype), _dptr(q), _dptr(kv_pool), _dptr(pt_pages),
                           _dptr(items), _dptr(bin_offsets), int(n_bins), int(num_items), _dptr(unit_splits),
                           _dptr(unit_partial_base), int(num_partials), _dptr(out), _dptr(lse), float(sm_scale),
                           _dptr(workspace), 0 if workspace is None else workspace.numel() * workspace.element_size(),
-                          _dptr(timestamps))
+                          _dptr(timestamps), _dptr(live_len), int(layer))
 
 
 def tg_decode(args: tg_decode_args, stream=None):
@@ -343,3 +355,15 @@ def tg_memory_footprint(geom, ctx_len, ratio, budget, group_of) -> dict:
     _check(_lib.tg_memory_footprint(C.byref(g), len(ctx), _ptr(ctx), _ptr(r), _ptr(bud),
                                     _ptr(_host(group_of, np.int32)), C.byref(out)), "tg_memory_footprint")
     return {f[0]: int(getattr(out, f[0])) for f in tg_footprint._fields_}
+
+
+def make_append_args(geom, batch, layer, dtype, k_tok, v_tok, kv_pool, pt_pages, pt_offsets, group_of, slot_of,
+                     live_len, full=None) -> tg_append_args:
+    """Packs a tg_append_args from device tensors (kept alive by the caller)."""
+    return tg_append_args(_geom(geom), int(batch), int(layer), int(dtype), _dptr(k_tok), _dptr(v_tok),
+                          _dptr(kv_pool), _dptr(pt_pages), _dptr(pt_offsets), _dptr(group_of), _dptr(slot_of),
+                          _dptr(live_len), _dptr(full))
+
+
+def tg_append(args: tg_append_args, stream=None):
+    _check(_lib.tg_append(C.byref(args), _stream(stream)), "tg_append")

@@ -45,7 +45,7 @@ def test_c_struct_layouts_match_the_binding(tmp_path):
         pytest.skip("no host C compiler")
     structs = {"tg_decode_args": tg.tg_decode_args, "tg_prefill_args": tg.tg_prefill_args,
                "tg_compress_args": tg.tg_compress_args, "tg_geometry": tg.tg_geometry,
-               "tg_footprint": tg.tg_footprint}
+               "tg_footprint": tg.tg_footprint, "tg_append_args": tg.tg_append_args}
     items = {"tg_work_item": tg.WORK_ITEM_DTYPE, "tg_compress_item": tg.COMPRESS_ITEM_DTYPE}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "tangram.h"', "int main(void) {"]
     for name, cls in structs.items():

@@ -1,0 +1,132 @@
+"""Decode steps through the C ABI: tg_append writes each step's token after every head's entries, and one
+open-ended plan built before the first step serves every later step (tg_decode with live lengths)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_helpers import check_close, say
+from workloads import Geometry, custom, host_pool
+
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    from paper_2606_06302_amd import tangram as tg
+    from paper_2606_06302_amd.runner import TORCH_DTYPE, DecodeSession, Tables
+
+
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _f64(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def _session(geom, B, dtype, ctx, T, mode, seed, n_bins=64):
+    wl = custom(seed, geom, B, dtype, ctx)
+    tables = Tables(wl, headroom=np.full(B, T, dtype=np.int32))
+    pool = torch.from_numpy(host_pool(wl, tables.pool_pages)).to(TORCH_DTYPE[dtype]).cuda()
+    s = DecodeSession(wl, tables=tables, mode=mode, n_bins=n_bins, split_target=2 * n_bins, fill="host", pool=pool,
+                      open_end=True)
+    s.enable_append()
+    return wl, tables, s
+
+
+def _step_inputs(rng, s, dtype):
+    g = s.wl.geom
+    shape_tok = (g.num_layers, s.wl.batch, g.num_kv_heads, g.head_dim)
+    k = torch.from_numpy(rng.standard_normal(shape_tok, dtype=np.float32)).to(TORCH_DTYPE[dtype])
+    v = torch.from_numpy(rng.standard_normal(shape_tok, dtype=np.float32)).to(TORCH_DTYPE[dtype])
+    q = torch.from_numpy(rng.standard_normal(tuple(s.q.shape), dtype=np.float32)).to(TORCH_DTYPE[dtype])
+    s.k_tok.copy_(k.cuda())
+    s.v_tok.copy_(v.cuda())
+    s.q.copy_(q.cuda())
+    return _f64(k), _f64(v)
+
+
+@pytest.mark.parametrize("geom,dtype,mode", [
+    (Geometry(2, 8, 32, 128, 16, 2), "bf16", "fill"),
+    (Geometry(2, 8, 40, 128, 16, 2), "bf16", "aot"),
+    (Geometry(1, 4, 8, 64, 16, 2), "f32", "fill"),
+])
+def test_steps_with_one_plan_match_oracle(geom, dtype, mode):
+    _gpu()
+    T, B = 37, 4
+    m = tg.TG_PLAN_AOT_FILL if mode == "fill" else tg.TG_PLAN_AOT
+    wl, t, s = _session(geom, B, dtype, (20, 900), T, m, 4242 + geom.num_q_heads)
+    say(f"decode steps {geom} {dtype} {mode}: ctx {wl.ctx_len.tolist()}, {T} steps")
+    rng = np.random.default_rng(99)
+    ref_pool = _f64(s.pool)
+    live = t.kv_len.copy()
+    for step in range(1, T + 1):
+        ks, vs = _step_inputs(rng, s, dtype)
+        s.run_decode_step()
+        for l in range(geom.num_layers):
+            ref_pool, live, full = oracle.append_token(ks[l], vs[l], ref_pool, l, geom=geom, live_len=live,
+                                                       offsets=t.pt_offsets, pages=t.pt_pages, group_of=t.group_of,
+                                                       slot_of=t.slot_of)
+            assert full == []
+        if step in (1, 16, T):
+            torch.cuda.synchronize()
+            assert np.array_equal(s.live_len.cpu().numpy(), live)
+            assert np.array_equal(_f64(s.pool), ref_pool), f"pool differs after step {step}"
+            q = _f64(s.q)
+            for l in range(geom.num_layers):
+                O, lse = oracle.decode_attention(q[l], ref_pool, l, geom=geom, batch=B, kv_len=live,
+                                                 offsets=t.pt_offsets, pages=t.pt_pages, group_of=t.group_of,
+                                                 slot_of=t.slot_of)
+                got = _f64(s.out[l]).reshape(-1, geom.head_dim)
+                check_close(got, O.reshape(-1, geom.head_dim), dtype, f"step {step} layer {l}")
+            say(f"  step {step}: ok")
+    assert int(s.full.item()) == 0
+
+
+def test_append_without_room_sets_flag_and_writes_nothing():
+    _gpu()
+    g = Geometry(1, 4, 8, 64, 16, 2)
+    B = 2
+    wl = custom(77, g, B, "bf16", [512, 512], budget=np.array([[1.0, 0.5, 0.25, 0.125]]), jitter=0.0)
+    t = Tables(wl)           # no headroom: heads 0 (512 of 512) and 2 (128 of 128) are full
+    pool = torch.from_numpy(host_pool(wl, t.pool_pages)).to(torch.bfloat16).cuda()
+    s = DecodeSession(wl, tables=t, mode=tg.TG_PLAN_AOT_FILL, n_bins=16, fill="host", pool=pool, open_end=True)
+    s.enable_append()
+    rng = np.random.default_rng(5)
+    ks, vs = _step_inputs(rng, s, "bf16")
+    before = _f64(s.pool)
+    s.append_layer(0)
+    torch.cuda.synchronize()
+    ref, live, full = oracle.append_token(ks[0], vs[0], before, 0, geom=g, live_len=t.kv_len, offsets=t.pt_offsets,
+                                          pages=t.pt_pages, group_of=t.group_of, slot_of=t.slot_of)
+    assert sorted(full) == [(0, 0), (0, 2), (1, 0), (1, 2)]
+    assert int(s.full.item()) == 1
+    assert np.array_equal(s.live_len.cpu().numpy(), live)
+    assert np.array_equal(_f64(s.pool), ref)
+
+
+def test_reused_plan_equals_fresh_plan():
+    """After T steps, the open plan built before the first step and a plan built on the grown lengths give
+    the same attention (both within tolerance of the oracle, and of each other)."""
+    _gpu()
+    g = Geometry(1, 8, 64, 128, 16, 2)
+    B, T = 8, 50
+    wl, t, s = _session(g, B, "bf16", (500, 5000), T, tg.TG_PLAN_AOT_FILL, 515)
+    rng = np.random.default_rng(3)
+    for _ in range(T):
+        _step_inputs(rng, s, "bf16")
+        s.run_decode_step()
+    torch.cuda.synchronize()
+    reused = _f64(s.out[0])
+    live = s.live_len.cpu().numpy()
+    fresh = tg.tg_build_plan(g, B, 0, live, t.pt_offsets, t.group_of, t.slot_of, tg.TG_PLAN_AOT_FILL, 64)
+    from paper_2606_06302_amd.device import bind_decode, upload_plan
+    dp = upload_plan(g, B, fresh, "cuda")
+    out2 = torch.zeros_like(s.out[0])
+    bind_decode(dp, g, B, tg.TG_BF16, s.q[0], s.pool, t.d_pt_pages, out2)
+    tg.tg_decode(dp.args)
+    torch.cuda.synchronize()
+    O, _ = oracle.decode_attention(_f64(s.q[0]), _f64(s.pool), 0, geom=g, batch=B, kv_len=live, offsets=t.pt_offsets,
+                                   pages=t.pt_pages, group_of=t.group_of, slot_of=t.slot_of)
+    check_close(reused.reshape(-1, 128), O.reshape(-1, 128), "bf16", "reused plan")
+    check_close(_f64(out2).reshape(-1, 128), O.reshape(-1, 128), "bf16", "fresh plan")

@@ -388,3 +388,64 @@ def test_footprint_budget_broadcast_and_errors():
         with pytest.raises(tg.TangramError) as e:
             tg.tg_memory_footprint(geom, *args)
         assert e.value.code == tg.TG_ERR_INVALID_ARG
+
+
+# ------------------------------------------------ decode steps: headroom, open-ended plans
+
+@settings(max_examples=40, deadline=None)
+@given(st.data())
+def test_headroom_and_open_plans_bit_exact(data):
+    H = data.draw(st.sampled_from([2, 4, 8]))
+    Hp = data.draw(st.sampled_from([h for h in (1, 2, 4) if H % h == 0]))
+    L = data.draw(st.integers(1, 3))
+    P = data.draw(st.sampled_from([1, 5, 16]))
+    B = data.draw(st.integers(1, 5))
+    geom = Geometry(L, H, 2 * H, 64, P, Hp)
+    rng = np.random.default_rng(data.draw(st.integers(0, 2**31)))
+    budget = rng.uniform(0.01, 1.0, size=(L, H))
+    ratio = np.clip(budget[None] + rng.uniform(-0.05, 0.05, size=(B, L, H)), 0.01, 1.0)
+    ctx = rng.integers(1, 2000, size=B).astype(np.int32)
+    headroom = rng.integers(0, 300, size=B).astype(np.int32)
+    _, gof, sof = tg.tg_cluster_heads(geom, budget)
+    res = tg.tg_reserve(geom, ctx, ratio, None, gof, np.arange(10**6, dtype=np.int32), 10**6, headroom=headroom)
+    ores = oracle.reserve(ratio, ctx, gof, H // Hp, P, np.arange(10**6), headroom=headroom)
+    assert np.array_equal(res["pt_offsets"], ores["offsets"]) and np.array_equal(res["kv_len"], ores["kv_len"])
+    mode = data.draw(st.sampled_from([tg.TG_PLAN_AOT, tg.TG_PLAN_NAIVE, tg.TG_PLAN_UNIFORM, tg.TG_PLAN_AOT_FILL]))
+    layer = data.draw(st.integers(0, L - 1))
+    pl = tg.tg_build_plan(geom, B, layer, res["kv_len"], res["pt_offsets"], gof, sof, mode | tg.TG_PLAN_OPEN_END,
+                          7, 29)
+    opl = oracle.partition_plan(ores["kv_len"], ores["offsets"], gof, sof, layer, num_layers=L, num_groups=H // Hp,
+                                page_size=P, mode=mode, n_bins=7, split_target=29, open_end=True)
+    assert _items_as_tuples(pl["items"]) == opl["items"]
+    assert pl["bin_offsets"].tolist() == opl["bin_offsets"].tolist()
+    assert sum(1 for it in opl["items"] if it[5] < 0) == B * H
+
+
+def test_headroom_config1_hand_and_errors():
+    wl = config(1)
+    _, gof, _ = tg.tg_cluster_heads(wl.geom, wl.budget)
+    res = tg.tg_reserve(wl.geom, wl.ctx_len, wl.ratio, None, gof, np.arange(100, dtype=np.int32), 100,
+                        headroom=[20, 20])
+    assert res["pt_offsets"].tolist() == [0, 10, 44, 54, 88]
+    with pytest.raises(tg.TangramError) as e:
+        tg.tg_reserve(wl.geom, wl.ctx_len, wl.ratio, None, gof, np.arange(100, dtype=np.int32), 100,
+                      headroom=[0, -1])
+    assert e.value.code == tg.TG_ERR_INVALID_ARG
+    with pytest.raises(tg.TangramError) as e:
+        tg.tg_build_plan(wl.geom, 2, 0, res["kv_len"], res["pt_offsets"], gof, gof, 0x200)
+    assert e.value.code == tg.TG_ERR_INVALID_ARG
+
+
+def test_append_launch_validation_on_host():
+    g = Geometry(1, 2, 2, 128, 16, 2)
+    bad = tg.tg_append_args(tg._geom(Geometry(1, 2, 2, 96, 16, 2)), 1, 0, tg.TG_BF16, *([None] * 8), None)
+    with pytest.raises(tg.TangramError) as e:
+        tg.tg_append(bad)
+    assert e.value.code == tg.TG_ERR_UNSUPPORTED
+    for kw in (dict(layer=1), dict(batch=0), dict(layer=0)):   # the last: NULL device pointers
+        a = dict(batch=1, layer=0)
+        a.update(kw)
+        args = tg.tg_append_args(tg._geom(g), a["batch"], a["layer"], tg.TG_BF16, *([None] * 8), None)
+        with pytest.raises(tg.TangramError) as e:
+            tg.tg_append(args)
+        assert e.value.code == tg.TG_ERR_INVALID_ARG, kw
