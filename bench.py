@@ -17,6 +17,7 @@ divided by the measured step time.
     python bench.py --config 5             # chunked prefill + compression of the chunk
     python bench.py --compress-chunk C     # chunk compression alone, chunk of C tokens
     python bench.py --memory               # host only: memory reclaimed per paging scheme
+    python bench.py --plan-reuse           # planning cost vs decode step, 28 to 80 layers
     python bench.py --copy-probe BYTES     # plain copy kernel, for counter calibration
 """
 from __future__ import annotations
@@ -366,6 +367,64 @@ def bench_memory(args):
                       "data": "synthetic", "rows": rows}), flush=True)
 
 
+def bench_plan_reuse(args):
+    """Planning cost against the decode step (the analog of the paper's Table 1) for four model shapes.
+    One decode step = for every layer, the new token's K/V appended (tg_append) and attention over the
+    cache (tg_decode).  The ahead-of-time open-ended plans are built once, before the first step, and
+    serve every step; a planner run at every step would cost plan_build_ms (host) + plan_upload_ms."""
+    import torch
+    from paper_2606_06302_amd import tangram as tg
+    from paper_2606_06302_amd.device import upload_plan
+    from paper_2606_06302_amd.runner import DecodeSession, Tables
+    from workloads import MODEL_SHAPES, model_step
+    rows = []
+    steps, warmup = args.steps, args.warmup
+    for name in MODEL_SHAPES:
+        wl = model_step(name)
+        g = wl.geom
+        log(f"[bench] {wl.name}: {g.num_layers} layers, tables and pool")
+        t = Tables(wl, headroom=np.full(wl.batch, steps + warmup + 2, dtype=np.int32))
+        s = DecodeSession(wl, tables=t, mode=tg.TG_PLAN_AOT_FILL, open_end=True)
+        s.enable_append()
+        torch.cuda.synchronize()
+        # host planning of every layer, as a per-step planner would have to redo it
+        t0 = time.perf_counter()
+        plans = [tg.tg_build_plan(g, wl.batch, l, t.kv_len, t.pt_offsets, t.group_of, t.slot_of,
+                                  tg.TG_PLAN_AOT_FILL | tg.TG_PLAN_OPEN_END, s.n_bins) for l in s.layers]
+        plan_ms = (time.perf_counter() - t0) * 1e3
+        t0 = time.perf_counter()
+        for p_ in plans:
+            upload_plan(g, wl.batch, p_, "cuda")
+        torch.cuda.synchronize()
+        upload_ms = (time.perf_counter() - t0) * 1e3
+        stream = torch.cuda.Stream()
+        with torch.cuda.stream(stream):
+            for _ in range(warmup):
+                s.run_decode_step(stream)
+            stream.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(steps):
+                s.run_decode_step(stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+        step_ms = e0.elapsed_time(e1) / steps
+        assert int(s.full.item()) == 0, "decode headroom exhausted"
+        kv = int(s.live_len.sum().item()) * 2 * g.head_dim * 2
+        rows.append({"model": name, "layers": g.num_layers, "q_heads": g.num_q_heads, "kv_heads": g.num_kv_heads,
+                     "batch": wl.batch, "step_ms": round(step_ms, 3), "kv_GB_per_step": round(kv / 1e9, 2),
+                     "kv_GBps": round(kv / (step_ms * 1e-3) / 1e9, 1),
+                     "plan_build_ms": round(plan_ms, 3), "plan_upload_ms": round(upload_ms, 3),
+                     "replan_share": round((plan_ms + upload_ms) / (plan_ms + upload_ms + step_ms), 4),
+                     "aot_plan_share": 0.0})
+        log(f"[bench]   step {step_ms:.3f} ms ({rows[-1]['kv_GBps']} GB/s), plan {plan_ms:.2f} ms + upload "
+            f"{upload_ms:.2f} ms")
+        del s, t, plans
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": "planning cost vs decode step (append + attention, all layers)",
+                      "data": "synthetic", "steps": steps, "warmup": warmup, "rows": rows}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -384,6 +443,8 @@ def main():
     ap.add_argument("--compress-chunk", type=int, default=0,
                     help="time only the compression of a chunk of this many tokens (config 5's requests)")
     ap.add_argument("--rows-per-item", type=int, default=0)
+    ap.add_argument("--plan-reuse", action="store_true",
+                    help="planning cost against the decode step (append + attention) for 28 to 80 layers")
     ap.add_argument("--memory", action="store_true",
                     help="host-only: memory reclaimed by ragged paging for each heads-per-group and grouping")
     ap.add_argument("--free-order", default="shuffled", choices=["shuffled", "sequential"],
@@ -407,6 +468,8 @@ def main():
 
     if args.compress_chunk:
         return bench_compress(args)
+    if args.plan_reuse:
+        return bench_plan_reuse(args)
     if args.config == 5:
         return bench_prefill(args)
     mode = {"aot": tg.TG_PLAN_AOT, "fill": tg.TG_PLAN_AOT_FILL, "naive": tg.TG_PLAN_NAIVE,

@@ -149,6 +149,33 @@ def config(cfg: int) -> Workload:
     raise ValueError(f"unknown config {cfg}")
 
 
+# Decode-step shapes of the four models of the paper's planning-cost table (Table 1), with config 3's batch,
+# contexts and retention structure: (layers, query heads, KV heads).
+MODEL_SHAPES = {
+    "qwen2.5-7b": (28, 28, 4),
+    "llama3.1-8b": (32, 32, 8),
+    "qwen3-32b": (64, 64, 8),
+    "llama3.1-70b": (80, 64, 8),
+}
+
+
+def model_step(name: str) -> Workload:
+    """A decode step of one of MODEL_SHAPES: B = 64, d = 128, bf16, page 16, groups of 2 heads, contexts
+    clip(round(exp(ln 16384 + 0.75 Z)), 2048, 65536), 20 % of (layer, head) pairs ~U(0.6, 1.0), the rest
+    ~U(0.03, 0.15), per-request jitter (config 3's recipe)."""
+    L, Hq, H = MODEL_SHAPES[name]
+    seed = 2000 + sorted(MODEL_SHAPES).index(name)
+    ss = np.random.SeedSequence(seed).spawn(N_STREAMS)
+    r_ratio = np.random.default_rng(ss[S_RATIO])
+    r_ctx = np.random.default_rng(ss[S_CTX])
+    g = Geometry(L, H, Hq, 128, 16, 2)
+    budget = _two_level_profile(r_ratio, L, H, 0.20, (0.6, 1.0), (0.03, 0.15))
+    ratio = _jitter(r_ratio, budget, 64)
+    z = r_ctx.standard_normal(64)
+    ctx = np.clip(np.round(np.exp(math.log(16384.0) + 0.75 * z)), 2048, 65536).astype(np.int32)
+    return Workload(f"{name}-decode-step-bf16", seed, g, 64, "bf16", ctx, budget, ratio)
+
+
 def custom(seed: int, geom: Geometry, batch: int, dtype: str, ctx_len, budget=None, ratio=None,
            frac_hi=0.25, hi=(0.7, 1.0), lo=(0.05, 0.2), jitter=0.03, chunk_len=0,
            q_scale=1.0, kv_scale=1.0) -> Workload:
