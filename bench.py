@@ -431,7 +431,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--config", type=int, default=3)
-    ap.add_argument("--mode", default="fill", choices=["aot", "fill", "naive", "uniform"])
+    ap.add_argument("--mode", default="fill", choices=["aot", "fill", "naive", "uniform", "splitmap"])
     ap.add_argument("--n-bins", type=int, default=0)
     ap.add_argument("--split-target", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -473,7 +473,7 @@ def main():
     if args.config == 5:
         return bench_prefill(args)
     mode = {"aot": tg.TG_PLAN_AOT, "fill": tg.TG_PLAN_AOT_FILL, "naive": tg.TG_PLAN_NAIVE,
-            "uniform": tg.TG_PLAN_UNIFORM}[args.mode]
+            "uniform": tg.TG_PLAN_UNIFORM, "splitmap": tg.TG_PLAN_SPLIT_MAP}[args.mode]
     wl = config(args.config)
     log(f"[bench] workload {wl.name}: building tables, plans and a "
         f"{'device-filled' if args.config != 1 else 'host-filled'} pool")

@@ -62,7 +62,7 @@ enum { TG_F32 = 0, TG_BF16 = 1 };
 /* head grouping for tg_cluster_heads */
 enum { TG_GROUP_CLUSTERED = 0, TG_GROUP_ADJACENT = 1 };
 /* partition modes for tg_build_plan */
-enum { TG_PLAN_AOT = 0, TG_PLAN_NAIVE = 1, TG_PLAN_UNIFORM = 2, TG_PLAN_AOT_FILL = 3 };
+enum { TG_PLAN_AOT = 0, TG_PLAN_NAIVE = 1, TG_PLAN_UNIFORM = 2, TG_PLAN_AOT_FILL = 3, TG_PLAN_SPLIT_MAP = 4 };
 /* flag OR'ed into a tg_build_plan mode: plans that stay valid while decode
  * steps append tokens (see tg_build_plan) */
 enum { TG_PLAN_OPEN_END = 0x100 };
@@ -171,6 +171,12 @@ int32_t tg_decode_max_ctas(const tg_geometry* geom, int32_t dtype, int32_t devic
  *            in proportion to its length; s_u = number of pieces of u.
  *            Weights let a plan give less work to workers that run slower
  *            (e.g. measured per-XCD throughput differences).
+ *   SPLIT_MAP: Algorithm 1's split map used as is: bin_weights holds the
+ *            layer's row S[layer][0..G-1] of tg_split_map (each in 1..65535;
+ *            n_bins is ignored).  Group g's units, in (b, h) order, are laid
+ *            end to end and cut like AOT_FILL into S[layer][g] equal page
+ *            ranges; the groups' bins follow each other in group order, so
+ *            there are sum_g S[layer][g] bins.
  *   chunk c < s_u of unit u covers pages [c*n_u/s_u, (c+1)*n_u/s_u) and tokens
  *   [p0*P, min(p1*P, kv_len)).  out_idx = -1 when s_u == 1, else
  *   unit_partial_base[u] + c (partials numbered over units in order).
@@ -187,10 +193,11 @@ int32_t tg_decode_max_ctas(const tg_geometry* geom, int32_t dtype, int32_t devic
  * Arguments (host): kv_len [B][L][H] and pt_offsets [B*L*G+1] from tg_reserve;
  *   group_of, slot_of [L][H]; 0 <= layer < L; n_bins >= 1 (AOT, AOT_FILL, UNIFORM);
  *   split_target >= 1 (AOT); bin_weights [n_bins] in 1..65535, or NULL
- *   (AOT_FILL only; NULL otherwise); items [item_capacity] out, or NULL for a size
+ *   (AOT_FILL), [G] (SPLIT_MAP, required), NULL otherwise; items [item_capacity] out, or NULL for a size
  *   query (num_items, num_partials and the bin count are still written);
- *   bin_offsets [bins+1] out, where bins = n_bins (AOT, AOT_FILL), B*H (NAIVE) or the
- *   number of chunks (UNIFORM) - its capacity is bin_capacity entries;
+ *   bin_offsets [bins+1] out, where bins = n_bins (AOT, AOT_FILL), B*H (NAIVE), the
+ *   number of chunks (UNIFORM) or sum_g S[layer][g] (SPLIT_MAP) - its capacity is
+ *   bin_capacity entries;
  *   unit_splits [B][H] out; unit_partial_base [B][H] out (-1 when unsplit);
  *   num_items, num_bins, num_partials out.
  * Errors: TG_ERR_INVALID_ARG; TG_ERR_BUFFER_TOO_SMALL when item_capacity <

@@ -73,7 +73,7 @@ import math
 
 import numpy as np
 
-MODE_AOT, MODE_NAIVE, MODE_UNIFORM, MODE_FILL = 0, 1, 2, 3
+MODE_AOT, MODE_NAIVE, MODE_UNIFORM, MODE_FILL, MODE_SPLIT_MAP = 0, 1, 2, 3, 4
 GROUP_CLUSTERED, GROUP_ADJACENT = 0, 1
 
 
@@ -325,6 +325,8 @@ def _partition_plan(kv_len, offsets, group_of, slot_of, layer, *, num_layers, nu
     Bn, L, H = kv_len.shape
     P = page_size
     lens = [[int(kv_len[b, layer, h]) for h in range(H)] for b in range(Bn)]
+    if mode == MODE_SPLIT_MAP:
+        return _split_map_plan(lens, offsets, group_of, slot_of, layer, num_layers, num_groups, P, bin_weights)
     if mode == MODE_FILL:
         return _fill_plan(lens, offsets, group_of, slot_of, layer, num_layers, num_groups, P, n_bins,
                           bin_weights)
@@ -382,6 +384,54 @@ def _partition_plan(kv_len, offsets, group_of, slot_of, layer, *, num_layers, nu
     return dict(items=items, bin_offsets=np.array(bin_offsets, dtype=np.int64),
                 unit_splits=splits, unit_partial_base=base, num_partials=nparts,
                 bin_load=np.array(bin_load, dtype=np.int64))
+
+
+def _split_map_plan(lens, offsets, group_of, slot_of, layer, num_layers, num_groups, P, S_row):
+    """Algorithm 1's split map used as the executed plan: head group g of this
+    layer gets S_row[g] workers, which share the group's work over the whole
+    batch (its units (b, h) in (b, h) order, pages laid end to end) in equal
+    page ranges.  The groups' bins follow each other in group order."""
+    Bn, H = len(lens), len(lens[0])
+    pieces = []                               # (bin, (b, h), first page, end page)
+    first_bin = 0
+    for g in range(num_groups):
+        units = [(b, h) for b in range(Bn) for h in range(H) if int(group_of[layer, h]) == g]
+        start = [0]
+        for b, h in units:
+            start.append(start[-1] + -(-lens[b][h] // P))
+        total, S = start[-1], int(S_row[g])
+        for k in range(S):
+            lo, hi = total * k // S, total * (k + 1) // S
+            for i, u in enumerate(units):
+                a, z = max(lo, start[i]), min(hi, start[i + 1])
+                if a < z:
+                    pieces.append((first_bin + k, u, a - start[i], z - start[i]))
+        first_bin += S
+    splits = np.zeros((Bn, H), dtype=np.int64)
+    for _, (b, h), _, _ in pieces:
+        splits[b, h] += 1
+    base = np.full((Bn, H), -1, dtype=np.int64)
+    nparts = 0
+    for b in range(Bn):
+        for h in range(H):
+            if splits[b, h] > 1:
+                base[b, h] = nparts
+                nparts += int(splits[b, h])
+    seen = np.zeros((Bn, H), dtype=np.int64)
+    bins = [[] for _ in range(first_bin)]
+    for k, (b, h), p0, p1 in pieces:
+        c = int(seen[b, h])
+        seen[b, h] += 1
+        pt_base = int(offsets[(b * num_layers + layer) * num_groups + int(group_of[layer, h])])
+        out_idx = -1 if splits[b, h] == 1 else int(base[b, h]) + c
+        bins[k].append((pt_base, b, h, int(slot_of[layer, h]), p0 * P, min(p1 * P, lens[b][h]), out_idx))
+    items, bin_offsets, bin_load = [], [0], []
+    for blist in bins:
+        items.extend(blist)
+        bin_offsets.append(len(items))
+        bin_load.append(sum(it[5] - it[4] for it in blist))
+    return dict(items=items, bin_offsets=np.array(bin_offsets, dtype=np.int64), unit_splits=splits,
+                unit_partial_base=base, num_partials=nparts, bin_load=np.array(bin_load, dtype=np.int64))
 
 
 def _fill_plan(lens, offsets, group_of, slot_of, layer, num_layers, num_groups, P, n_bins, bin_weights=None):

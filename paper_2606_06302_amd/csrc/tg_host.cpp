@@ -49,38 +49,57 @@ static bool ratio_ok(double r) { return r > 0.0 && r <= 1.0; }  // false for NaN
 using tg::ceil_div;
 using tg::fail;
 
-// TG_PLAN_AOT_FILL: the units' pages laid end to end (unit order b, h) and cut
-// into n_bins equal page ranges; a unit is split wherever a boundary falls in it.
-static int32_t fill_plan(int L, int G, int H, int64_t P, int batch, int layer, const std::vector<int64_t>& len,
-                         const std::vector<int64_t>& base, const int32_t* slot_of, int32_t n_bins,
-                         const int32_t* bin_weights, tg_work_item* items, int32_t item_capacity,
-                         int32_t* bin_offsets, int32_t bin_capacity, int32_t* unit_splits, int32_t* unit_partial_base,
-                         int32_t* num_items, int32_t* num_bins, int32_t* num_partials) {
-  (void)L;
-  (void)G;
-  const int64_t n_units = (int64_t)batch * H;
-  std::vector<int64_t> start(n_units + 1, 0);
-  for (int64_t u = 0; u < n_units; ++u) start[u + 1] = start[u] + ceil_div(len[u], P);
-  const int64_t total = start[n_units];
-  // bin k covers pages [cut[k], cut[k+1]): cut[k] = floor(total * W_k / W), W_k the
-  // weight of the bins before k (every weight 1 when bin_weights is NULL)
-  std::vector<int64_t> cut(n_bins + 1);
-  {
-    std::vector<int64_t> wsum(n_bins + 1, 0);
-    for (int32_t k = 0; k < n_bins; ++k) wsum[k + 1] = wsum[k] + (bin_weights ? bin_weights[k] : 1);
-    for (int32_t k = 0; k <= n_bins; ++k) cut[k] = (int64_t)((__int128)total * wsum[k] / wsum[n_bins]);
-  }
-  // pass 1: count pieces per unit (bins walk the units monotonically)
+// Sequential fill over segments: each segment is a list of units laid end to
+// end (in the given order) and cut into its own number of bins whose page
+// shares follow the segment's weights (equal when NULL).  Bins are numbered
+// across segments in order; a unit cut by a boundary is split, and partial
+// indices are numbered over all units in (b, h) order.
+//   TG_PLAN_AOT_FILL:  one segment, every unit, n_bins bins (optionally weighted);
+//   TG_PLAN_SPLIT_MAP: one segment per head group g (its units in (b, h) order)
+//                      with S[layer][g] bins: Algorithm 1's split map as is.
+struct FillSegment {
+  std::vector<int64_t> units;
+  int64_t n_bins;
+  const int32_t* weights;
+};
+
+static int32_t segmented_fill(int H, int64_t P, int layer, const std::vector<int64_t>& len,
+                              const std::vector<int64_t>& base, const int32_t* slot_of,
+                              const std::vector<FillSegment>& segs, tg_work_item* items, int32_t item_capacity,
+                              int32_t* bin_offsets, int32_t bin_capacity, int32_t* unit_splits,
+                              int32_t* unit_partial_base, int32_t* num_items, int32_t* num_bins,
+                              int32_t* num_partials) {
+  const int64_t n_units = (int64_t)len.size();
+  struct Cut {
+    std::vector<int64_t> start, cut;
+  };
+  std::vector<Cut> cuts(segs.size());
   std::vector<int64_t> pieces(n_units, 0);
-  int64_t n_items = 0;
-  for (int64_t k = 0, u = 0; k < n_bins; ++k) {
-    const int64_t lo = cut[k], hi = cut[k + 1];
-    while (u < n_units && start[u + 1] <= lo) ++u;
-    for (int64_t v = u; v < n_units && start[v] < hi; ++v)
-      if (std::max(lo, start[v]) < std::min(hi, start[v + 1])) {
-        ++pieces[v];
-        ++n_items;
-      }
+  int64_t n_items = 0, total_bins = 0;
+  for (size_t si = 0; si < segs.size(); ++si) {
+    const FillSegment& sg = segs[si];
+    Cut& c = cuts[si];
+    const int64_t nu = (int64_t)sg.units.size();
+    c.start.assign(nu + 1, 0);
+    for (int64_t i = 0; i < nu; ++i) c.start[i + 1] = c.start[i] + ceil_div(len[sg.units[i]], P);
+    const int64_t total = c.start[nu];
+    // bin k covers pages [cut[k], cut[k+1]): cut[k] = floor(total * W_k / W), W_k the
+    // weight of the segment's bins before k
+    std::vector<int64_t> wsum(sg.n_bins + 1, 0);
+    for (int64_t k = 0; k < sg.n_bins; ++k) wsum[k + 1] = wsum[k] + (sg.weights ? sg.weights[k] : 1);
+    c.cut.resize(sg.n_bins + 1);
+    for (int64_t k = 0; k <= sg.n_bins; ++k) c.cut[k] = (int64_t)((__int128)total * wsum[k] / wsum[sg.n_bins]);
+    // count the pieces of every unit (bins walk the units monotonically)
+    for (int64_t k = 0, i = 0; k < sg.n_bins; ++k) {
+      const int64_t lo = c.cut[k], hi = c.cut[k + 1];
+      while (i < nu && c.start[i + 1] <= lo) ++i;
+      for (int64_t j = i; j < nu && c.start[j] < hi; ++j)
+        if (std::max(lo, c.start[j]) < std::min(hi, c.start[j + 1])) {
+          ++pieces[sg.units[j]];
+          ++n_items;
+        }
+    }
+    total_bins += sg.n_bins;
   }
   int64_t nparts = 0;
   for (int64_t u = 0; u < n_units; ++u) {
@@ -88,36 +107,43 @@ static int32_t fill_plan(int L, int G, int H, int64_t P, int batch, int layer, c
     unit_partial_base[u] = pieces[u] > 1 ? (int32_t)nparts : -1;
     if (pieces[u] > 1) nparts += pieces[u];
   }
-  if (n_items > INT32_MAX || nparts > INT32_MAX) return fail(TG_ERR_INVALID_ARG, "plan too large");
+  if (n_items > INT32_MAX || nparts > INT32_MAX || total_bins > INT32_MAX - 1)
+    return fail(TG_ERR_INVALID_ARG, "plan too large");
   *num_items = (int32_t)n_items;
-  *num_bins = n_bins;
+  *num_bins = (int32_t)total_bins;
   *num_partials = (int32_t)nparts;
   if (!items) return TG_OK;  // size query
   if (!bin_offsets) return fail(TG_ERR_INVALID_ARG, "bin_offsets is NULL");
   if (item_capacity < n_items) return fail(TG_ERR_BUFFER_TOO_SMALL, "items holds %d, need %lld", item_capacity, (long long)n_items);
-  if (bin_capacity < (int64_t)n_bins + 1) return fail(TG_ERR_BUFFER_TOO_SMALL, "bin_offsets holds %d, need %d", bin_capacity, n_bins + 1);
-  // pass 2: emit
+  if (bin_capacity < total_bins + 1)
+    return fail(TG_ERR_BUFFER_TOO_SMALL, "bin_offsets holds %d, need %lld", bin_capacity, (long long)(total_bins + 1));
   std::vector<int64_t> seen(n_units, 0);
-  int64_t it = 0;
+  int64_t it = 0, bin = 0;
   bin_offsets[0] = 0;
-  for (int64_t k = 0, u = 0; k < n_bins; ++k) {
-    const int64_t lo = cut[k], hi = cut[k + 1];
-    while (u < n_units && start[u + 1] <= lo) ++u;
-    for (int64_t v = u; v < n_units && start[v] < hi; ++v) {
-      const int64_t a = std::max(lo, start[v]), z = std::min(hi, start[v + 1]);
-      if (a >= z) continue;
-      tg_work_item w;
-      w.pt_base = base[v];
-      w.b = (int32_t)(v / H);
-      w.kv_head = (int32_t)(v % H);
-      w.slot = slot_of[(int64_t)layer * H + w.kv_head];
-      w.tok_begin = (int32_t)((a - start[v]) * P);
-      w.tok_end = (int32_t)std::min((z - start[v]) * P, len[v]);
-      w.out_idx = pieces[v] == 1 ? -1 : (int32_t)(unit_partial_base[v] + seen[v]);
-      ++seen[v];
-      items[it++] = w;
+  for (size_t si = 0; si < segs.size(); ++si) {
+    const FillSegment& sg = segs[si];
+    const Cut& c = cuts[si];
+    const int64_t nu = (int64_t)sg.units.size();
+    for (int64_t k = 0, i = 0; k < sg.n_bins; ++k) {
+      const int64_t lo = c.cut[k], hi = c.cut[k + 1];
+      while (i < nu && c.start[i + 1] <= lo) ++i;
+      for (int64_t j = i; j < nu && c.start[j] < hi; ++j) {
+        const int64_t a = std::max(lo, c.start[j]), z = std::min(hi, c.start[j + 1]);
+        if (a >= z) continue;
+        const int64_t v = sg.units[j];
+        tg_work_item w;
+        w.pt_base = base[v];
+        w.b = (int32_t)(v / H);
+        w.kv_head = (int32_t)(v % H);
+        w.slot = slot_of[(int64_t)layer * H + w.kv_head];
+        w.tok_begin = (int32_t)((a - c.start[j]) * P);
+        w.tok_end = (int32_t)std::min((z - c.start[j]) * P, len[v]);
+        w.out_idx = pieces[v] == 1 ? -1 : (int32_t)(unit_partial_base[v] + seen[v]);
+        ++seen[v];
+        items[it++] = w;
+      }
+      bin_offsets[++bin] = (int32_t)it;
     }
-    bin_offsets[k + 1] = (int32_t)it;
   }
   return TG_OK;
 }
@@ -282,16 +308,22 @@ static int32_t build_plan_core(const tg_geometry* geom, int32_t batch, int32_t l
   const int64_t P = geom->page_size;
   if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
   if (layer < 0 || layer >= L) return fail(TG_ERR_INVALID_ARG, "layer %d out of range", layer);
-  if (mode != TG_PLAN_AOT && mode != TG_PLAN_NAIVE && mode != TG_PLAN_UNIFORM && mode != TG_PLAN_AOT_FILL)
+  if (mode != TG_PLAN_AOT && mode != TG_PLAN_NAIVE && mode != TG_PLAN_UNIFORM && mode != TG_PLAN_AOT_FILL &&
+      mode != TG_PLAN_SPLIT_MAP)
     return fail(TG_ERR_INVALID_ARG, "unknown plan mode %d", mode);
-  if (mode != TG_PLAN_NAIVE && n_bins < 1) return fail(TG_ERR_INVALID_ARG, "n_bins must be >= 1");
+  if (mode != TG_PLAN_NAIVE && mode != TG_PLAN_SPLIT_MAP && n_bins < 1)
+    return fail(TG_ERR_INVALID_ARG, "n_bins must be >= 1");
   if (mode == TG_PLAN_AOT && split_target < 1) return fail(TG_ERR_INVALID_ARG, "split_target must be >= 1");
-  if (bin_weights && mode != TG_PLAN_AOT_FILL)
-    return fail(TG_ERR_INVALID_ARG, "bin_weights apply to TG_PLAN_AOT_FILL only");
-  if (bin_weights)
-    for (int32_t k = 0; k < n_bins; ++k)
+  if (bin_weights && mode != TG_PLAN_AOT_FILL && mode != TG_PLAN_SPLIT_MAP)
+    return fail(TG_ERR_INVALID_ARG, "bin_weights apply to TG_PLAN_AOT_FILL and TG_PLAN_SPLIT_MAP only");
+  if (mode == TG_PLAN_SPLIT_MAP && !bin_weights)
+    return fail(TG_ERR_INVALID_ARG, "TG_PLAN_SPLIT_MAP needs the layer's split map row in bin_weights");
+  if (bin_weights) {
+    const int32_t nw = mode == TG_PLAN_SPLIT_MAP ? geom->num_kv_heads / geom->heads_per_group : n_bins;
+    for (int32_t k = 0; k < nw; ++k)
       if (bin_weights[k] < 1 || bin_weights[k] > 65535)
         return fail(TG_ERR_INVALID_ARG, "bin_weights[%d] = %d outside [1, 65535]", k, bin_weights[k]);
+  }
   const int64_t n_units = (int64_t)batch * H;
   // lengths of this layer, checked against the capacity of their table
   std::vector<int64_t> len(n_units), base(n_units);
@@ -311,9 +343,24 @@ static int32_t build_plan_core(const tg_geometry* geom, int32_t batch, int32_t l
       base[u] = pt_offsets[t];
       W += len[u];
     }
-  if (mode == TG_PLAN_AOT_FILL)
-    return fill_plan(L, G, H, P, batch, layer, len, base, slot_of, n_bins, bin_weights, items, item_capacity,
-                     bin_offsets, bin_capacity, unit_splits, unit_partial_base, num_items, num_bins, num_partials);
+  if (mode == TG_PLAN_AOT_FILL || mode == TG_PLAN_SPLIT_MAP) {
+    std::vector<FillSegment> segs;
+    if (mode == TG_PLAN_AOT_FILL) {
+      FillSegment sg{std::vector<int64_t>(n_units), n_bins, bin_weights};
+      for (int64_t u = 0; u < n_units; ++u) sg.units[u] = u;
+      segs.push_back(std::move(sg));
+    } else {
+      for (int g = 0; g < G; ++g) {
+        FillSegment sg{{}, bin_weights[g], nullptr};
+        for (int b = 0; b < batch; ++b)
+          for (int h = 0; h < H; ++h)
+            if (group_of[(int64_t)layer * H + h] == g) sg.units.push_back((int64_t)b * H + h);
+        segs.push_back(std::move(sg));
+      }
+    }
+    return segmented_fill(H, P, layer, len, base, slot_of, segs, items, item_capacity, bin_offsets, bin_capacity,
+                          unit_splits, unit_partial_base, num_items, num_bins, num_partials);
+  }
   // split counts
   std::vector<int64_t> splits(n_units);
   int64_t total = 0, nparts = 0;

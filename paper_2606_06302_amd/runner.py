@@ -105,9 +105,15 @@ class DecodeSession:
         # timed: this is the host planning cost the paper's Table 1 measures for a runtime planner
         t0 = time.perf_counter()
         mode = self.mode | (tg.TG_PLAN_OPEN_END if self.open_end else 0)
+        if self.mode == tg.TG_PLAN_SPLIT_MAP:
+            # Algorithm 1 on the static budgets with N_CTA = n_bins: one row of S per layer
+            S = tg.tg_split_map(g, self.wl.budget, self.t.perm, self.n_bins)
+            weights = {l: S[l] for l in self.layers}
+        else:
+            weights = {l: self.bin_weights for l in self.layers}
         self.plans = {l: tg.tg_build_plan(g, B, l, self.t.kv_len, self.t.pt_offsets, self.t.group_of,
                                           self.t.slot_of, mode, self.n_bins, self.split_target,
-                                          bin_weights=self.bin_weights) for l in self.layers}
+                                          bin_weights=weights[l]) for l in self.layers}
         self.plan_build_us = (time.perf_counter() - t0) * 1e6
         self.dplans = {l: upload_plan(g, B, p, self.device) for l, p in self.plans.items()}
 

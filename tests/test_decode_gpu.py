@@ -255,3 +255,17 @@ def test_xcd_calibrated_fill_plan_matches_oracle():
     for l in range(2):
         compare_layer(s, l, what=f"calibrated layer {l}")
     assert torch.allclose(s.out.float(), ref.float(), atol=2e-2, rtol=0)
+
+
+def test_split_map_plan_vs_oracle():
+    """Algorithm 1's split map executed as is (S[l][g] workers per head group) gives the same attention."""
+    _gpu()
+    g = Geometry(2, 8, 32, 128, 16, 2)
+    wl = custom(321, g, 6, "bf16", (100, 4000))
+    say(f"split-map plan: ctx {wl.ctx_len.tolist()}")
+    s = DecodeSession(wl, mode=tg.TG_PLAN_SPLIT_MAP, n_bins=128, fill="host")
+    s.run_step()
+    torch.cuda.synchronize()
+    for l in range(g.num_layers):
+        assert s.plans[l]["num_bins"] == int(tg.tg_split_map(g, wl.budget, s.t.perm, 128)[l].sum())
+        compare_layer(s, l, what=f"split map layer {l}")

@@ -449,3 +449,36 @@ def test_append_launch_validation_on_host():
         with pytest.raises(tg.TangramError) as e:
             tg.tg_append(args)
         assert e.value.code == tg.TG_ERR_INVALID_ARG, kw
+
+
+@settings(max_examples=40, deadline=None)
+@given(st.data())
+def test_split_map_plan_bit_exact(data):
+    H = data.draw(st.sampled_from([2, 4, 8]))
+    Hp = data.draw(st.sampled_from([h for h in (1, 2, 4, 8) if H % h == 0]))
+    L = data.draw(st.integers(1, 3))
+    P = data.draw(st.sampled_from([1, 16]))
+    B = data.draw(st.integers(1, 6))
+    geom = Geometry(L, H, H, 64, P, Hp)
+    rng = np.random.default_rng(data.draw(st.integers(0, 2**31)))
+    budget = rng.uniform(0.01, 1.0, size=(L, H))
+    ratio = np.clip(budget[None] + rng.uniform(-0.05, 0.05, size=(B, L, H)), 0.01, 1.0)
+    ctx = rng.integers(1, 3000, size=B).astype(np.int32)
+    perm, gof, sof = tg.tg_cluster_heads(geom, budget)
+    res = tg.tg_reserve(geom, ctx, ratio, None, gof, np.arange(10**6, dtype=np.int32), 10**6)
+    n_cta = data.draw(st.sampled_from([1, 7, 256, 1024]))
+    S = tg.tg_split_map(geom, budget, perm, n_cta)
+    flag = data.draw(st.sampled_from([0, tg.TG_PLAN_OPEN_END]))
+    for layer in range(L):
+        pl = tg.tg_build_plan(geom, B, layer, res["kv_len"], res["pt_offsets"], gof, sof,
+                              tg.TG_PLAN_SPLIT_MAP | flag, 1, 1, bin_weights=S[layer])
+        opl = oracle.partition_plan(res["kv_len"], res["pt_offsets"], gof, sof, layer, num_layers=L,
+                                    num_groups=H // Hp, page_size=P, mode=oracle.MODE_SPLIT_MAP, bin_weights=S[layer],
+                                    open_end=bool(flag))
+        assert _items_as_tuples(pl["items"]) == opl["items"]
+        assert pl["bin_offsets"].tolist() == opl["bin_offsets"].tolist()
+        assert np.array_equal(pl["unit_splits"], opl["unit_splits"])
+        assert np.array_equal(pl["unit_partial_base"], opl["unit_partial_base"])
+        assert pl["num_bins"] == int(S[layer].sum())
+    with pytest.raises(tg.TangramError):
+        tg.tg_build_plan(geom, B, 0, res["kv_len"], res["pt_offsets"], gof, sof, tg.TG_PLAN_SPLIT_MAP, 1, 1)

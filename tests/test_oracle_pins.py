@@ -972,3 +972,67 @@ def test_append_without_room_writes_nothing():
     assert full == [(0, 0), (0, 2), (1, 0), (1, 2)]
     assert (live - res["kv_len"]).tolist() == [[[0, 1, 0, 1]], [[0, 1, 0, 1]]]
     assert int((out != 0).sum()) == 2 * 2 * 2 * 64      # two heads of two requests, a K and a V row each
+
+
+# ------------------------------------------ Algorithm 1's split map executed as is
+
+def test_split_map_plan_config1_hand():
+    """Config 1 at N_CTA = 8: S = [2, 6].  Group {3,2}: units b0h2 (8 pages), b0h3 (4), b1h2 (8), b1h3 (4),
+    24 pages in 2 bins of 12.  Group {1,0}: b0h0 (32), b0h1 (16), b1h0 (32), b1h1 (16), 96 pages in 6 bins of
+    16, so each 512-token head is split in two (partials 0-1 and 2-3)."""
+    budget, ratio, ctx = cfg1_arrays()
+    perm, gof, sof = oracle.cluster_heads(budget, 2)
+    res = oracle.reserve(ratio, ctx, gof, 2, 16, np.arange(100))
+    S = oracle.split_map(budget, perm, 2, 8)
+    assert S.tolist() == [[2, 6]]
+    pl = oracle.partition_plan(res["kv_len"], res["offsets"], gof, sof, 0, num_layers=1, num_groups=2, page_size=16,
+                               mode=oracle.MODE_SPLIT_MAP, bin_weights=S[0])
+    # (pt_base, b, h, slot, t0, t1, out_idx); group 0 tables start at 0 and 40, group 1 at 8 and 48
+    assert pl["items"] == [(0, 0, 2, 1, 0, 128, -1), (0, 0, 3, 0, 0, 64, -1),
+                           (40, 1, 2, 1, 0, 128, -1), (40, 1, 3, 0, 0, 64, -1),
+                           (8, 0, 0, 1, 0, 256, 0), (8, 0, 0, 1, 256, 512, 1), (8, 0, 1, 0, 0, 256, -1),
+                           (48, 1, 0, 1, 0, 256, 2), (48, 1, 0, 1, 256, 512, 3), (48, 1, 1, 0, 0, 256, -1)]
+    assert pl["bin_offsets"].tolist() == [0, 2, 4, 5, 6, 7, 8, 9, 10]
+    assert pl["bin_load"].tolist() == [192, 192] + [256] * 6
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_split_map_plan_with_one_group_is_the_fill_plan(seed):
+    """With H_p = H there is one group per layer, whose S bins cut the whole layer: the sequential-fill plan
+    with S bins (two separately written constructions)."""
+    rng = np.random.default_rng(seed)
+    L, H, B = 2, 4, 3
+    budget = rng.uniform(0.05, 1.0, size=(L, H))
+    ratio = np.clip(budget[None] + rng.uniform(-0.03, 0.03, size=(B, L, H)), 0.02, 1.0)
+    perm, gof, sof = oracle.cluster_heads(budget, H)
+    res = oracle.reserve(ratio, rng.integers(10, 900, size=B), gof, 1, 8, np.arange(10**4))
+    for n_cta in (1, 5, 37):
+        S = oracle.split_map(budget, perm, H, n_cta)
+        for l in range(L):
+            kw = dict(num_layers=L, num_groups=1, page_size=8)
+            a = oracle.partition_plan(res["kv_len"], res["offsets"], gof, sof, l, mode=oracle.MODE_SPLIT_MAP,
+                                      bin_weights=S[l], **kw)
+            b = oracle.partition_plan(res["kv_len"], res["offsets"], gof, sof, l, mode=oracle.MODE_FILL,
+                                      n_bins=int(S[l, 0]), **kw)
+            assert a["items"] == b["items"] and a["bin_offsets"].tolist() == b["bin_offsets"].tolist()
+
+
+def test_split_map_plan_decodes_exactly():
+    rng = np.random.default_rng(12)
+    g = Geometry(1, 4, 8, 8, 4, 2)
+    B = 3
+    budget = rng.uniform(0.05, 1.0, size=(1, 4))
+    ratio = np.clip(budget[None] + rng.uniform(-0.03, 0.03, size=(B, 1, 4)), 0.02, 1.0)
+    perm, gof, sof = oracle.cluster_heads(budget, 2)
+    res = oracle.reserve(ratio, rng.integers(5, 90, size=B), gof, 2, 4, rng.permutation(300))
+    pool = rng.standard_normal((300, 2, 2, 4, 8))
+    q = rng.standard_normal((B, 8, 8))
+    S = oracle.split_map(budget, perm, 2, 11)
+    pl = oracle.partition_plan(res["kv_len"], res["offsets"], gof, sof, 0, num_layers=1, num_groups=2, page_size=4,
+                               mode=oracle.MODE_SPLIT_MAP, bin_weights=S[0])
+    ref, _ = oracle.decode_attention(q, pool, 0, geom=g, batch=B, kv_len=res["kv_len"], offsets=res["offsets"],
+                                     pages=res["pages"], group_of=gof, slot_of=sof)
+    got, _ = oracle.decode_by_plan(q, pool, 0, pl, geom=g, batch=B, offsets=res["offsets"], pages=res["pages"],
+                                   group_of=gof, slot_of=sof)
+    assert np.abs(got - ref).max() < 1e-12
+    assert len(pl["bin_offsets"]) - 1 == int(S.sum())
