@@ -35,6 +35,13 @@ in the paper's order and notation:
                         workgroups: the same idea as the decode partition
                         (cost known from the retained lengths before the step,
                         Section 4.3), longest-processing-time onto the XCDs.
+  * implicit_ratios   - calibration (Section 4.1): the per-head share each head
+  * calibrate_budget    gets from the layer-wide top-ceil(rho*H*N) selection
+                        (Eq. 3) on a sample, and B = min(1, mu + alpha*sigma)
+                        over the samples.
+  * release_requests  - request lifecycle: a finished request's pages return to
+  * concat_tables       the free list and the surviving tables are compacted;
+                        newly admitted requests' tables are appended.
   * memory_footprint  - KV slots each paging scheme allocates for the same
                         retained lengths: the uncompressed cache, a monolithic
                         page table spanning all L x H heads (PagedAttention,
@@ -58,6 +65,11 @@ Readings of points the paper leaves open (each also listed in the design doc):
   - Softmax scale 1/sqrt(d) unless given.
   - A prefill chunk sees all of its head's compressed history and, causally
     and inclusively, its own (uncompressed) keys.
+  - Eq. 3's global selection ranks like Top() (descending score, NaN last, -0
+    equal to +0) with ties broken by the lower flattened index h*N + t.
+  - sigma is the population standard deviation over the samples; mu and
+    sigma are accumulated in sample order; a budget below `floor` is raised
+    to it (the method needs B > 0).
   - Chunk-wise compression keeps, after the first x context tokens, ceil(r*x)
     entries of a head (Eq. 4 on the prefix), capped by the head's reserved
     length; a chunk keeps the difference, so the counts of all chunks of a
@@ -766,3 +778,85 @@ def compress_plan(ratio, capacity, chunk_start, chunk_tokens, offsets, group_of,
             for r0 in range(0, cnt, rows_per_item):
                 items.append((base, b, h, int(slot_of[layer, h]), n, c0, cnt, r0, min(cnt, r0 + rows_per_item)))
     return items, cursor, count
+
+
+# ------------------------------------------------ calibration (Section 4.1, Eq. 3)
+
+def implicit_ratios(scores, rho):
+    """Implicit per-head retention ratio of one sample under non-uniform
+    compression (Eq. 3): per layer, the top ceil(rho*H*N) of the H*N flattened
+    scores are kept (descending score, NaN last, -0 equal to +0, ties to the
+    lower flattened index h*N + t); head h's ratio is its kept count / N.
+    scores [L][H][N]; returns ([L][H] float64 ratios, [L][H] int counts)."""
+    scores = np.asarray(scores)
+    L, H, N = scores.shape
+    if not (0.0 < rho <= 1.0) or N < 1:
+        raise OracleError("rho must be in (0, 1] and N >= 1")
+    k = math.ceil(float(rho) * (H * N))
+    counts = np.zeros((L, H), dtype=np.int64)
+    for l in range(L):
+        def rank_key(i):
+            v = float(scores[l, i // N, i % N])
+            return (1, 0.0, i) if math.isnan(v) else (0, -v, i)
+        for i in sorted(range(H * N), key=rank_key)[:k]:
+            counts[l, i // N] += 1
+    ratios = np.zeros((L, H), dtype=np.float64)
+    for l in range(L):
+        for h in range(H):
+            ratios[l, h] = int(counts[l, h]) / N
+    return ratios, counts
+
+
+def calibrate_budget(ratios, alpha, floor):
+    """B_{l,h} = min(1, mu + alpha * sigma) over S samples of implicit ratios
+    ([S][L][H]), mu the mean and sigma the population standard deviation, both
+    accumulated in sample order; raised to `floor` when below it."""
+    ratios = np.asarray(ratios, dtype=np.float64)
+    S, L, H = ratios.shape
+    if S < 1 or not (0.0 < floor <= 1.0) or alpha < 0:
+        raise OracleError("need S >= 1, floor in (0, 1], alpha >= 0")
+    B = np.zeros((L, H), dtype=np.float64)
+    for l in range(L):
+        for h in range(H):
+            acc = 0.0
+            for s_ in range(S):
+                acc += float(ratios[s_, l, h])
+            mu = acc / S
+            var = 0.0
+            for s_ in range(S):
+                dev = float(ratios[s_, l, h]) - mu
+                var += dev * dev
+            sigma = math.sqrt(var / S)
+            b = mu + float(alpha) * sigma
+            B[l, h] = max(float(floor), min(1.0, b))
+    return B
+
+
+# ------------------------------------------------------------ request lifecycle
+
+def release_requests(offsets, pages, finished, num_layers, num_groups):
+    """Finished requests give their pages back: returns (freed page ids in table
+    order, offsets and pages of the surviving requests' tables, compacted in
+    request order; page ids are unchanged)."""
+    Bn = len(finished)
+    per = num_layers * num_groups
+    freed, kept_pages, new_offsets = [], [], []
+    for b in range(Bn):
+        lo, hi = int(offsets[b * per]), int(offsets[(b + 1) * per])
+        if finished[b]:
+            freed.extend(int(p) for p in pages[lo:hi])
+        else:
+            shift = len(kept_pages) - lo
+            for t in range(per):
+                new_offsets.append(int(offsets[b * per + t]) + shift)
+            kept_pages.extend(int(p) for p in pages[lo:hi])
+    new_offsets.append(len(kept_pages))
+    return np.array(freed, dtype=np.int64), np.array(new_offsets, dtype=np.int64), np.array(kept_pages, dtype=np.int64)
+
+
+def concat_tables(offsets_a, pages_a, offsets_b, pages_b):
+    """The tables of batch b appended after those of batch a (request order a, then b)."""
+    n = int(offsets_a[-1])
+    offsets = [int(x) for x in offsets_a[:-1]] + [int(x) + n for x in offsets_b]
+    return np.array(offsets, dtype=np.int64), np.concatenate([np.asarray(pages_a, dtype=np.int64),
+                                                              np.asarray(pages_b, dtype=np.int64)])

@@ -1036,3 +1036,107 @@ def test_split_map_plan_decodes_exactly():
                                    group_of=gof, slot_of=sof)
     assert np.abs(got - ref).max() < 1e-12
     assert len(pl["bin_offsets"]) - 1 == int(S.sum())
+
+
+# ------------------------------------------------ calibration and request lifecycle
+
+def test_implicit_ratios_hand():
+    """L = 1, H = 2, N = 4, rho = 0.5: the layer keeps ceil(0.5*8) = 4 of the flattened scores.  0.9 (h0 t0) and
+    0.8 (h1 t1) come first; three entries tie at 0.5 (h0 t2, h0 t3, h1 t0) and the two lower flattened indices
+    (both in head 0) win, so head 0 keeps 3 of 4 and head 1 keeps 1 of 4."""
+    sc = np.array([[[0.9, 0.1, 0.5, 0.5], [0.5, 0.8, 0.0, -0.0]]], dtype=np.float32)
+    r, c = oracle.implicit_ratios(sc, 0.5)
+    assert c.tolist() == [[3, 1]] and r.tolist() == [[0.75, 0.25]]
+
+
+def test_implicit_ratios_reduce_to_uniform_when_heads_agree():
+    """Identical heads with distinct scores: the global selection keeps rho*N entries of every head when rho*H*N
+    is a multiple of H (the uniform compression of Eq. 2)."""
+    rng = np.random.default_rng(2)
+    N, H = 40, 4
+    row = rng.permutation(N).astype(np.float32)
+    sc = np.broadcast_to(row, (1, H, N)).copy()
+    for rho in (0.25, 0.5, 0.75, 1.0):
+        r, c = oracle.implicit_ratios(sc, rho)
+        assert c.tolist() == [[int(rho * N)] * H]
+        kept = oracle.top_entries(row, int(rho * N))
+        assert set(kept) == set(np.argsort(-row)[: int(rho * N)].tolist())
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_implicit_ratios_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    for _ in range(20):
+        L, H, N = 1, int(rng.integers(1, 4)), int(rng.integers(1, 7))
+        sc = _tiny_scores(rng, L * H * N).reshape(L, H, N)
+        rho = float(rng.choice([0.1, 0.3, 0.5, 1.0, rng.uniform(0.01, 1.0)]))
+        r, c = oracle.implicit_ratios(sc, rho)
+        k = math.ceil(rho * H * N)
+        assert int(c.sum()) == k
+        flat = sc.reshape(-1)
+        # some kept set of these per-head counts must beat every dropped entry: check via the sorted order
+        order = sorted(range(H * N), key=lambda i: (1, 0.0, i) if math.isnan(float(flat[i])) else (0, -float(flat[i]), i))
+        kept = set(order[:k])
+        assert all(_beats(flat, t, u) for t in kept for u in range(H * N) if u not in kept)
+        assert [sum(1 for i in kept if i // N == h) for h in range(H)] == c[0].tolist()
+
+
+def test_calibrated_budget_hand_and_cases():
+    # two samples 0.2 and 0.4: mu = 0.3, population sigma = 0.1, alpha = 2 -> 0.5 (the sample standard deviation
+    # would give 0.583)
+    B = oracle.calibrate_budget(np.array([[[0.2]], [[0.4]]]), 2.0, 0.01)
+    assert abs(B[0, 0] - 0.5) < 1e-15
+    samples = np.array([[[0.1, 0.9, 0.0]], [[0.3, 0.95, 0.0]], [[0.2, 0.85, 0.0]]])
+    B0 = oracle.calibrate_budget(samples, 0.0, 0.01)
+    assert np.allclose(B0, [[0.2, 0.9, 0.01]], rtol=0, atol=1e-15)          # alpha 0: the mean; a never-kept head: floor
+    assert oracle.calibrate_budget(samples, 3.0, 0.01)[0, 1] == 1.0          # 0.9 + 3 * 0.0408 > 1: capped
+    one = oracle.calibrate_budget(samples[:1], 3.0, 0.01)
+    assert one.tolist() == [[0.1, 0.9, 0.01]]                                # one sample: sigma = 0
+
+
+def test_calibrated_budgets_sum_to_the_global_budget():
+    """With alpha = 0 and one sample, the per-head budgets keep the layer's global count up to rounding:
+    sum_h ceil(B_h * N) lies within [ceil(rho*H*N), ceil(rho*H*N) + H]."""
+    rng = np.random.default_rng(8)
+    for _ in range(10):
+        L, H, N = 2, 4, int(rng.integers(20, 200))
+        sc = rng.standard_normal((L, H, N)).astype(np.float32) * rng.uniform(0.2, 3.0, size=(1, H, 1))
+        rho = float(rng.uniform(0.1, 0.9))
+        r, _ = oracle.implicit_ratios(sc, rho)
+        B = oracle.calibrate_budget(r[None], 0.0, 1e-9)
+        k = math.ceil(rho * H * N)
+        for l in range(L):
+            tot = sum(math.ceil(float(B[l, h]) * N) for h in range(H))
+            assert k <= tot <= k + H
+
+
+def test_release_and_readmit_config1_hand():
+    budget, ratio, ctx = cfg1_arrays()
+    _, gof, _ = oracle.cluster_heads(budget, 2)
+    res = oracle.reserve(ratio, ctx, gof, 2, 16, np.arange(100))
+    assert res["offsets"].tolist() == [0, 8, 40, 48, 80]
+    freed, off, pages = oracle.release_requests(res["offsets"], res["pages"], [True, False], 1, 2)
+    assert freed.tolist() == list(range(40)) and off.tolist() == [0, 8, 40] and pages.tolist() == list(range(40, 80))
+    freed, off, pages = oracle.release_requests(res["offsets"], res["pages"], [False, True], 1, 2)
+    assert freed.tolist() == list(range(40, 80)) and off.tolist() == [0, 8, 40] and pages.tolist() == list(range(40))
+    # readmit the released request from the freed pages: the batch's tables hold every page once again
+    again = oracle.reserve(ratio[1:], ctx[1:], gof, 2, 16, freed)
+    o2, p2 = oracle.concat_tables(off, pages, again["offsets"], again["pages"])
+    assert o2.tolist() == res["offsets"].tolist() and sorted(p2.tolist()) == list(range(80))
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_release_invariants(seed):
+    rng = np.random.default_rng(seed)
+    L, H, B = 2, 4, 6
+    budget = rng.uniform(0.05, 1.0, size=(L, H))
+    _, gof, _ = oracle.cluster_heads(budget, 2)
+    ratio = np.broadcast_to(budget, (B, L, H))
+    ctx = rng.integers(1, 500, size=B)
+    res = oracle.reserve(ratio, ctx, gof, 2, 16, rng.permutation(10**4))
+    fin = rng.random(B) < 0.5
+    freed, off, pages = oracle.release_requests(res["offsets"], res["pages"], fin, L, 2)
+    assert sorted(freed.tolist() + pages.tolist()) == sorted(res["pages"].tolist())
+    survivors = [b for b in range(B) if not fin[b]]
+    sizes = np.diff(res["offsets"]).reshape(B, L * 2)
+    assert np.diff(off).tolist() == sizes[survivors].reshape(-1).tolist()
