@@ -18,6 +18,7 @@ divided by the measured step time.
     python bench.py --compress-chunk C     # chunk compression alone, chunk of C tokens
     python bench.py --memory               # host only: memory reclaimed per paging scheme
     python bench.py --plan-reuse           # planning cost vs decode step, 28 to 80 layers
+    python bench.py --lifecycle            # host only: calibration, reservation threads, release
     python bench.py --copy-probe BYTES     # plain copy kernel, for counter calibration
 """
 from __future__ import annotations
@@ -425,6 +426,85 @@ def bench_plan_reuse(args):
                       "data": "synthetic", "steps": steps, "warmup": warmup, "rows": rows}), flush=True)
 
 
+def bench_lifecycle(args):
+    """Host only: budget calibration from synthetic retention samples (B = min(1, mu + 2 sigma) over 50
+    pilot samples, checked on 50 held-out ones), the reservation at one head per group with 1 and 16
+    host threads, and releasing / readmitting a quarter of a batch."""
+    sys.path.insert(0, ROOT)
+    from paper_2606_06302_amd import tangram as tg
+    from workloads import Geometry, config, retention_scores
+    out = {"metric": "calibration and request lifecycle (host)", "data": "synthetic"}
+    # calibration: a Llama-3.1-8B-shaped layer stack, 16384-token pilot contexts, rho = 0.3
+    L, H, N, rho, alpha, n_pilot = 32, 8, 16384, 0.3, 2.0, 50
+    t_ratio, pilot = 0.0, []
+    for s_ in range(n_pilot):
+        sc = retention_scores(77, s_, L, H, N)
+        t0 = time.perf_counter()
+        r, _ = tg.tg_implicit_ratios(sc, rho)
+        t_ratio += time.perf_counter() - t0
+        pilot.append(r)
+    t0 = time.perf_counter()
+    B = tg.tg_calibrate_budget(np.stack(pilot), alpha, 1.0 / N)
+    t_cal = time.perf_counter() - t0
+    over, excess, reserved = 0, [], []
+    for s_ in range(n_pilot, 2 * n_pilot):
+        r, _ = tg.tg_implicit_ratios(retention_scores(77, s_, L, H, N), rho)
+        over += int((r > B).sum())
+        excess.extend((r[r > B] - B[r > B]).tolist())
+    for l in range(L):
+        reserved.append(sum(math.ceil(float(B[l, h]) * N) for h in range(H)) / math.ceil(rho * H * N))
+    out["calibration"] = {
+        "layers": L, "kv_heads": H, "pilot_tokens": N, "rho": rho, "alpha": alpha, "pilot_samples": n_pilot,
+        "implicit_ratio_ms_per_sample": round(t_ratio / n_pilot * 1e3, 2), "calibrate_ms": round(t_cal * 1e3, 3),
+        "budget_mean": round(float(B.mean()), 4), "budget_min": round(float(B.min()), 4),
+        "budget_max": round(float(B.max()), 4),
+        "heldout_over_budget_frac": round(over / (n_pilot * L * H), 5),
+        "heldout_mean_excess_ratio": round(float(np.mean(excess)) if excess else 0.0, 5),
+        "reserved_over_global_budget": round(float(np.mean(reserved)), 4)}
+    log(f"[bench] calibration: {out['calibration']}")
+    # reservation at one head per group (32768 tables of the 64-layer decode workload)
+    wl = config(3)
+    g = wl.geom
+    geom = Geometry(g.num_layers, g.num_kv_heads, g.num_q_heads, g.head_dim, g.page_size, 1)
+    _, gof, _ = tg.tg_cluster_heads(geom, wl.budget)
+    need = tg.tg_reserve(geom, wl.ctx_len, wl.ratio, None, gof, np.zeros(0, np.int32), 0,
+                         size_query=True)["pages_needed"]
+    free = np.random.default_rng(0).permutation(need).astype(np.int32)
+    res_ms = {}
+    for thr in (1, 16):
+        os.environ["TG_HOST_THREADS"] = str(thr)
+        best = []
+        for _ in range(4):
+            t0 = time.perf_counter()
+            res = tg.tg_reserve(geom, wl.ctx_len, wl.ratio, None, gof, free, need)
+            best.append(time.perf_counter() - t0)
+        res_ms[thr] = round(min(best) * 1e3, 2)
+    os.environ.pop("TG_HOST_THREADS", None)
+    t0 = time.perf_counter()
+    tg.tg_reserve(geom, wl.ctx_len, wl.ratio, None, gof, free, need, size_query=True)
+    sq_ms = (time.perf_counter() - t0) * 1e3
+    # a quarter of the batch finishes; the same number of requests is admitted from the freed pages
+    fin = np.zeros(wl.batch, dtype=bool)
+    fin[np.random.default_rng(1).permutation(wl.batch)[: wl.batch // 4]] = True
+    t0 = time.perf_counter()
+    freed, off, pages = tg.tg_release_requests(geom, res["pt_offsets"], res["pt_pages"], fin)
+    t_rel = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    again = tg.tg_reserve(geom, wl.ctx_len[fin], wl.ratio[fin], None, gof, freed, need)
+    off2, pages2 = tg.tg_concat_tables(geom, off, pages, again["pt_offsets"], again["pt_pages"])
+    t_adm = time.perf_counter() - t0
+    out["reservation"] = {"workload": wl.name, "heads_per_group": 1, "tables": int(wl.batch * g.num_layers *
+                          g.num_kv_heads), "pages": int(need), "size_query_ms": round(sq_ms, 3),
+                          "reserve_ms_1_thread": res_ms[1], "reserve_ms_16_threads": res_ms[16],
+                          "host_threads_available": os.cpu_count()}
+    out["lifecycle"] = {"released_requests": int(fin.sum()), "released_pages": int(len(freed)),
+                        "release_ms": round(t_rel * 1e3, 2), "readmit_and_concat_ms": round(t_adm * 1e3, 2),
+                        "pages_conserved": bool(sorted(pages2.tolist()) == sorted(res["pt_pages"].tolist()))}
+    log(f"[bench] reservation: {out['reservation']}")
+    log(f"[bench] lifecycle: {out['lifecycle']}")
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -445,6 +525,8 @@ def main():
     ap.add_argument("--rows-per-item", type=int, default=0)
     ap.add_argument("--plan-reuse", action="store_true",
                     help="planning cost against the decode step (append + attention) for 28 to 80 layers")
+    ap.add_argument("--lifecycle", action="store_true",
+                    help="host only: budget calibration, reservation threads, release and readmission")
     ap.add_argument("--memory", action="store_true",
                     help="host-only: memory reclaimed by ragged paging for each heads-per-group and grouping")
     ap.add_argument("--free-order", default="shuffled", choices=["shuffled", "sequential"],
@@ -459,6 +541,8 @@ def main():
         return
     if args.memory:
         return bench_memory(args)
+    if args.lifecycle:
+        return bench_lifecycle(args)
 
     import torch
     sys.path.insert(0, ROOT)

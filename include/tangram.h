@@ -27,7 +27,9 @@
  *   - Arguments are validated on the host before anything is written or
  *     enqueued.  On error nothing is written past what the error's
  *     description says, and no page is consumed.
- *   - Host integer calls are pure, deterministic and thread-safe.  The only
+ *   - Host integer calls are pure, deterministic and thread-safe (tg_reserve
+ *     checks and copies large page lists on up to 16 helper threads, or
+ *     TG_HOST_THREADS; results do not depend on the thread count).  The only
  *     library state is a per-device cache of compute-unit counts.
  *   - Physical page layout (Section 4.2.1: a page holds H_p x 2 x P x d
  *     elements for the H_p heads of one group in one layer):
@@ -506,6 +508,45 @@ typedef struct {
 
 int32_t tg_memory_footprint(const tg_geometry* geom, int32_t batch, const int32_t* ctx_len, const double* ratio,
                             const double* budget, const int32_t* group_of, tg_footprint* out);
+
+/* ------------------------------------------------ 7. budget calibration
+ * Section 4.1 (budget calibration) and Eq. 3, host, offline.
+ * 7a. tg_implicit_ratios: the per-head retention ratio one sample gets under
+ * non-uniform compression.  For every layer the top ceil(rho * H * N) of the
+ * H*N flattened scores [H][N] are kept (one fp64 multiply, then ceil); the
+ * ranking is by descending score, -0.0 equal to +0.0, NaN below every number,
+ * ties to the lower flattened index h*N + t.  ratios[l][h] = kept count of
+ * head h / N (fp64 division), counts[l][h] the count (or NULL).
+ *   scores [L][H][N] float32; rho in (0, 1]; L, H, N >= 1, H*N < 2^31.
+ * 7b. tg_calibrate_budget: B[l][h] = min(1, mu + alpha * sigma) over S
+ * samples of implicit ratios [S][L][H], mu the mean and sigma the population
+ * standard deviation (both summed in sample order, fp64), raised to floor when
+ * below it (a head must keep at least some entries).  alpha >= 0, floor in
+ * (0, 1].  All host memory.  Errors: TG_ERR_INVALID_ARG (nothing written). */
+int32_t tg_implicit_ratios(int32_t num_layers, int32_t num_heads, int32_t n_tokens, const float* scores, double rho,
+                           double* ratios, int32_t* counts);
+int32_t tg_calibrate_budget(int32_t samples, int32_t num_layers, int32_t num_heads, const double* ratios,
+                            double alpha, double floor, double* budget);
+
+/* ------------------------------------------------ 8. request lifecycle
+ * Section 4.1 (pages are reserved once at admission) and Section 4.2.3 (the
+ * Vectorized Block Table of a batch).  Host, integer.
+ * 8a. tg_release_requests: requests with finished[b] != 0 give their pages
+ * back: freed receives them in table order (request, layer, group, page);
+ * new_offsets / new_pages receive the surviving requests' tables, compacted
+ * in request order (page ids unchanged; new_offsets has S*L*G + 1 entries for
+ * S survivors).  Pass freed = NULL and new_pages = NULL for a size query
+ * (num_freed, num_kept, num_survivors are always written).
+ * 8b. tg_concat_tables: the tables of batch b appended after those of batch
+ * a: offsets [(Ba+Bb)*L*G + 1], pages [offsets_a[end] + offsets_b[end]].
+ * Errors: TG_ERR_INVALID_ARG; TG_ERR_BUFFER_TOO_SMALL when a capacity is short. */
+int32_t tg_release_requests(const tg_geometry* geom, int32_t batch, const int64_t* pt_offsets,
+                            const int32_t* pt_pages, const uint8_t* finished, int32_t* freed, int64_t freed_capacity,
+                            int64_t* new_offsets, int32_t* new_pages, int64_t pages_capacity, int64_t* num_freed,
+                            int64_t* num_kept, int32_t* num_survivors);
+int32_t tg_concat_tables(const tg_geometry* geom, int32_t batch_a, const int64_t* offsets_a, const int32_t* pages_a,
+                         int32_t batch_b, const int64_t* offsets_b, const int32_t* pages_b, int64_t* offsets,
+                         int32_t* pages);
 
 #ifdef __cplusplus
 }

@@ -7,8 +7,11 @@
 // fp64 product ceil(r * N) and Algorithm 1's quotients are plain fp64 ops.
 #include <algorithm>
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <functional>
+#include <memory>
+#include <thread>
 #include <queue>
 #include <string>
 #include <utility>
@@ -45,6 +48,29 @@ int32_t check_geometry(const tg_geometry* g) {
 static bool ratio_ok(double r) { return r > 0.0 && r <= 1.0; }  // false for NaN
 
 }  // namespace tg
+
+// Host threads for n independent items: one per 256 Ki items, at most the
+// machine's hardware threads and 16 (TG_HOST_THREADS overrides the cap).
+static int host_threads(int64_t n) {
+  int cap = 16;
+  if (const char* e = std::getenv("TG_HOST_THREADS")) cap = std::max(1, std::atoi(e));
+  const int hw = std::max(1u, std::thread::hardware_concurrency());
+  return (int)std::max<int64_t>(1, std::min<int64_t>({(int64_t)std::min(cap, hw), n >> 18}));
+}
+
+// fn(worker, lo, hi) over [0, n) cut into `threads` contiguous chunks; the
+// calling thread runs chunk 0.
+template <typename F>
+static void parallel_chunks(int64_t n, int threads, F fn) {
+  if (threads <= 1) {
+    fn(0, 0, n);
+    return;
+  }
+  std::vector<std::thread> pool;
+  for (int w = 1; w < threads; ++w) pool.emplace_back(fn, w, n * w / threads, n * (w + 1) / threads);
+  fn(0, 0, n / threads);
+  for (auto& t : pool) t.join();
+}
 
 using tg::ceil_div;
 using tg::fail;
@@ -246,15 +272,38 @@ int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_le
   if (!pt_pages) return TG_OK;  // size query: nothing consumed, free list not examined
   if (k > num_free) return fail(TG_ERR_OUT_OF_PAGES, "reservation needs %lld pages, %lld free", (long long)k, (long long)num_free);
   if (pt_capacity < k) return fail(TG_ERR_BUFFER_TOO_SMALL, "pt_pages holds %lld, need %lld", (long long)pt_capacity, (long long)k);
-  // the consumed ids must be distinct pages of the pool
-  std::vector<uint8_t> seen((size_t)pool_pages, 0);
-  for (int64_t i = 0; i < k; ++i) {
-    const int32_t p = free_pages[i];
-    if (p < 0 || p >= pool_pages) return fail(TG_ERR_INVALID_ARG, "free_pages[%lld] = %d outside the pool", (long long)i, p);
-    if (seen[p]) return fail(TG_ERR_INVALID_ARG, "page id %d appears twice in the free list", p);
-    seen[p] = 1;
+  // the consumed ids must be distinct pages of the pool: chunks checked in
+  // parallel against one atomic bitmap; on any failure a sequential pass
+  // reports the first offending entry, so the message does not depend on timing
+  std::unique_ptr<uint64_t[]> seen(new uint64_t[(size_t)(pool_pages + 63) / 64]());
+  const int nthreads = host_threads(k);
+  std::vector<uint8_t> bad((size_t)nthreads, 0);
+  parallel_chunks(k, nthreads, [&](int w, int64_t lo, int64_t hi) {
+    for (int64_t i = lo; i < hi; ++i) {
+      const int32_t p = free_pages[i];
+      if (p < 0 || p >= pool_pages) {
+        bad[w] = 1;
+        return;
+      }
+      const uint64_t bit = 1ull << (p & 63);
+      if (__atomic_fetch_or(&seen[p >> 6], bit, __ATOMIC_RELAXED) & bit) {
+        bad[w] = 1;
+        return;
+      }
+    }
+  });
+  if (std::find(bad.begin(), bad.end(), 1) != bad.end()) {
+    std::vector<uint8_t> once((size_t)pool_pages, 0);
+    for (int64_t i = 0; i < k; ++i) {
+      const int32_t p = free_pages[i];
+      if (p < 0 || p >= pool_pages) return fail(TG_ERR_INVALID_ARG, "free_pages[%lld] = %d outside the pool", (long long)i, p);
+      if (once[p]) return fail(TG_ERR_INVALID_ARG, "page id %d appears twice in the free list", p);
+      once[p] = 1;
+    }
   }
-  std::memcpy(pt_pages, free_pages, (size_t)k * sizeof(int32_t));
+  parallel_chunks(k, nthreads, [&](int, int64_t lo, int64_t hi) {
+    std::memcpy(pt_pages + lo, free_pages + lo, (size_t)(hi - lo) * sizeof(int32_t));
+  });
   return TG_OK;
 }
 
@@ -668,5 +717,132 @@ extern "C" int32_t tg_memory_footprint(const tg_geometry* geom, int32_t batch, c
     f.monolithic_slots += ceil_div(longest, P) * P * L * H;
   }
   *out = f;
+  return TG_OK;
+}
+
+// Order-preserving 32-bit key of an fp32 score: larger number, larger key;
+// -0 and +0 share a key; NaN gets 0, below -inf.
+static inline uint32_t score_key(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, sizeof(u));
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0u;
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// Implicit per-head retention ratios of one sample (Eq. 3's layer-wide top-k).
+extern "C" int32_t tg_implicit_ratios(int32_t num_layers, int32_t num_heads, int32_t n_tokens, const float* scores,
+                                      double rho, double* ratios, int32_t* counts) {
+  if (num_layers < 1 || num_heads < 1 || n_tokens < 1) return fail(TG_ERR_INVALID_ARG, "L, H and N must be >= 1");
+  if ((int64_t)num_heads * n_tokens >= INT32_MAX) return fail(TG_ERR_INVALID_ARG, "H * N too large");
+  if (!(rho > 0.0 && rho <= 1.0)) return fail(TG_ERR_INVALID_ARG, "rho outside (0, 1]");
+  if (!scores || !ratios) return fail(TG_ERR_INVALID_ARG, "NULL array");
+  const int64_t HN = (int64_t)num_heads * n_tokens;
+  const int64_t k = (int64_t)std::ceil(rho * (double)HN);
+  // composite key: score key, then the lower flattened index first (a total order)
+  std::vector<uint64_t> key((size_t)HN), sorted;
+  for (int l = 0; l < num_layers; ++l) {
+    const float* s = scores + (int64_t)l * HN;
+    for (int64_t i = 0; i < HN; ++i)
+      key[i] = ((uint64_t)score_key(s[i]) << 32) | (uint64_t)(0xffffffffu - (uint32_t)i);
+    sorted = key;
+    std::nth_element(sorted.begin(), sorted.begin() + (k - 1), sorted.end(), std::greater<uint64_t>());
+    const uint64_t kth = sorted[k - 1];
+    for (int h = 0; h < num_heads; ++h) {
+      int64_t c = 0;
+      for (int64_t t = 0; t < n_tokens; ++t) c += key[(int64_t)h * n_tokens + t] >= kth;
+      ratios[(int64_t)l * num_heads + h] = (double)c / (double)n_tokens;
+      if (counts) counts[(int64_t)l * num_heads + h] = (int32_t)c;
+    }
+  }
+  return TG_OK;
+}
+
+// B = min(1, mu + alpha * sigma) over the samples, at least floor.
+extern "C" int32_t tg_calibrate_budget(int32_t samples, int32_t num_layers, int32_t num_heads, const double* ratios,
+                                       double alpha, double floor, double* budget) {
+  if (samples < 1 || num_layers < 1 || num_heads < 1) return fail(TG_ERR_INVALID_ARG, "S, L and H must be >= 1");
+  if (!(alpha >= 0.0) || !(floor > 0.0 && floor <= 1.0)) return fail(TG_ERR_INVALID_ARG, "alpha < 0 or floor outside (0, 1]");
+  if (!ratios || !budget) return fail(TG_ERR_INVALID_ARG, "NULL array");
+  const int64_t LH = (int64_t)num_layers * num_heads;
+  for (int64_t i = 0; i < LH * samples; ++i)
+    if (!(ratios[i] >= 0.0 && ratios[i] <= 1.0)) return fail(TG_ERR_INVALID_ARG, "ratio %lld outside [0, 1]", (long long)i);
+  for (int64_t i = 0; i < LH; ++i) {
+    double acc = 0.0;
+    for (int s = 0; s < samples; ++s) acc += ratios[(int64_t)s * LH + i];
+    const double mu = acc / samples;
+    double var = 0.0;
+    for (int s = 0; s < samples; ++s) {
+      const double dev = ratios[(int64_t)s * LH + i] - mu;
+      var += dev * dev;
+    }
+    const double sigma = std::sqrt(var / samples);
+    const double b = mu + alpha * sigma;
+    budget[i] = std::max(floor, std::min(1.0, b));
+  }
+  return TG_OK;
+}
+
+// Finished requests give their pages back; the survivors' tables are compacted.
+extern "C" int32_t tg_release_requests(const tg_geometry* geom, int32_t batch, const int64_t* pt_offsets,
+                                       const int32_t* pt_pages, const uint8_t* finished, int32_t* freed,
+                                       int64_t freed_capacity, int64_t* new_offsets, int32_t* new_pages,
+                                       int64_t pages_capacity, int64_t* num_freed, int64_t* num_kept,
+                                       int32_t* num_survivors) {
+  if (int32_t rc = tg::check_geometry(geom)) return rc;
+  if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
+  if (!pt_offsets || !finished || !num_freed || !num_kept || !num_survivors) return fail(TG_ERR_INVALID_ARG, "NULL array");
+  const int64_t per = (int64_t)geom->num_layers * (geom->num_kv_heads / geom->heads_per_group);
+  if (pt_offsets[0] != 0) return fail(TG_ERR_INVALID_ARG, "pt_offsets must start at 0");
+  for (int64_t t = 0; t < batch * per; ++t)
+    if (pt_offsets[t + 1] < pt_offsets[t]) return fail(TG_ERR_INVALID_ARG, "pt_offsets decreases at %lld", (long long)t);
+  int64_t nf = 0, nk = 0;
+  int32_t ns = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int64_t n = pt_offsets[(b + 1) * per] - pt_offsets[b * per];
+    if (finished[b]) {
+      nf += n;
+    } else {
+      nk += n;
+      ++ns;
+    }
+  }
+  *num_freed = nf;
+  *num_kept = nk;
+  *num_survivors = ns;
+  if (!freed && !new_pages) return TG_OK;  // size query
+  if (!freed || !new_pages || !new_offsets || !pt_pages) return fail(TG_ERR_INVALID_ARG, "NULL output array");
+  if (freed_capacity < nf || pages_capacity < nk) return fail(TG_ERR_BUFFER_TOO_SMALL, "output arrays too small");
+  int64_t f = 0, k = 0, t_out = 0;
+  for (int b = 0; b < batch; ++b) {
+    const int64_t lo = pt_offsets[b * per], hi = pt_offsets[(b + 1) * per];
+    if (finished[b]) {
+      std::memcpy(freed + f, pt_pages + lo, (size_t)(hi - lo) * sizeof(int32_t));
+      f += hi - lo;
+    } else {
+      for (int64_t t = 0; t < per; ++t) new_offsets[t_out++] = pt_offsets[b * per + t] - lo + k;
+      std::memcpy(new_pages + k, pt_pages + lo, (size_t)(hi - lo) * sizeof(int32_t));
+      k += hi - lo;
+    }
+  }
+  new_offsets[t_out] = k;
+  return TG_OK;
+}
+
+// The tables of batch b appended after those of batch a.
+extern "C" int32_t tg_concat_tables(const tg_geometry* geom, int32_t batch_a, const int64_t* offsets_a,
+                                    const int32_t* pages_a, int32_t batch_b, const int64_t* offsets_b,
+                                    const int32_t* pages_b, int64_t* offsets, int32_t* pages) {
+  if (int32_t rc = tg::check_geometry(geom)) return rc;
+  if (batch_a < 0 || batch_b < 0) return fail(TG_ERR_INVALID_ARG, "negative batch");
+  if (!offsets_a || !offsets_b || !offsets) return fail(TG_ERR_INVALID_ARG, "NULL array");
+  const int64_t per = (int64_t)geom->num_layers * (geom->num_kv_heads / geom->heads_per_group);
+  const int64_t na = offsets_a[(int64_t)batch_a * per], nb = offsets_b[(int64_t)batch_b * per];
+  if (offsets_a[0] != 0 || offsets_b[0] != 0 || na < 0 || nb < 0) return fail(TG_ERR_INVALID_ARG, "bad offsets");
+  if ((na > 0 && !pages_a) || (nb > 0 && !pages_b) || (na + nb > 0 && !pages)) return fail(TG_ERR_INVALID_ARG, "NULL pages");
+  for (int64_t t = 0; t < (int64_t)batch_a * per; ++t) offsets[t] = offsets_a[t];
+  for (int64_t t = 0; t <= (int64_t)batch_b * per; ++t) offsets[(int64_t)batch_a * per + t] = offsets_b[t] + na;
+  if (na) std::memcpy(pages, pages_a, (size_t)na * sizeof(int32_t));
+  if (nb) std::memcpy(pages + na, pages_b, (size_t)nb * sizeof(int32_t));
   return TG_OK;
 }

@@ -121,6 +121,10 @@ _SIGS = {
     "tg_compress_plan": (_i32, [_G, _i32, _i32, _i32, _P, _P, _P, _P, _P, _P, _P, _P, _i32, _P, _i32, _P, _P, _P]),
     "tg_compress": (_i32, [C.POINTER(tg_compress_args), _P]),
     "tg_memory_footprint": (_i32, [_G, _i32, _P, _P, _P, _P, C.POINTER(tg_footprint)]),
+    "tg_implicit_ratios": (_i32, [_i32, _i32, _i32, _P, C.c_double, _P, _P]),
+    "tg_calibrate_budget": (_i32, [_i32, _i32, _i32, _P, C.c_double, C.c_double, _P]),
+    "tg_release_requests": (_i32, [_G, _i32, _P, _P, _P, _P, _i64, _P, _P, _i64, _P, _P, _P]),
+    "tg_concat_tables": (_i32, [_G, _i32, _P, _P, _i32, _P, _P, _P, _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -197,7 +201,7 @@ def tg_reserve(geom, ctx_len, ratio, budget, group_of, free_pages, pool_pages, s
     _check(rc, "tg_reserve")
     pages = None
     if not size_query:
-        pages = np.zeros(max(1, need.value), np.int32)
+        pages = np.empty(max(1, need.value), np.int32)
         rc = _lib.tg_reserve(*args, _ptr(pages), need.value, C.byref(need))
         _check(rc, "tg_reserve")
         pages = pages[: need.value]
@@ -367,3 +371,56 @@ def make_append_args(geom, batch, layer, dtype, k_tok, v_tok, kv_pool, pt_pages,
 
 def tg_append(args: tg_append_args, stream=None):
     _check(_lib.tg_append(C.byref(args), _stream(stream)), "tg_append")
+
+
+def tg_implicit_ratios(scores, rho):
+    """scores [L][H][N] float32 -> (ratios [L][H] float64, counts [L][H] int32)."""
+    sc = _host(scores, np.float32)
+    L, H, N = sc.shape
+    r = np.zeros((L, H), np.float64)
+    c = np.zeros((L, H), np.int32)
+    _check(_lib.tg_implicit_ratios(L, H, N, _ptr(sc), float(rho), _ptr(r), _ptr(c)), "tg_implicit_ratios")
+    return r, c
+
+
+def tg_calibrate_budget(ratios, alpha=2.0, floor=1e-3):
+    """ratios [S][L][H] float64 -> budgets [L][H]."""
+    r = _host(ratios, np.float64)
+    S, L, H = r.shape
+    out = np.zeros((L, H), np.float64)
+    _check(_lib.tg_calibrate_budget(S, L, H, _ptr(r), float(alpha), float(floor), _ptr(out)), "tg_calibrate_budget")
+    return out
+
+
+def tg_release_requests(geom, pt_offsets, pt_pages, finished):
+    """-> (freed page ids, new_offsets, new_pages) for the requests that did not finish."""
+    g = _geom(geom)
+    off = _host(pt_offsets, np.int64)
+    pages = _host(pt_pages, np.int32)
+    fin = _host(finished, np.uint8)
+    B = len(fin)
+    nf, nk, ns = C.c_int64(0), C.c_int64(0), C.c_int32(0)
+    head = (C.byref(g), B, _ptr(off), _ptr(pages), _ptr(fin))
+    _check(_lib.tg_release_requests(*head, None, 0, None, None, 0, C.byref(nf), C.byref(nk), C.byref(ns)),
+           "tg_release_requests")
+    per = g.num_layers * (g.num_kv_heads // g.heads_per_group)
+    freed = np.zeros(max(1, nf.value), np.int32)
+    new_pages = np.zeros(max(1, nk.value), np.int32)
+    new_off = np.zeros(ns.value * per + 1, np.int64)
+    _check(_lib.tg_release_requests(*head, _ptr(freed), len(freed), _ptr(new_off), _ptr(new_pages), len(new_pages),
+                                    C.byref(nf), C.byref(nk), C.byref(ns)), "tg_release_requests")
+    return freed[: nf.value], new_off, new_pages[: nk.value]
+
+
+def tg_concat_tables(geom, offsets_a, pages_a, offsets_b, pages_b):
+    """-> (offsets, pages) of batch a followed by batch b."""
+    g = _geom(geom)
+    per = g.num_layers * (g.num_kv_heads // g.heads_per_group)
+    oa, ob = _host(offsets_a, np.int64), _host(offsets_b, np.int64)
+    pa, pb = _host(pages_a, np.int32), _host(pages_b, np.int32)
+    ba, bb = (len(oa) - 1) // per, (len(ob) - 1) // per
+    off = np.zeros((ba + bb) * per + 1, np.int64)
+    pages = np.zeros(max(1, int(oa[-1] + ob[-1])), np.int32)
+    _check(_lib.tg_concat_tables(C.byref(g), ba, _ptr(oa), _ptr(pa), bb, _ptr(ob), _ptr(pb), _ptr(off), _ptr(pages)),
+           "tg_concat_tables")
+    return off, pages[: int(oa[-1] + ob[-1])]

@@ -482,3 +482,58 @@ def test_split_map_plan_bit_exact(data):
         assert pl["num_bins"] == int(S[layer].sum())
     with pytest.raises(tg.TangramError):
         tg.tg_build_plan(geom, B, 0, res["kv_len"], res["pt_offsets"], gof, sof, tg.TG_PLAN_SPLIT_MAP, 1, 1)
+
+
+# ------------------------------------------------ calibration and request lifecycle
+
+@settings(max_examples=40, deadline=None)
+@given(st.data())
+def test_implicit_ratios_and_budget_bit_exact(data):
+    rng = np.random.default_rng(data.draw(st.integers(0, 2**31)))
+    L, H, N = data.draw(st.integers(1, 3)), data.draw(st.integers(1, 8)), data.draw(st.integers(1, 60))
+    S = data.draw(st.integers(1, 5))
+    rho = data.draw(st.sampled_from([0.05, 0.3, 0.5, 0.7, 1.0, float(rng.uniform(0.01, 1.0))]))
+    samples = []
+    for _ in range(S):
+        sc = (rng.integers(-6, 7, size=(L, H, N)) / 2).astype(np.float32)       # many ties
+        sc[rng.random(sc.shape) < 0.05] = np.nan
+        sc[rng.random(sc.shape) < 0.05] = -0.0
+        r, c = tg.tg_implicit_ratios(sc, rho)
+        orr, oc = oracle.implicit_ratios(sc, rho)
+        assert np.array_equal(c, oc) and np.array_equal(r, orr)
+        samples.append(r)
+    alpha = data.draw(st.sampled_from([0.0, 1.0, 2.0, 3.5]))
+    B = tg.tg_calibrate_budget(np.stack(samples), alpha, 1e-3)
+    assert np.array_equal(B, oracle.calibrate_budget(np.stack(samples), alpha, 1e-3))
+
+
+def test_calibration_errors():
+    for args in ((np.zeros((1, 1, 4), np.float32), 0.0), (np.zeros((1, 1, 4), np.float32), 1.5)):
+        with pytest.raises(tg.TangramError):
+            tg.tg_implicit_ratios(*args)
+    for kw in (dict(alpha=-1.0), dict(floor=0.0), dict(floor=1.5)):
+        with pytest.raises(tg.TangramError):
+            tg.tg_calibrate_budget(np.full((2, 1, 1), 0.5), **kw)
+    with pytest.raises(tg.TangramError):
+        tg.tg_calibrate_budget(np.full((2, 1, 1), 1.5))
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 4])
+def test_release_and_concat_bit_exact(cfg):
+    wl = config(cfg)
+    g = wl.geom
+    _, gof, _ = tg.tg_cluster_heads(g, wl.budget)
+    pool = 10**7
+    res = tg.tg_reserve(g, wl.ctx_len, wl.ratio, None, gof, free_list(wl, pool), pool)
+    rng = np.random.default_rng(cfg)
+    fin = rng.random(wl.batch) < 0.4
+    freed, off, pages = tg.tg_release_requests(g, res["pt_offsets"], res["pt_pages"], fin)
+    of, oo, op = oracle.release_requests(res["pt_offsets"], res["pt_pages"], fin, g.num_layers, g.num_groups)
+    assert np.array_equal(freed, of) and np.array_equal(off, oo) and np.array_equal(pages, op)
+    # readmit the finished requests from the freed pages and append their tables
+    if fin.any():
+        again = tg.tg_reserve(g, wl.ctx_len[fin], wl.ratio[fin], None, gof, freed, pool)
+        o2, p2 = tg.tg_concat_tables(g, off, pages, again["pt_offsets"], again["pt_pages"])
+        e2, q2 = oracle.concat_tables(off, pages, again["pt_offsets"], again["pt_pages"])
+        assert np.array_equal(o2, e2) and np.array_equal(p2, q2)
+        assert sorted(p2.tolist()) == sorted(res["pt_pages"].tolist())

@@ -176,6 +176,20 @@ def model_step(name: str) -> Workload:
     return Workload(f"{name}-decode-step-bf16", seed, g, 64, "bf16", ctx, budget, ratio)
 
 
+def retention_scores(seed: int, sample: int, num_layers: int, num_heads: int, n_tokens: int,
+                     head_spread: float = 1.0, sample_jitter: float = 0.1) -> np.ndarray:
+    """Importance scores [L][H][N] float32 of one calibration sample: head (l, h) scores its tokens
+    a_{l,h} + d_{s,l,h} + N(0, 1), with a static head offset a ~ N(0, head_spread^2) drawn from `seed`
+    alone (the input-invariant head ranking) and a per-sample offset d ~ N(0, sample_jitter^2) (the
+    narrow per-input band).  Stands in for a compression method's scores on a pilot context."""
+    a = np.random.default_rng(np.random.SeedSequence(seed).spawn(1)[0]).standard_normal(
+        (num_layers, num_heads, 1)) * head_spread
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 1 + sample]))
+    d = rng.standard_normal((num_layers, num_heads, 1)) * sample_jitter
+    z = rng.standard_normal((num_layers, num_heads, n_tokens), dtype=np.float32)
+    return (z + (a + d).astype(np.float32)).astype(np.float32)
+
+
 def custom(seed: int, geom: Geometry, batch: int, dtype: str, ctx_len, budget=None, ratio=None,
            frac_hi=0.25, hi=(0.7, 1.0), lo=(0.05, 0.2), jitter=0.03, chunk_len=0,
            q_scale=1.0, kv_scale=1.0) -> Workload:
