@@ -188,6 +188,15 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
 #pragma unroll
     for (int kk = 0; kk < 8; ++kk) qb[cb][kk] = row_ok[cb] ? qp[kk * 2 + hf] : u4(0u);
   }
+  // Settle the query loads here, once: the compiler's wait-count pass cannot
+  // see the inline-assembly LDS DMAs, so a load still pending at the loop
+  // entry would make it wait for vmcnt(0) - every DMA in flight - at the first
+  // use of qb on every tile.  Routing qb through an empty asm places that one
+  // wait before the loop and leaves no compiler-tracked load behind.
+#pragma unroll
+  for (int cb = 0; cb < kCB; ++cb)
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk) asm volatile("" : "+v"(qb[cb][kk]));
   const int wave_i_max = min(C - 1, (min(row0 + wave * kRowsPerWave + kRowsPerWave, rows_total) - 1) / gqa);
   const int wave_i_min = min(C - 1, (row0 + wave * kRowsPerWave) / gqa);
 
@@ -287,12 +296,31 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
 #pragma unroll
       for (int cb = 0; cb < kCB; ++cb) sc[cb] = f32x16(0.f);
       const int krow = kb * 32 + k_row;
+      // all eight K operands of the block, and the V^T operands of its p.v
+      // products (they do not depend on p), are requested before the first
+      // product, so their LDS latency hides under q.k and the softmax
+      u4 ka[8];
 #pragma unroll
-      for (int kk = 0; kk < 8; ++kk) {
-        const u4 a = *reinterpret_cast<const u4*>(kt + krow * 256 + (((kk * 2 + hf) ^ (krow & 15)) << 4));
+      for (int kk = 0; kk < 8; ++kk)
+        ka[kk] = *reinterpret_cast<const u4*>(kt + krow * 256 + (((kk * 2 + hf) ^ (krow & 15)) << 4));
+      u4 va[2][4];
 #pragma unroll
-        for (int cb = 0; cb < kCB; ++cb) sc[cb] = mfma(a, qb[cb][kk], sc[cb]);
+      for (int q16 = 0; q16 < 2; ++q16) {
+        const int g0 = kb * 32 + q16 * 16 + 4 * hf;    // tile row of the A operand's first key
+        const int r0 = g0 + tr_key, r1 = g0 + 8 + tr_key;  // source rows of the two transposed reads
+#pragma unroll
+        for (int db = 0; db < 4; ++db) {
+          const int c = 4 * db + tr_chunk;
+          const u2v lo = lds_read_tr16(vt + r0 * 256 + ((c ^ (4 * (r0 & 3))) << 4) + tr_half * 8);
+          const u2v hi = lds_read_tr16(vt + r1 * 256 + ((c ^ (4 * (r1 & 3))) << 4) + tr_half * 8);
+          va[q16][db] = u4{lo.x, lo.y, hi.x, hi.y};
+        }
       }
+      __builtin_amdgcn_sched_barrier(0);   // keep the reads ahead of the products
+#pragma unroll
+      for (int kk = 0; kk < 8; ++kk)
+#pragma unroll
+        for (int cb = 0; cb < kCB; ++cb) sc[cb] = mfma(ka[kk], qb[cb][kk], sc[cb]);
       // only the block holding the end of the history and the chunk blocks
       // that reach past the wave's first row need a mask
       const bool masked = is_chunk ? kbase + 31 > wave_i_min : kbase + 32 > hist;
@@ -337,19 +365,11 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
       }
       // O^T += V^T P^T over the two 16-key halves of the block
 #pragma unroll
-      for (int q16 = 0; q16 < 2; ++q16) {
-        const int g0 = kb * 32 + q16 * 16 + 4 * hf;    // tile row of the A operand's first key
-        const int r0 = g0 + tr_key, r1 = g0 + 8 + tr_key;  // source rows of the two transposed reads
+      for (int q16 = 0; q16 < 2; ++q16)
 #pragma unroll
-        for (int db = 0; db < 4; ++db) {
-          const int c = 4 * db + tr_chunk;
-          const u2v lo = lds_read_tr16(vt + r0 * 256 + ((c ^ (4 * (r0 & 3))) << 4) + tr_half * 8);
-          const u2v hi = lds_read_tr16(vt + r1 * 256 + ((c ^ (4 * (r1 & 3))) << 4) + tr_half * 8);
-          const u4 a = u4{lo.x, lo.y, hi.x, hi.y};
+        for (int db = 0; db < 4; ++db)
 #pragma unroll
-          for (int cb = 0; cb < kCB; ++cb) acc[cb][db] = mfma(a, pb[cb][q16], acc[cb][db]);
-        }
-      }
+          for (int cb = 0; cb < kCB; ++cb) acc[cb][db] = mfma(va[q16][db], pb[cb][q16], acc[cb][db]);
     }
   }
   wait_vmcnt<0>();
