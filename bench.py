@@ -547,6 +547,8 @@ def main():
     ap.add_argument("--calibrate-xcd", action="store_true",
                     help="rebuild the fill plans with per-XCD bin weights measured in one stamped step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--probe-workers", type=int, default=8192,
+                    help="waves of the streaming-read ceiling probe (8 per SIMD by default)")
     ap.add_argument("--copy-probe", type=int, default=0)
     ap.add_argument("--compress-chunk", type=int, default=0,
                     help="time only the compression of a chunk of this many tokens (config 5's requests)")
@@ -652,6 +654,27 @@ def main():
             lay_ms += np.array([a.elapsed_time(b) for a, b in evs])
         lay_ms /= nrep
         busy = s.worker_busy(stream)   # an extra untimed step with per-worker stamps
+        # streaming-read ceiling of the same access pattern: the probe reads exactly the page slabs the
+        # decode reads on a sample of layers, with the same number of workers and no arithmetic
+        probe_layers = s.layers[:: max(1, len(s.layers) // 8)]
+        t_probe = t_dec = 0.0
+        probe_bytes = 0
+        probe_workers = args.probe_workers
+        out_ck = torch.zeros(probe_workers, dtype=torch.int32, device="cuda")
+        for l in probe_layers:
+            pages, slots = s.layer_slabs(l)
+            dp, ds = torch.from_numpy(pages).cuda(), torch.from_numpy(slots).cuda()
+            tg.tg_read_probe(g, s.tg_dtype, s.pool, dp, ds, probe_workers, out_ck, stream)   # untimed warm-up
+            a_, b_, c_ = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+            a_.record(stream)
+            tg.tg_read_probe(g, s.tg_dtype, s.pool, dp, ds, probe_workers, out_ck, stream)
+            b_.record(stream)
+            s.run_layer(l, stream)
+            c_.record(stream)
+            torch.cuda.synchronize()
+            t_probe += a_.elapsed_time(b_)
+            t_dec += b_.elapsed_time(c_)
+            probe_bytes += len(pages) * 2 * g.page_size * g.head_dim * (2 if wl.dtype == "bf16" else 4)
     launch_bytes = np.array([s.t.kv_bytes(l) for l in s.layers], dtype=np.float64)
     achieved = float(launch_bytes.sum() / (lay_ms.sum() * 1e-3) / 1e9)
     imb = [s.bin_load_stats(l) for l in s.layers]
@@ -675,6 +698,11 @@ def main():
                                   + str(np.round(xcd_speed, 3).tolist()),
                    "parallelism": "single GPU"},
         "us_per_step": round((med if flush else ms_per_step) * 1e3, 1),
+        "stream_ceiling": {"value": round(probe_bytes / (t_probe * 1e-3) / 1e9, 1), "unit": "GB/s",
+                           "layers": len(probe_layers),
+                           "workers": args.probe_workers,
+                           "what": "tg_read_probe: the same page slabs as the decode, no arithmetic"},
+        "frac_of_stream_ceiling": round(t_probe / t_dec, 4),
         "hbm_frac": round(value / HBM_PEAK_GBS, 4),
         "plan_build_us": round(s.plan_build_us, 1),
         "load_imbalance_planned": round(planned_imbalance, 4),

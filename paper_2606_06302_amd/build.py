@@ -22,7 +22,7 @@ HIPCC = os.path.join(ROCM, "bin", "hipcc")
 ARCH = "gfx950"
 
 HOST_SOURCES = ["tg_host.cpp"]
-HIP_SOURCES = ["tg_decode.hip", "tg_prefill.hip", "tg_compress.hip", "tg_append.hip"]
+HIP_SOURCES = ["tg_decode.hip", "tg_prefill.hip", "tg_compress.hip", "tg_append.hip", "tg_probe.hip"]
 
 HIP_FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-fPIC", "-std=c++17",

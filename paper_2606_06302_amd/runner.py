@@ -221,6 +221,20 @@ class DecodeSession:
             res.append((float(busy.max()), float(busy.mean())))
         return res
 
+    def layer_slabs(self, l):
+        """(page id, slot) of every page slab layer l's plan reads, in item order: the decode's reads
+        without its queries, for the streaming-read ceiling."""
+        g = self.wl.geom
+        P = g.page_size
+        items = self.plans[l]["items"]
+        ntok = self.item_tokens(l)
+        npg = -(-ntok // P)
+        first = items["pt_base"] + items["tok_begin"] // P
+        starts = np.repeat(first, npg) + (np.arange(int(npg.sum())) - np.repeat(np.cumsum(npg) - npg, npg))
+        pages = self.t.pt_pages[starts].astype(np.int32)
+        slots = np.repeat(items["slot"], npg).astype(np.int32)
+        return pages, slots
+
     def bin_load_stats(self, l):
         """Planned token load per bin: (max, mean)."""
         p = self.plans[l]

@@ -125,6 +125,7 @@ _SIGS = {
     "tg_calibrate_budget": (_i32, [_i32, _i32, _i32, _P, C.c_double, C.c_double, _P]),
     "tg_release_requests": (_i32, [_G, _i32, _P, _P, _P, _P, _i64, _P, _P, _i64, _P, _P, _P]),
     "tg_concat_tables": (_i32, [_G, _i32, _P, _P, _i32, _P, _P, _P, _P]),
+    "tg_read_probe": (_i32, [_G, _i32, _P, _P, _P, _i64, _i32, _P, _P]),
 }
 for _name, (_res, _args) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -424,3 +425,10 @@ def tg_concat_tables(geom, offsets_a, pages_a, offsets_b, pages_b):
     _check(_lib.tg_concat_tables(C.byref(g), ba, _ptr(oa), _ptr(pa), bb, _ptr(ob), _ptr(pb), _ptr(off), _ptr(pages)),
            "tg_concat_tables")
     return off, pages[: int(oa[-1] + ob[-1])]
+
+
+def tg_read_probe(geom, dtype, kv_pool, page_ids, slots, n_workers, out, stream=None):
+    """Streams the K and V slabs of every (page_ids[i], slots[i]) (device int32 tensors); out is a device
+    uint32/int32 tensor of n_workers checksums."""
+    _check(_lib.tg_read_probe(C.byref(_geom(geom)), int(dtype), _dptr(kv_pool), _dptr(page_ids), _dptr(slots),
+                              int(page_ids.numel()), int(n_workers), _dptr(out), _stream(stream)), "tg_read_probe")

@@ -269,3 +269,29 @@ def test_split_map_plan_vs_oracle():
     for l in range(g.num_layers):
         assert s.plans[l]["num_bins"] == int(tg.tg_split_map(g, wl.budget, s.t.perm, 128)[l].sum())
         compare_layer(s, l, what=f"split map layer {l}")
+
+
+def test_read_probe_checksums():
+    """The streaming-read probe reads exactly the slabs the decode reads: every worker's XOR checksum equals
+    the host's over the same (page, slot) K and V slabs."""
+    _gpu()
+    wl = config(1)
+    s = DecodeSession(wl, n_bins=8, split_target=16, fill="host")
+    pages, slots = s.layer_slabs(0)
+    pool = s.pool.contiguous()
+    n_workers = 7
+    out = torch.zeros(n_workers, dtype=torch.int32, device="cuda")
+    tg.tg_read_probe(wl.geom, tg.TG_F32, pool, torch.from_numpy(pages).cuda(), torch.from_numpy(slots).cuda(),
+                     n_workers, out)
+    torch.cuda.synchronize()
+    words = pool.cpu().numpy().view(np.uint32).reshape(s.t.pool_pages, 2, wl.geom.heads_per_group, -1)
+    n = len(pages)
+    want = []
+    for w in range(n_workers):
+        lo, hi = n * w // n_workers, n * (w + 1) // n_workers
+        x = np.uint32(0)
+        for i in range(lo, hi):
+            x ^= np.bitwise_xor.reduce(words[pages[i], 0, slots[i]]) ^ np.bitwise_xor.reduce(words[pages[i], 1, slots[i]])
+        want.append(int(x))
+    assert out.cpu().numpy().view(np.uint32).tolist() == want
+    assert n == int(sum(-(-(it["tok_end"] - it["tok_begin"]) // 16) for it in s.plans[0]["items"]))
