@@ -56,7 +56,8 @@ enum {
   TG_ERR_OUT_OF_PAGES = -2,    /* free list shorter than the reservation needs */
   TG_ERR_BUFFER_TOO_SMALL = -3,/* caller output / workspace buffer too small */
   TG_ERR_UNSUPPORTED = -4,     /* valid but not implemented (head_dim, page size) */
-  TG_ERR_HIP = -5              /* a HIP runtime call or kernel launch failed */
+  TG_ERR_HIP = -5,             /* a HIP runtime call or kernel launch failed */
+  TG_ERR_NO_MEMORY = -6        /* a host allocation inside a host call failed */
 };
 
 /* storage / arithmetic types of Q, K, V and outputs */

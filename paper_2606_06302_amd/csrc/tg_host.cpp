@@ -11,6 +11,7 @@
 #include <cstring>
 #include <functional>
 #include <memory>
+#include <new>
 #include <thread>
 #include <queue>
 #include <string>
@@ -49,6 +50,20 @@ static bool ratio_ok(double r) { return r > 0.0 && r <= 1.0; }  // false for NaN
 
 }  // namespace tg
 
+// Runs an entry point's body so that no C++ exception reaches a C caller: a
+// failed host allocation becomes TG_ERR_NO_MEMORY, anything else
+// TG_ERR_INVALID_ARG, with nothing consumed.
+template <typename F>
+static int32_t guarded(F&& body) {
+  try {
+    return body();
+  } catch (const std::bad_alloc&) {
+    return tg::fail(TG_ERR_NO_MEMORY, "host memory allocation failed");
+  } catch (...) {
+    return tg::fail(TG_ERR_INVALID_ARG, "unexpected host error");
+  }
+}
+
 // Host threads for n independent items: one per 256 Ki items, at most the
 // machine's hardware threads and 16 (TG_HOST_THREADS overrides the cap).
 static int host_threads(int64_t n) {
@@ -59,7 +74,8 @@ static int host_threads(int64_t n) {
 }
 
 // fn(worker, lo, hi) over [0, n) cut into `threads` contiguous chunks; the
-// calling thread runs chunk 0.
+// calling thread runs chunk 0, and any chunk whose thread cannot be started.
+// No exception leaves: a C caller must never see one.
 template <typename F>
 static void parallel_chunks(int64_t n, int threads, F fn) {
   if (threads <= 1) {
@@ -67,8 +83,16 @@ static void parallel_chunks(int64_t n, int threads, F fn) {
     return;
   }
   std::vector<std::thread> pool;
-  for (int w = 1; w < threads; ++w) pool.emplace_back(fn, w, n * w / threads, n * (w + 1) / threads);
+  std::vector<int> inline_chunks;
+  for (int w = 1; w < threads; ++w) {
+    try {
+      pool.emplace_back(fn, w, n * w / threads, n * (w + 1) / threads);
+    } catch (...) {
+      inline_chunks.push_back(w);
+    }
+  }
   fn(0, 0, n / threads);
+  for (int w : inline_chunks) fn(w, n * w / threads, n * (w + 1) / threads);
   for (auto& t : pool) t.join();
 }
 
@@ -184,6 +208,7 @@ const char* tg_status_string(int32_t code) {
     case TG_ERR_BUFFER_TOO_SMALL: return "buffer too small";
     case TG_ERR_UNSUPPORTED: return "unsupported";
     case TG_ERR_HIP: return "HIP error";
+    case TG_ERR_NO_MEMORY: return "out of host memory";
     default: return "unknown status";
   }
 }
@@ -196,27 +221,29 @@ int32_t tg_version(void) { return (1 << 16) | 1; }
 // equal budgets keep ascending head index) and cut into groups of H_p.
 int32_t tg_cluster_heads(const tg_geometry* geom, const double* budget, int32_t grouping,
                          int32_t* perm, int32_t* group_of, int32_t* slot_of) {
-  if (int32_t rc = tg::check_geometry(geom)) return rc;
-  if (!budget || !perm || !group_of || !slot_of) return fail(TG_ERR_INVALID_ARG, "NULL array");
-  if (grouping != TG_GROUP_CLUSTERED && grouping != TG_GROUP_ADJACENT)
-    return fail(TG_ERR_INVALID_ARG, "unknown grouping %d", grouping);
-  const int L = geom->num_layers, H = geom->num_kv_heads, Hp = geom->heads_per_group;
-  for (int64_t i = 0; i < (int64_t)L * H; ++i)
-    if (!tg::ratio_ok(budget[i])) return fail(TG_ERR_INVALID_ARG, "budget[%lld] outside (0,1]", (long long)i);
-  std::vector<int32_t> order(H);
-  for (int l = 0; l < L; ++l) {
-    const double* bl = budget + (int64_t)l * H;
-    for (int h = 0; h < H; ++h) order[h] = h;
-    if (grouping == TG_GROUP_CLUSTERED)
-      std::stable_sort(order.begin(), order.end(), [bl](int32_t a, int32_t b) { return bl[a] < bl[b]; });
-    for (int j = 0; j < H; ++j) {
-      const int h = order[j];
-      perm[(int64_t)l * H + j] = h;
-      group_of[(int64_t)l * H + h] = j / Hp;
-      slot_of[(int64_t)l * H + h] = j % Hp;
+  return guarded([&]() -> int32_t {
+    if (int32_t rc = tg::check_geometry(geom)) return rc;
+    if (!budget || !perm || !group_of || !slot_of) return fail(TG_ERR_INVALID_ARG, "NULL array");
+    if (grouping != TG_GROUP_CLUSTERED && grouping != TG_GROUP_ADJACENT)
+      return fail(TG_ERR_INVALID_ARG, "unknown grouping %d", grouping);
+    const int L = geom->num_layers, H = geom->num_kv_heads, Hp = geom->heads_per_group;
+    for (int64_t i = 0; i < (int64_t)L * H; ++i)
+      if (!tg::ratio_ok(budget[i])) return fail(TG_ERR_INVALID_ARG, "budget[%lld] outside (0,1]", (long long)i);
+    std::vector<int32_t> order(H);
+    for (int l = 0; l < L; ++l) {
+      const double* bl = budget + (int64_t)l * H;
+      for (int h = 0; h < H; ++h) order[h] = h;
+      if (grouping == TG_GROUP_CLUSTERED)
+        std::stable_sort(order.begin(), order.end(), [bl](int32_t a, int32_t b) { return bl[a] < bl[b]; });
+      for (int j = 0; j < H; ++j) {
+        const int h = order[j];
+        perm[(int64_t)l * H + j] = h;
+        group_of[(int64_t)l * H + h] = j / Hp;
+        slot_of[(int64_t)l * H + h] = j % Hp;
+      }
     }
-  }
-  return TG_OK;
+    return TG_OK;
+  });
 }
 
 // Eq. 4 + Section 4.1 (Precise Page Allocation) + Section 4.2.1/4.2.3.
@@ -225,72 +252,73 @@ int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_le
                    int64_t num_free,
                    int64_t pool_pages, int32_t* kv_len, int32_t* group_len, int64_t* pt_offsets,
                    int32_t* pt_pages, int64_t pt_capacity, int64_t* pages_needed) {
-  if (int32_t rc = tg::check_geometry(geom)) return rc;
-  if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
-  if (!ctx_len || !group_of || !kv_len || !group_len || !pt_offsets || !pages_needed)
-    return fail(TG_ERR_INVALID_ARG, "NULL array");
-  if (!ratio && !budget) return fail(TG_ERR_INVALID_ARG, "ratio and budget are both NULL");
-  if (num_free < 0 || pool_pages < 0) return fail(TG_ERR_INVALID_ARG, "negative pool size");
-  if (num_free > 0 && !free_pages) return fail(TG_ERR_INVALID_ARG, "free_pages is NULL");
-  const int L = geom->num_layers, H = geom->num_kv_heads, G = H / geom->heads_per_group;
-  const int64_t P = geom->page_size;
-  for (int64_t i = 0; i < (int64_t)L * H; ++i)
-    if (group_of[i] < 0 || group_of[i] >= G) return fail(TG_ERR_INVALID_ARG, "group_of[%lld] out of range", (long long)i);
-  for (int b = 0; b < batch; ++b) {
-    if (ctx_len[b] < 1) return fail(TG_ERR_INVALID_ARG, "ctx_len[%d] < 1", b);
-    if (headroom && headroom[b] < 0) return fail(TG_ERR_INVALID_ARG, "headroom[%d] < 0", b);
-  }
-  // retained lengths first (validating every ratio before anything is written)
-  for (int b = 0; b < batch; ++b)
-    for (int64_t i = 0; i < (int64_t)L * H; ++i) {
-      const double r = ratio ? ratio[(int64_t)b * L * H + i] : budget[i];
-      if (!tg::ratio_ok(r)) return fail(TG_ERR_INVALID_ARG, "ratio of request %d entry %lld outside (0,1]", b, (long long)i);
+  return guarded([&]() -> int32_t {
+    if (int32_t rc = tg::check_geometry(geom)) return rc;
+    if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
+    if (!ctx_len || !group_of || !kv_len || !group_len || !pt_offsets || !pages_needed)
+      return fail(TG_ERR_INVALID_ARG, "NULL array");
+    if (!ratio && !budget) return fail(TG_ERR_INVALID_ARG, "ratio and budget are both NULL");
+    if (num_free < 0 || pool_pages < 0) return fail(TG_ERR_INVALID_ARG, "negative pool size");
+    if (num_free > 0 && !free_pages) return fail(TG_ERR_INVALID_ARG, "free_pages is NULL");
+    const int L = geom->num_layers, H = geom->num_kv_heads, G = H / geom->heads_per_group;
+    const int64_t P = geom->page_size;
+    for (int64_t i = 0; i < (int64_t)L * H; ++i)
+      if (group_of[i] < 0 || group_of[i] >= G) return fail(TG_ERR_INVALID_ARG, "group_of[%lld] out of range", (long long)i);
+    for (int b = 0; b < batch; ++b) {
+      if (ctx_len[b] < 1) return fail(TG_ERR_INVALID_ARG, "ctx_len[%d] < 1", b);
+      if (headroom && headroom[b] < 0) return fail(TG_ERR_INVALID_ARG, "headroom[%d] < 0", b);
     }
-  for (int b = 0; b < batch; ++b) {
-    const double n = (double)ctx_len[b];
-    for (int64_t i = 0; i < (int64_t)L * H; ++i) {
-      const double r = ratio ? ratio[(int64_t)b * L * H + i] : budget[i];
-      kv_len[(int64_t)b * L * H + i] = (int32_t)std::ceil(r * n);
-    }
-  }
-  // group lengths and the CSR offsets of every (b, l, g) table
-  int64_t k = 0;
-  for (int b = 0; b < batch; ++b)
-    for (int l = 0; l < L; ++l) {
-      int32_t* gl = group_len + ((int64_t)b * L + l) * G;
-      for (int g = 0; g < G; ++g) gl[g] = 0;
-      const int32_t* kl = kv_len + ((int64_t)b * L + l) * H;
-      const int32_t* gof = group_of + (int64_t)l * H;
-      for (int h = 0; h < H; ++h) gl[gof[h]] = std::max(gl[gof[h]], kl[h]);
-      for (int g = 0; g < G; ++g) {
-        pt_offsets[((int64_t)b * L + l) * G + g] = k;
-        k += ceil_div((int64_t)gl[g] + (headroom ? headroom[b] : 0), P);
+    // retained lengths first (validating every ratio before anything is written)
+    for (int b = 0; b < batch; ++b)
+      for (int64_t i = 0; i < (int64_t)L * H; ++i) {
+        const double r = ratio ? ratio[(int64_t)b * L * H + i] : budget[i];
+        if (!tg::ratio_ok(r)) return fail(TG_ERR_INVALID_ARG, "ratio of request %d entry %lld outside (0,1]", b, (long long)i);
+      }
+    for (int b = 0; b < batch; ++b) {
+      const double n = (double)ctx_len[b];
+      for (int64_t i = 0; i < (int64_t)L * H; ++i) {
+        const double r = ratio ? ratio[(int64_t)b * L * H + i] : budget[i];
+        kv_len[(int64_t)b * L * H + i] = (int32_t)std::ceil(r * n);
       }
     }
-  pt_offsets[(int64_t)batch * L * G] = k;
-  *pages_needed = k;
-  if (!pt_pages) return TG_OK;  // size query: nothing consumed, free list not examined
-  if (k > num_free) return fail(TG_ERR_OUT_OF_PAGES, "reservation needs %lld pages, %lld free", (long long)k, (long long)num_free);
-  if (pt_capacity < k) return fail(TG_ERR_BUFFER_TOO_SMALL, "pt_pages holds %lld, need %lld", (long long)pt_capacity, (long long)k);
-  // the consumed ids must be distinct pages of the pool: chunks checked in
-  // parallel against one atomic bitmap; on any failure a sequential pass
-  // reports the first offending entry, so the message does not depend on timing
-  std::unique_ptr<uint64_t[]> seen(new uint64_t[(size_t)(pool_pages + 63) / 64]());
-  const int nthreads = host_threads(k);
-  std::vector<uint8_t> bad((size_t)nthreads, 0);
-  parallel_chunks(k, nthreads, [&](int w, int64_t lo, int64_t hi) {
-    for (int64_t i = lo; i < hi; ++i) {
-      const int32_t p = free_pages[i];
-      if (p < 0 || p >= pool_pages) {
-        bad[w] = 1;
-        return;
+    // group lengths and the CSR offsets of every (b, l, g) table
+    int64_t k = 0;
+    for (int b = 0; b < batch; ++b)
+      for (int l = 0; l < L; ++l) {
+        int32_t* gl = group_len + ((int64_t)b * L + l) * G;
+        for (int g = 0; g < G; ++g) gl[g] = 0;
+        const int32_t* kl = kv_len + ((int64_t)b * L + l) * H;
+        const int32_t* gof = group_of + (int64_t)l * H;
+        for (int h = 0; h < H; ++h) gl[gof[h]] = std::max(gl[gof[h]], kl[h]);
+        for (int g = 0; g < G; ++g) {
+          pt_offsets[((int64_t)b * L + l) * G + g] = k;
+          k += ceil_div((int64_t)gl[g] + (headroom ? headroom[b] : 0), P);
+        }
       }
-      const uint64_t bit = 1ull << (p & 63);
-      if (__atomic_fetch_or(&seen[p >> 6], bit, __ATOMIC_RELAXED) & bit) {
-        bad[w] = 1;
-        return;
+    pt_offsets[(int64_t)batch * L * G] = k;
+    *pages_needed = k;
+    if (!pt_pages) return TG_OK;  // size query: nothing consumed, free list not examined
+    if (k > num_free) return fail(TG_ERR_OUT_OF_PAGES, "reservation needs %lld pages, %lld free", (long long)k, (long long)num_free);
+    if (pt_capacity < k) return fail(TG_ERR_BUFFER_TOO_SMALL, "pt_pages holds %lld, need %lld", (long long)pt_capacity, (long long)k);
+    // the consumed ids must be distinct pages of the pool: chunks checked in
+    // parallel against one atomic bitmap; on any failure a sequential pass
+    // reports the first offending entry, so the message does not depend on timing
+    std::unique_ptr<uint64_t[]> seen(new uint64_t[(size_t)(pool_pages + 63) / 64]());
+    const int nthreads = host_threads(k);
+    std::vector<uint8_t> bad((size_t)nthreads, 0);
+    parallel_chunks(k, nthreads, [&](int w, int64_t lo, int64_t hi) {
+      for (int64_t i = lo; i < hi; ++i) {
+        const int32_t p = free_pages[i];
+        if (p < 0 || p >= pool_pages) {
+          bad[w] = 1;
+          return;
+        }
+        const uint64_t bit = 1ull << (p & 63);
+        if (__atomic_fetch_or(&seen[p >> 6], bit, __ATOMIC_RELAXED) & bit) {
+          bad[w] = 1;
+          return;
+        }
       }
-    }
   });
   if (std::find(bad.begin(), bad.end(), 1) != bad.end()) {
     std::vector<uint8_t> once((size_t)pool_pages, 0);
@@ -305,6 +333,7 @@ int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_le
     std::memcpy(pt_pages + lo, free_pages + lo, (size_t)(hi - lo) * sizeof(int32_t));
   });
   return TG_OK;
+  });
 }
 
 // Algorithm 1, fp64, in the paper's order of operations.
@@ -498,23 +527,25 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
                       int32_t n_bins, int32_t split_target, const int32_t* bin_weights, tg_work_item* items,
                       int32_t item_capacity, int32_t* bin_offsets, int32_t bin_capacity, int32_t* unit_splits,
                       int32_t* unit_partial_base, int32_t* num_items, int32_t* num_bins, int32_t* num_partials) {
-  if ((mode & ~0x1ff) != 0) return fail(TG_ERR_INVALID_ARG, "unknown plan mode %d", mode);
-  const bool open_end = (mode & TG_PLAN_OPEN_END) != 0;
-  const int32_t rc = build_plan_core(geom, batch, layer, kv_len, pt_offsets, group_of, slot_of,
-                                     mode & ~TG_PLAN_OPEN_END, n_bins, split_target, bin_weights, items,
-                                     item_capacity, bin_offsets, bin_capacity, unit_splits, unit_partial_base,
-                                     num_items, num_bins, num_partials);
-  if (rc != TG_OK || !open_end || !items) return rc;
-  // the chunk that ends each unit runs to the live length, bounded by its table
-  const int64_t L = geom->num_layers, H = geom->num_kv_heads, G = H / geom->heads_per_group;
-  for (int32_t i = 0; i < *num_items; ++i) {
-    tg_work_item& it = items[i];
-    const int64_t lh = (int64_t)layer * H + it.kv_head;
-    if (it.tok_end != kv_len[((int64_t)it.b * L + layer) * H + it.kv_head]) continue;
-    const int64_t t = ((int64_t)it.b * L + layer) * G + group_of[lh];
-    it.tok_end = (int32_t)(-(pt_offsets[t + 1] - pt_offsets[t]) * geom->page_size);
-  }
-  return TG_OK;
+  return guarded([&]() -> int32_t {
+    if ((mode & ~0x1ff) != 0) return fail(TG_ERR_INVALID_ARG, "unknown plan mode %d", mode);
+    const bool open_end = (mode & TG_PLAN_OPEN_END) != 0;
+    const int32_t rc = build_plan_core(geom, batch, layer, kv_len, pt_offsets, group_of, slot_of,
+                                       mode & ~TG_PLAN_OPEN_END, n_bins, split_target, bin_weights, items,
+                                       item_capacity, bin_offsets, bin_capacity, unit_splits, unit_partial_base,
+                                       num_items, num_bins, num_partials);
+    if (rc != TG_OK || !open_end || !items) return rc;
+    // the chunk that ends each unit runs to the live length, bounded by its table
+    const int64_t L = geom->num_layers, H = geom->num_kv_heads, G = H / geom->heads_per_group;
+    for (int32_t i = 0; i < *num_items; ++i) {
+      tg_work_item& it = items[i];
+      const int64_t lh = (int64_t)layer * H + it.kv_head;
+      if (it.tok_end != kv_len[((int64_t)it.b * L + layer) * H + it.kv_head]) continue;
+      const int64_t t = ((int64_t)it.b * L + layer) * G + group_of[lh];
+      it.tok_end = (int32_t)(-(pt_offsets[t + 1] - pt_offsets[t]) * geom->page_size);
+    }
+    return TG_OK;
+  });
 }
 
 // Ahead-of-time workgroup schedule of tg_prefill: LPT placement of the
@@ -522,66 +553,68 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
 int32_t tg_prefill_schedule(const tg_geometry* geom, int32_t batch, int32_t chunk_len, int32_t layer,
                             const int32_t* kv_len, int32_t n_xcd, int32_t* order, int32_t capacity,
                             int32_t* num_blocks) {
-  if (int32_t rc = tg::check_geometry(geom)) return rc;
-  if (!kv_len || !num_blocks) return fail(TG_ERR_INVALID_ARG, "NULL array");
-  if (batch < 1 || chunk_len < 1) return fail(TG_ERR_INVALID_ARG, "batch and chunk_len must be >= 1");
-  if (layer < 0 || layer >= geom->num_layers) return fail(TG_ERR_INVALID_ARG, "layer %d out of range", layer);
-  if (n_xcd < 1 || n_xcd > 64) return fail(TG_ERR_INVALID_ARG, "n_xcd must be in 1..64");
-  const int64_t L = geom->num_layers, H = geom->num_kv_heads, gqa = geom->num_q_heads / geom->num_kv_heads;
-  const int64_t C = chunk_len, rows = C * gqa;
-  const int64_t row_tiles = tg::ceil_div(rows, TG_PREFILL_ROWS);
-  const int64_t n_units = (int64_t)batch * H;
-  if (n_units * row_tiles > INT32_MAX / 2) return fail(TG_ERR_INVALID_ARG, "too many prefill blocks");
-  // cost of every block and unit
-  std::vector<int64_t> chunk_tiles(row_tiles), unit_cost(n_units);
-  for (int64_t rt = 0; rt < row_tiles; ++rt) {
-    const int64_t i_last = std::min(C - 1, (std::min((rt + 1) * TG_PREFILL_ROWS, rows) - 1) / gqa);
-    chunk_tiles[rt] = i_last / TG_PREFILL_TILE + 1;
-  }
-  std::vector<int64_t> hist_tiles(n_units);
-  for (int64_t u = 0; u < n_units; ++u) {
-    const int64_t b = u / H, h = u % H;
-    const int64_t len = kv_len[(b * L + layer) * H + h];
-    if (len < 0) return fail(TG_ERR_INVALID_ARG, "negative kv_len at request %lld head %lld", (long long)b,
-                             (long long)h);
-    hist_tiles[u] = tg::ceil_div(len, TG_PREFILL_TILE);
-    unit_cost[u] = 0;
-    for (int64_t rt = 0; rt < row_tiles; ++rt) unit_cost[u] += hist_tiles[u] + chunk_tiles[rt];
-  }
-  // units to XCDs, longest first, each to the least-loaded XCD (ties: lowest index)
-  std::vector<int64_t> units(n_units);
-  for (int64_t u = 0; u < n_units; ++u) units[u] = u;
-  std::stable_sort(units.begin(), units.end(),
-                   [&](int64_t a, int64_t b) { return unit_cost[a] > unit_cost[b]; });
-  std::vector<int64_t> load(n_xcd, 0);
-  std::vector<std::vector<std::pair<int64_t, int64_t>>> blocks(n_xcd);   // (u, rt)
-  for (int64_t u : units) {
-    int x = 0;
-    for (int k = 1; k < n_xcd; ++k)
-      if (load[k] < load[x]) x = k;
-    load[x] += unit_cost[u];
-    for (int64_t rt = 0; rt < row_tiles; ++rt) blocks[x].emplace_back(u, rt);
-  }
-  size_t longest = 0;
-  for (auto& v : blocks) {
-    std::stable_sort(v.begin(), v.end(), [&](const std::pair<int64_t, int64_t>& a, const std::pair<int64_t, int64_t>& b) {
-      const int64_t ca = hist_tiles[a.first] + chunk_tiles[a.second];
-      const int64_t cb = hist_tiles[b.first] + chunk_tiles[b.second];
-      if (ca != cb) return ca > cb;
-      return a < b;
-    });
-    longest = std::max(longest, v.size());
-  }
-  const int64_t total = (int64_t)n_xcd * (int64_t)longest;
-  *num_blocks = (int32_t)total;
-  if (!order) return TG_OK;   // size query
-  if (capacity < total) return fail(TG_ERR_BUFFER_TOO_SMALL, "order holds %d, need %lld", capacity, (long long)total);
-  for (int64_t k = 0; k < total; ++k) {
-    const auto& v = blocks[k % n_xcd];
-    const size_t j = (size_t)(k / n_xcd);
-    order[k] = j < v.size() ? (int32_t)(v[j].first * row_tiles + v[j].second) : -1;
-  }
-  return TG_OK;
+  return guarded([&]() -> int32_t {
+    if (int32_t rc = tg::check_geometry(geom)) return rc;
+    if (!kv_len || !num_blocks) return fail(TG_ERR_INVALID_ARG, "NULL array");
+    if (batch < 1 || chunk_len < 1) return fail(TG_ERR_INVALID_ARG, "batch and chunk_len must be >= 1");
+    if (layer < 0 || layer >= geom->num_layers) return fail(TG_ERR_INVALID_ARG, "layer %d out of range", layer);
+    if (n_xcd < 1 || n_xcd > 64) return fail(TG_ERR_INVALID_ARG, "n_xcd must be in 1..64");
+    const int64_t L = geom->num_layers, H = geom->num_kv_heads, gqa = geom->num_q_heads / geom->num_kv_heads;
+    const int64_t C = chunk_len, rows = C * gqa;
+    const int64_t row_tiles = tg::ceil_div(rows, TG_PREFILL_ROWS);
+    const int64_t n_units = (int64_t)batch * H;
+    if (n_units * row_tiles > INT32_MAX / 2) return fail(TG_ERR_INVALID_ARG, "too many prefill blocks");
+    // cost of every block and unit
+    std::vector<int64_t> chunk_tiles(row_tiles), unit_cost(n_units);
+    for (int64_t rt = 0; rt < row_tiles; ++rt) {
+      const int64_t i_last = std::min(C - 1, (std::min((rt + 1) * TG_PREFILL_ROWS, rows) - 1) / gqa);
+      chunk_tiles[rt] = i_last / TG_PREFILL_TILE + 1;
+    }
+    std::vector<int64_t> hist_tiles(n_units);
+    for (int64_t u = 0; u < n_units; ++u) {
+      const int64_t b = u / H, h = u % H;
+      const int64_t len = kv_len[(b * L + layer) * H + h];
+      if (len < 0) return fail(TG_ERR_INVALID_ARG, "negative kv_len at request %lld head %lld", (long long)b,
+                               (long long)h);
+      hist_tiles[u] = tg::ceil_div(len, TG_PREFILL_TILE);
+      unit_cost[u] = 0;
+      for (int64_t rt = 0; rt < row_tiles; ++rt) unit_cost[u] += hist_tiles[u] + chunk_tiles[rt];
+    }
+    // units to XCDs, longest first, each to the least-loaded XCD (ties: lowest index)
+    std::vector<int64_t> units(n_units);
+    for (int64_t u = 0; u < n_units; ++u) units[u] = u;
+    std::stable_sort(units.begin(), units.end(),
+                     [&](int64_t a, int64_t b) { return unit_cost[a] > unit_cost[b]; });
+    std::vector<int64_t> load(n_xcd, 0);
+    std::vector<std::vector<std::pair<int64_t, int64_t>>> blocks(n_xcd);   // (u, rt)
+    for (int64_t u : units) {
+      int x = 0;
+      for (int k = 1; k < n_xcd; ++k)
+        if (load[k] < load[x]) x = k;
+      load[x] += unit_cost[u];
+      for (int64_t rt = 0; rt < row_tiles; ++rt) blocks[x].emplace_back(u, rt);
+    }
+    size_t longest = 0;
+    for (auto& v : blocks) {
+      std::stable_sort(v.begin(), v.end(), [&](const std::pair<int64_t, int64_t>& a, const std::pair<int64_t, int64_t>& b) {
+        const int64_t ca = hist_tiles[a.first] + chunk_tiles[a.second];
+        const int64_t cb = hist_tiles[b.first] + chunk_tiles[b.second];
+        if (ca != cb) return ca > cb;
+        return a < b;
+      });
+      longest = std::max(longest, v.size());
+    }
+    const int64_t total = (int64_t)n_xcd * (int64_t)longest;
+    *num_blocks = (int32_t)total;
+    if (!order) return TG_OK;   // size query
+    if (capacity < total) return fail(TG_ERR_BUFFER_TOO_SMALL, "order holds %d, need %lld", capacity, (long long)total);
+    for (int64_t k = 0; k < total; ++k) {
+      const auto& v = blocks[k % n_xcd];
+      const size_t j = (size_t)(k / n_xcd);
+      order[k] = j < v.size() ? (int32_t)(v[j].first * row_tiles + v[j].second) : -1;
+    }
+    return TG_OK;
+  });
 }
 
 }  // extern "C"
@@ -595,81 +628,83 @@ extern "C" int32_t tg_compress_plan(const tg_geometry* geom, int32_t batch, int3
                                     const int32_t* group_of, const int32_t* slot_of, int32_t rows_per_item,
                                     tg_compress_item* items, int32_t item_capacity, int32_t* keep_count,
                                     int32_t* write_begin, int32_t* num_items) {
-  if (int32_t rc = tg::check_geometry(geom)) return rc;
-  if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
-  const int L = geom->num_layers, H = geom->num_kv_heads, Hp = geom->heads_per_group, G = H / Hp;
-  const int64_t P = geom->page_size;
-  if (layer < 0 || layer >= L) return fail(TG_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, L);
-  if (chunk_len < 1 || chunk_len > TG_COMPRESS_MAX_CHUNK)
-    return fail(TG_ERR_INVALID_ARG, "chunk_len %d outside [1, %d]", chunk_len, (int)TG_COMPRESS_MAX_CHUNK);
-  if (rows_per_item < 1 || rows_per_item > TG_COMPRESS_MAX_ROWS)
-    return fail(TG_ERR_INVALID_ARG, "rows_per_item %d outside [1, %d]", rows_per_item, (int)TG_COMPRESS_MAX_ROWS);
-  if (!chunk_start || !chunk_tokens || !kv_len || !pt_offsets || !group_of || !slot_of || !keep_count ||
-      !write_begin || !num_items)
-    return fail(TG_ERR_INVALID_ARG, "NULL array");
-  if (!ratio && !budget) return fail(TG_ERR_INVALID_ARG, "ratio and budget are both NULL");
-  if (item_capacity < 0) return fail(TG_ERR_INVALID_ARG, "negative item_capacity");
-  for (int h = 0; h < H; ++h) {
-    const int64_t i = (int64_t)layer * H + h;
-    if (group_of[i] < 0 || group_of[i] >= G || slot_of[i] < 0 || slot_of[i] >= Hp)
-      return fail(TG_ERR_INVALID_ARG, "group_of / slot_of of head %d out of range", h);
-  }
-  // validate everything before writing anything
-  for (int b = 0; b < batch; ++b) {
-    if (chunk_start[b] < 0) return fail(TG_ERR_INVALID_ARG, "chunk_start[%d] < 0", b);
-    if (chunk_tokens[b] < 0 || chunk_tokens[b] > chunk_len)
-      return fail(TG_ERR_INVALID_ARG, "chunk_tokens[%d] = %d outside [0, %d]", b, chunk_tokens[b], chunk_len);
-    if ((int64_t)chunk_start[b] + chunk_tokens[b] > INT32_MAX)
-      return fail(TG_ERR_INVALID_ARG, "chunk_start + chunk_tokens of request %d overflows int32", b);
+  return guarded([&]() -> int32_t {
+    if (int32_t rc = tg::check_geometry(geom)) return rc;
+    if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
+    const int L = geom->num_layers, H = geom->num_kv_heads, Hp = geom->heads_per_group, G = H / Hp;
+    const int64_t P = geom->page_size;
+    if (layer < 0 || layer >= L) return fail(TG_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, L);
+    if (chunk_len < 1 || chunk_len > TG_COMPRESS_MAX_CHUNK)
+      return fail(TG_ERR_INVALID_ARG, "chunk_len %d outside [1, %d]", chunk_len, (int)TG_COMPRESS_MAX_CHUNK);
+    if (rows_per_item < 1 || rows_per_item > TG_COMPRESS_MAX_ROWS)
+      return fail(TG_ERR_INVALID_ARG, "rows_per_item %d outside [1, %d]", rows_per_item, (int)TG_COMPRESS_MAX_ROWS);
+    if (!chunk_start || !chunk_tokens || !kv_len || !pt_offsets || !group_of || !slot_of || !keep_count ||
+        !write_begin || !num_items)
+      return fail(TG_ERR_INVALID_ARG, "NULL array");
+    if (!ratio && !budget) return fail(TG_ERR_INVALID_ARG, "ratio and budget are both NULL");
+    if (item_capacity < 0) return fail(TG_ERR_INVALID_ARG, "negative item_capacity");
     for (int h = 0; h < H; ++h) {
-      const int64_t i = ((int64_t)b * L + layer) * H + h;
-      const double r = ratio ? ratio[i] : budget[(int64_t)layer * H + h];
-      if (!tg::ratio_ok(r)) return fail(TG_ERR_INVALID_ARG, "ratio of request %d head %d outside (0,1]", b, h);
-      if (kv_len[i] < 0) return fail(TG_ERR_INVALID_ARG, "kv_len of request %d head %d < 0", b, h);
-      const int64_t t = ((int64_t)b * L + layer) * G + group_of[(int64_t)layer * H + h];
-      if ((pt_offsets[t + 1] - pt_offsets[t]) * P < kv_len[i])
-        return fail(TG_ERR_INVALID_ARG, "page table of request %d head %d holds fewer than kv_len entries", b, h);
+      const int64_t i = (int64_t)layer * H + h;
+      if (group_of[i] < 0 || group_of[i] >= G || slot_of[i] < 0 || slot_of[i] >= Hp)
+        return fail(TG_ERR_INVALID_ARG, "group_of / slot_of of head %d out of range", h);
     }
-  }
-  int64_t n_items = 0;
-  for (int b = 0; b < batch; ++b) {
-    const double c0 = (double)chunk_start[b], c1 = (double)chunk_start[b] + (double)chunk_tokens[b];
-    for (int h = 0; h < H; ++h) {
-      const int64_t i = ((int64_t)b * L + layer) * H + h;
-      const double r = ratio ? ratio[i] : budget[(int64_t)layer * H + h];
-      const int64_t cap = kv_len[i];
-      const int64_t cursor = std::min((int64_t)std::ceil(r * c0), cap);
-      const int64_t end = std::min((int64_t)std::ceil(r * c1), cap);
-      keep_count[(int64_t)b * H + h] = (int32_t)(end - cursor);
-      write_begin[(int64_t)b * H + h] = (int32_t)cursor;
-      n_items += ceil_div(end - cursor, rows_per_item);
-    }
-  }
-  if (n_items > INT32_MAX) return fail(TG_ERR_INVALID_ARG, "too many work items");
-  *num_items = (int32_t)n_items;
-  if (!items) return TG_OK;
-  if (item_capacity < n_items)
-    return fail(TG_ERR_BUFFER_TOO_SMALL, "items holds %d, need %lld", item_capacity, (long long)n_items);
-  int64_t k = 0;
-  for (int b = 0; b < batch; ++b)
-    for (int h = 0; h < H; ++h) {
-      const int32_t cnt = keep_count[(int64_t)b * H + h];
-      const int64_t lh = (int64_t)layer * H + h;
-      const int64_t base = pt_offsets[((int64_t)b * L + layer) * G + group_of[lh]];
-      for (int32_t r0 = 0; r0 < cnt; r0 += rows_per_item) {
-        tg_compress_item& it = items[k++];
-        it.pt_base = base;
-        it.b = b;
-        it.kv_head = h;
-        it.slot = slot_of[lh];
-        it.n_valid = chunk_tokens[b];
-        it.cursor = write_begin[(int64_t)b * H + h];
-        it.count = cnt;
-        it.rank_begin = r0;
-        it.rank_end = std::min(cnt, r0 + rows_per_item);
+    // validate everything before writing anything
+    for (int b = 0; b < batch; ++b) {
+      if (chunk_start[b] < 0) return fail(TG_ERR_INVALID_ARG, "chunk_start[%d] < 0", b);
+      if (chunk_tokens[b] < 0 || chunk_tokens[b] > chunk_len)
+        return fail(TG_ERR_INVALID_ARG, "chunk_tokens[%d] = %d outside [0, %d]", b, chunk_tokens[b], chunk_len);
+      if ((int64_t)chunk_start[b] + chunk_tokens[b] > INT32_MAX)
+        return fail(TG_ERR_INVALID_ARG, "chunk_start + chunk_tokens of request %d overflows int32", b);
+      for (int h = 0; h < H; ++h) {
+        const int64_t i = ((int64_t)b * L + layer) * H + h;
+        const double r = ratio ? ratio[i] : budget[(int64_t)layer * H + h];
+        if (!tg::ratio_ok(r)) return fail(TG_ERR_INVALID_ARG, "ratio of request %d head %d outside (0,1]", b, h);
+        if (kv_len[i] < 0) return fail(TG_ERR_INVALID_ARG, "kv_len of request %d head %d < 0", b, h);
+        const int64_t t = ((int64_t)b * L + layer) * G + group_of[(int64_t)layer * H + h];
+        if ((pt_offsets[t + 1] - pt_offsets[t]) * P < kv_len[i])
+          return fail(TG_ERR_INVALID_ARG, "page table of request %d head %d holds fewer than kv_len entries", b, h);
       }
     }
-  return TG_OK;
+    int64_t n_items = 0;
+    for (int b = 0; b < batch; ++b) {
+      const double c0 = (double)chunk_start[b], c1 = (double)chunk_start[b] + (double)chunk_tokens[b];
+      for (int h = 0; h < H; ++h) {
+        const int64_t i = ((int64_t)b * L + layer) * H + h;
+        const double r = ratio ? ratio[i] : budget[(int64_t)layer * H + h];
+        const int64_t cap = kv_len[i];
+        const int64_t cursor = std::min((int64_t)std::ceil(r * c0), cap);
+        const int64_t end = std::min((int64_t)std::ceil(r * c1), cap);
+        keep_count[(int64_t)b * H + h] = (int32_t)(end - cursor);
+        write_begin[(int64_t)b * H + h] = (int32_t)cursor;
+        n_items += ceil_div(end - cursor, rows_per_item);
+      }
+    }
+    if (n_items > INT32_MAX) return fail(TG_ERR_INVALID_ARG, "too many work items");
+    *num_items = (int32_t)n_items;
+    if (!items) return TG_OK;
+    if (item_capacity < n_items)
+      return fail(TG_ERR_BUFFER_TOO_SMALL, "items holds %d, need %lld", item_capacity, (long long)n_items);
+    int64_t k = 0;
+    for (int b = 0; b < batch; ++b)
+      for (int h = 0; h < H; ++h) {
+        const int32_t cnt = keep_count[(int64_t)b * H + h];
+        const int64_t lh = (int64_t)layer * H + h;
+        const int64_t base = pt_offsets[((int64_t)b * L + layer) * G + group_of[lh]];
+        for (int32_t r0 = 0; r0 < cnt; r0 += rows_per_item) {
+          tg_compress_item& it = items[k++];
+          it.pt_base = base;
+          it.b = b;
+          it.kv_head = h;
+          it.slot = slot_of[lh];
+          it.n_valid = chunk_tokens[b];
+          it.cursor = write_begin[(int64_t)b * H + h];
+          it.count = cnt;
+          it.rank_begin = r0;
+          it.rank_end = std::min(cnt, r0 + rows_per_item);
+        }
+      }
+    return TG_OK;
+  });
 }
 
 // KV slots allocated by each paging scheme for the same retained lengths
@@ -677,47 +712,49 @@ extern "C" int32_t tg_compress_plan(const tg_geometry* geom, int32_t batch, int3
 extern "C" int32_t tg_memory_footprint(const tg_geometry* geom, int32_t batch, const int32_t* ctx_len,
                                        const double* ratio, const double* budget, const int32_t* group_of,
                                        tg_footprint* out) {
-  if (int32_t rc = tg::check_geometry(geom)) return rc;
-  if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
-  if (!ctx_len || !group_of || !out) return fail(TG_ERR_INVALID_ARG, "NULL array");
-  if (!ratio && !budget) return fail(TG_ERR_INVALID_ARG, "ratio and budget are both NULL");
-  const int L = geom->num_layers, H = geom->num_kv_heads, Hp = geom->heads_per_group, G = H / Hp;
-  const int64_t P = geom->page_size;
-  for (int64_t i = 0; i < (int64_t)L * H; ++i)
-    if (group_of[i] < 0 || group_of[i] >= G) return fail(TG_ERR_INVALID_ARG, "group_of[%lld] out of range", (long long)i);
-  for (int b = 0; b < batch; ++b) {
-    if (ctx_len[b] < 1) return fail(TG_ERR_INVALID_ARG, "ctx_len[%d] < 1", b);
-    for (int64_t i = 0; i < (int64_t)L * H; ++i) {
-      const double r = ratio ? ratio[(int64_t)b * L * H + i] : budget[i];
-      if (!tg::ratio_ok(r)) return fail(TG_ERR_INVALID_ARG, "ratio of request %d entry %lld outside (0,1]", b, (long long)i);
-    }
-  }
-  tg_footprint f = {0, 0, 0, 0, 0, (int64_t)batch * L * G};
-  std::vector<int64_t> gl(G);
-  for (int b = 0; b < batch; ++b) {
-    const double n = (double)ctx_len[b];
-    f.full_slots += ceil_div(ctx_len[b], P) * P * L * H;
-    int64_t longest = 0;
-    for (int l = 0; l < L; ++l) {
-      std::fill(gl.begin(), gl.end(), 0);
-      for (int h = 0; h < H; ++h) {
-        const int64_t i = (int64_t)l * H + h;
+  return guarded([&]() -> int32_t {
+    if (int32_t rc = tg::check_geometry(geom)) return rc;
+    if (batch < 1) return fail(TG_ERR_INVALID_ARG, "batch must be >= 1");
+    if (!ctx_len || !group_of || !out) return fail(TG_ERR_INVALID_ARG, "NULL array");
+    if (!ratio && !budget) return fail(TG_ERR_INVALID_ARG, "ratio and budget are both NULL");
+    const int L = geom->num_layers, H = geom->num_kv_heads, Hp = geom->heads_per_group, G = H / Hp;
+    const int64_t P = geom->page_size;
+    for (int64_t i = 0; i < (int64_t)L * H; ++i)
+      if (group_of[i] < 0 || group_of[i] >= G) return fail(TG_ERR_INVALID_ARG, "group_of[%lld] out of range", (long long)i);
+    for (int b = 0; b < batch; ++b) {
+      if (ctx_len[b] < 1) return fail(TG_ERR_INVALID_ARG, "ctx_len[%d] < 1", b);
+      for (int64_t i = 0; i < (int64_t)L * H; ++i) {
         const double r = ratio ? ratio[(int64_t)b * L * H + i] : budget[i];
-        const int64_t len = (int64_t)std::ceil(r * n);
-        f.retained_slots += len;
-        longest = std::max(longest, len);
-        gl[group_of[i]] = std::max(gl[group_of[i]], len);
-      }
-      for (int g = 0; g < G; ++g) {
-        const int64_t pages = ceil_div(gl[g], P);
-        f.ragged_pages += pages;
-        f.ragged_slots += pages * P * Hp;
+        if (!tg::ratio_ok(r)) return fail(TG_ERR_INVALID_ARG, "ratio of request %d entry %lld outside (0,1]", b, (long long)i);
       }
     }
-    f.monolithic_slots += ceil_div(longest, P) * P * L * H;
-  }
-  *out = f;
-  return TG_OK;
+    tg_footprint f = {0, 0, 0, 0, 0, (int64_t)batch * L * G};
+    std::vector<int64_t> gl(G);
+    for (int b = 0; b < batch; ++b) {
+      const double n = (double)ctx_len[b];
+      f.full_slots += ceil_div(ctx_len[b], P) * P * L * H;
+      int64_t longest = 0;
+      for (int l = 0; l < L; ++l) {
+        std::fill(gl.begin(), gl.end(), 0);
+        for (int h = 0; h < H; ++h) {
+          const int64_t i = (int64_t)l * H + h;
+          const double r = ratio ? ratio[(int64_t)b * L * H + i] : budget[i];
+          const int64_t len = (int64_t)std::ceil(r * n);
+          f.retained_slots += len;
+          longest = std::max(longest, len);
+          gl[group_of[i]] = std::max(gl[group_of[i]], len);
+        }
+        for (int g = 0; g < G; ++g) {
+          const int64_t pages = ceil_div(gl[g], P);
+          f.ragged_pages += pages;
+          f.ragged_slots += pages * P * Hp;
+        }
+      }
+      f.monolithic_slots += ceil_div(longest, P) * P * L * H;
+    }
+    *out = f;
+    return TG_OK;
+  });
 }
 
 // Order-preserving 32-bit key of an fp32 score: larger number, larger key;
@@ -733,29 +770,31 @@ static inline uint32_t score_key(float f) {
 // Implicit per-head retention ratios of one sample (Eq. 3's layer-wide top-k).
 extern "C" int32_t tg_implicit_ratios(int32_t num_layers, int32_t num_heads, int32_t n_tokens, const float* scores,
                                       double rho, double* ratios, int32_t* counts) {
-  if (num_layers < 1 || num_heads < 1 || n_tokens < 1) return fail(TG_ERR_INVALID_ARG, "L, H and N must be >= 1");
-  if ((int64_t)num_heads * n_tokens >= INT32_MAX) return fail(TG_ERR_INVALID_ARG, "H * N too large");
-  if (!(rho > 0.0 && rho <= 1.0)) return fail(TG_ERR_INVALID_ARG, "rho outside (0, 1]");
-  if (!scores || !ratios) return fail(TG_ERR_INVALID_ARG, "NULL array");
-  const int64_t HN = (int64_t)num_heads * n_tokens;
-  const int64_t k = (int64_t)std::ceil(rho * (double)HN);
-  // composite key: score key, then the lower flattened index first (a total order)
-  std::vector<uint64_t> key((size_t)HN), sorted;
-  for (int l = 0; l < num_layers; ++l) {
-    const float* s = scores + (int64_t)l * HN;
-    for (int64_t i = 0; i < HN; ++i)
-      key[i] = ((uint64_t)score_key(s[i]) << 32) | (uint64_t)(0xffffffffu - (uint32_t)i);
-    sorted = key;
-    std::nth_element(sorted.begin(), sorted.begin() + (k - 1), sorted.end(), std::greater<uint64_t>());
-    const uint64_t kth = sorted[k - 1];
-    for (int h = 0; h < num_heads; ++h) {
-      int64_t c = 0;
-      for (int64_t t = 0; t < n_tokens; ++t) c += key[(int64_t)h * n_tokens + t] >= kth;
-      ratios[(int64_t)l * num_heads + h] = (double)c / (double)n_tokens;
-      if (counts) counts[(int64_t)l * num_heads + h] = (int32_t)c;
+  return guarded([&]() -> int32_t {
+    if (num_layers < 1 || num_heads < 1 || n_tokens < 1) return fail(TG_ERR_INVALID_ARG, "L, H and N must be >= 1");
+    if ((int64_t)num_heads * n_tokens >= INT32_MAX) return fail(TG_ERR_INVALID_ARG, "H * N too large");
+    if (!(rho > 0.0 && rho <= 1.0)) return fail(TG_ERR_INVALID_ARG, "rho outside (0, 1]");
+    if (!scores || !ratios) return fail(TG_ERR_INVALID_ARG, "NULL array");
+    const int64_t HN = (int64_t)num_heads * n_tokens;
+    const int64_t k = (int64_t)std::ceil(rho * (double)HN);
+    // composite key: score key, then the lower flattened index first (a total order)
+    std::vector<uint64_t> key((size_t)HN), sorted;
+    for (int l = 0; l < num_layers; ++l) {
+      const float* s = scores + (int64_t)l * HN;
+      for (int64_t i = 0; i < HN; ++i)
+        key[i] = ((uint64_t)score_key(s[i]) << 32) | (uint64_t)(0xffffffffu - (uint32_t)i);
+      sorted = key;
+      std::nth_element(sorted.begin(), sorted.begin() + (k - 1), sorted.end(), std::greater<uint64_t>());
+      const uint64_t kth = sorted[k - 1];
+      for (int h = 0; h < num_heads; ++h) {
+        int64_t c = 0;
+        for (int64_t t = 0; t < n_tokens; ++t) c += key[(int64_t)h * n_tokens + t] >= kth;
+        ratios[(int64_t)l * num_heads + h] = (double)c / (double)n_tokens;
+        if (counts) counts[(int64_t)l * num_heads + h] = (int32_t)c;
+      }
     }
-  }
-  return TG_OK;
+    return TG_OK;
+  });
 }
 
 // B = min(1, mu + alpha * sigma) over the samples, at least floor.

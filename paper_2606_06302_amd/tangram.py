@@ -16,6 +16,7 @@ import numpy as np
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtangram.so")
 
 TG_OK, TG_ERR_INVALID_ARG, TG_ERR_OUT_OF_PAGES, TG_ERR_BUFFER_TOO_SMALL, TG_ERR_UNSUPPORTED, TG_ERR_HIP = 0, -1, -2, -3, -4, -5
+TG_ERR_NO_MEMORY = -6
 TG_F32, TG_BF16 = 0, 1
 TG_GROUP_CLUSTERED, TG_GROUP_ADJACENT = 0, 1
 TG_PLAN_AOT, TG_PLAN_NAIVE, TG_PLAN_UNIFORM, TG_PLAN_AOT_FILL, TG_PLAN_SPLIT_MAP = 0, 1, 2, 3, 4

@@ -189,6 +189,7 @@ def test_plan_rejects_length_beyond_table():
 def test_status_strings_and_version():
     assert tg.tg_status_string(0) == "ok"
     assert tg.tg_status_string(tg.TG_ERR_OUT_OF_PAGES) == "out of pages"
+    assert tg.tg_status_string(tg.TG_ERR_NO_MEMORY) == "out of host memory"
     assert tg.tg_version() >> 16 == 1
 
 
