@@ -27,13 +27,13 @@ def _oracle(ps, rows):
     for b, qh in rows:
         h = qh // g.gqa
         base = int(t.pt_offsets[(b * L + ps.layer) * G + t.group_of[ps.layer, h]])
-        need.append(t.pt_pages[base: base + (int(t.kv_len[b, ps.layer, h]) + P - 1) // P])
-    idx = np.unique(np.concatenate(need)).astype(np.int64)
+        need.append(t.pt_pages[base: base + (int(ps.hist[b, ps.layer, h]) + P - 1) // P])
+    idx = np.unique(np.concatenate(need + [np.zeros(1, dtype=np.int64)])).astype(np.int64)
     sub = ps.pool[torch.from_numpy(idx).cuda()].float().cpu().numpy().astype(np.float64)
     remap = np.full(t.pool_pages, -1, dtype=np.int64)
     remap[idx] = np.arange(len(idx))
     f = lambda x: x.float().cpu().numpy().astype(np.float64)
-    return oracle.prefill_attention(f(ps.q), f(ps.k_new), f(ps.v_new), sub, ps.layer, geom=g, kv_len=t.kv_len,
+    return oracle.prefill_attention(f(ps.q), f(ps.k_new), f(ps.v_new), sub, ps.layer, geom=g, kv_len=ps.hist,
                                     offsets=t.pt_offsets, pages=remap[t.pt_pages], group_of=t.group_of,
                                     slot_of=t.slot_of, rows=rows)
 
@@ -63,6 +63,23 @@ def test_prefill_small_vs_oracle(gqa, C, Hp, ctx):
     torch.cuda.synchronize()
     rows = [(b, q) for b in range(wl.batch) for q in range(g.num_q_heads)]
     _compare(ps, rows, f"gqa {gqa} C {C}")
+
+
+def test_prefill_short_and_empty_histories():
+    """Histories shorter than the reservation, down to none at all (a prompt's first chunk): heads with 0,
+    1, 15, 16, 17 and 63 retained rows and one with its whole reservation, NaN in every pool row past them."""
+    _gpu()
+    g = Geometry(1, 8, 32, 128, 16, 2)
+    wl = custom(640, g, 3, "bf16", (200, 900), chunk_len=77)
+    tables = Tables(wl)
+    pool = torch.from_numpy(poisoned_host_pool(wl, tables)).to(torch.bfloat16).cuda()
+    hist = np.minimum(tables.kv_len, np.array([0, 1, 15, 16, 17, 63, 10**6, 0], dtype=np.int32)[None, None, :])
+    hist[1] = 0                                   # a request with no history in any head
+    say(f"prefill short histories {hist[:, 0].tolist()}")
+    ps = PrefillSession(wl, tables=tables, fill="host", pool=pool, hist_len=hist)
+    ps.run()
+    torch.cuda.synchronize()
+    _compare(ps, [(b, q) for b in range(wl.batch) for q in range(g.num_q_heads)], "short histories")
 
 
 def test_prefill_chunk_of_one_matches_decode_path():
