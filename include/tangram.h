@@ -332,6 +332,8 @@ int32_t tg_append(const tg_append_args* args, void* hip_stream);
  * (row = i*gqa + j for query head h*gqa + j) of one (b, h); it walks the
  * history and then its causal part of the chunk in tiles of
  * TG_PREFILL_TILE keys.  The result does not depend on block_order.
+ * A history length outside [0, pages of the head's table * page_size] is
+ * clamped to that range on the device.
  * Supported: dtype TG_BF16, head_dim 128, page_size 16, gqa 1..16,
  * chunk_len >= 1.  The kernel needs no workspace (workspace may be NULL). */
 typedef struct {

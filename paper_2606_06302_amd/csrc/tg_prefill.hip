@@ -164,10 +164,13 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
   const TG_CONST int64_t* pt_offsets = (const TG_CONST int64_t*)p.pt_offsets;
   const TG_CONST int32_t* pt_pages = (const TG_CONST int32_t*)p.pt_pages;
 
-  const int hist = kv_len[((int64_t)b * p.num_layers + p.layer) * p.num_kv_heads + h];
   const int grp = group_of[(int64_t)p.layer * p.num_kv_heads + h];
   const int slot = slot_of[(int64_t)p.layer * p.num_kv_heads + h];
-  const int64_t tbase = pt_offsets[((int64_t)b * p.num_layers + p.layer) * p.num_groups + grp];
+  const int64_t tidx = ((int64_t)b * p.num_layers + p.layer) * p.num_groups + grp;
+  const int64_t tbase = pt_offsets[tidx];
+  // the history is clamped to the head's table: [0, pages * page_size]
+  const int64_t cap = (pt_offsets[tidx + 1] - tbase) * kPage;
+  const int hist = (int)max<int64_t>(0, min<int64_t>(kv_len[((int64_t)b * p.num_layers + p.layer) * p.num_kv_heads + h], cap));
   const int npages = (hist + kPage - 1) / kPage;
   const int i_last = min(C - 1, (min(row0 + kRows, rows_total) - 1) / gqa);   // last chunk row of the block
   const int n_hist_tiles = (hist + kTile - 1) / kTile;

@@ -82,6 +82,32 @@ def test_prefill_short_and_empty_histories():
     _compare(ps, [(b, q) for b in range(wl.batch) for q in range(g.num_q_heads)], "short histories")
 
 
+def test_prefill_history_lengths_are_clamped_to_the_table():
+    """A history length past the head's table, or below zero, is clamped to [0, pages * page_size] on the
+    device: the output equals the oracle's over the clamped lengths."""
+    _gpu()
+    g = Geometry(1, 8, 32, 128, 16, 2)
+    wl = custom(652, g, 2, "bf16", (100, 700), chunk_len=40)
+    tables = Tables(wl)
+    L, G, P = g.num_layers, g.num_groups, g.page_size
+    cap = np.zeros_like(tables.kv_len)
+    for b in range(wl.batch):
+        for h in range(g.num_kv_heads):
+            t = (b * L) * G + int(tables.group_of[0, h])
+            cap[b, 0, h] = (int(tables.pt_offsets[t + 1]) - int(tables.pt_offsets[t])) * P
+    raw = tables.kv_len.copy()
+    raw[0, 0, :4] = cap[0, 0, :4] + np.array([1, 16, 1000, 2 ** 30])
+    raw[1, 0, 0] = -5
+    raw[1, 0, 1] = np.iinfo(np.int32).min
+    say(f"prefill raw lengths {raw[:, 0].tolist()} capacity {cap[:, 0].tolist()}")
+    # every reserved row holds data here: clamping to the capacity makes rows past kv_len part of the history
+    ps = PrefillSession(wl, tables=tables, fill="host", hist_len=raw, schedule=False)
+    ps.run()
+    torch.cuda.synchronize()
+    ps.hist = np.clip(raw, 0, cap).astype(np.int32)   # what the oracle is given
+    _compare(ps, [(b, q) for b in range(wl.batch) for q in range(g.num_q_heads)], "clamped lengths")
+
+
 def test_prefill_chunk_of_one_matches_decode_path():
     """C = 1: the prefill kernel and the decode kernel see the same keys when the
     decode cache holds the chunk's key; both must match the oracle."""
