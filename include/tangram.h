@@ -240,6 +240,9 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
  *   pt_pages CSR page ids (device copy of tg_reserve's output)
  *   items [num_items], bin_offsets [n_bins+1], unit_splits [B][H],
  *   unit_partial_base [B][H]: device copies of tg_build_plan's output
+ *            for the same tables; the kernels read page ids
+ *            pt_pages[pt_base + t / P] for t in [tok_begin, tok_end) of
+ *            every item without re-checking them against the tables
  *   out      [B][Hq][d] dtype, written for every (b, qh)
  *   lse      [B][Hq] float32 natural-log normaliser, or NULL
  *   workspace >= tg_decode_workspace_bytes(geom, batch, num_partials) bytes
