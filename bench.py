@@ -237,7 +237,7 @@ def bench_prefill(args):
             pre_ms += ev[0].elapsed_time(ev[1]) / nrep
             comp_ms += ev[1].elapsed_time(ev[2]) / nrep
     # timing protocol: per-step events after a MALL flush (the chunk's history fits the 256 MB MALL)
-    med, p10, p90 = step_stats(lambda: (s.run(stream), cs.run(stream)), stream, max(args.steps, 20), True)
+    med, p10, p90 = step_stats(lambda: (s.run(stream), cs.run(stream)), stream, max(args.steps, 50), True)
     tflops = flops / (med * 1e-3) / 1e12
     pre_tflops = flops / (pre_ms * 1e-3) / 1e12
     comp_gbs = comp_bytes / (comp_ms * 1e-3) / 1e9
@@ -536,8 +536,8 @@ def bench_lifecycle(args):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--mode", default="fill", choices=["aot", "fill", "naive", "uniform", "splitmap"])
     ap.add_argument("--n-bins", type=int, default=0)
@@ -640,7 +640,7 @@ def main():
         # MALL are flushed before every step (the 64-layer step streams ~85 GB and needs no flush)
         flush = g.num_layers == 1
         med, p10, p90 = step_stats((lambda: graph.replay()) if graph is not None else (lambda: s.run_step(stream)),
-                                   stream, max(args.steps, 20), flush)
+                                   stream, max(args.steps, 50), flush)
         # per-launch timing of the decode call (roofline), events on the launch stream
         nrep = max(1, min(args.steps, 5))
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in s.layers]
