@@ -37,16 +37,18 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 HBM_PEAK_GBS = 8000.0
 METRIC = "ragged paged decode attn: KV GB/s, % of HBM peak, µs/decode step"
 DECODE_SRC = os.path.join(ROOT, "paper_2606_06302_amd", "csrc", "tg_decode.hip")
+PREFILL_SRC = os.path.join(ROOT, "paper_2606_06302_amd", "csrc", "tg_prefill.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_traffic.json")
+PREFILL_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "prefill_traffic.json")
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def source_sha():
+def source_sha(src=DECODE_SRC):
     h = hashlib.sha256()
-    for p in (DECODE_SRC, os.path.join(ROOT, "paper_2606_06302_amd", "csrc", "tg_device.h")):
+    for p in (src, os.path.join(ROOT, "paper_2606_06302_amd", "csrc", "tg_device.h")):
         h.update(open(p, "rb").read())
     return h.hexdigest()[:16]
 
@@ -61,14 +63,14 @@ def copy_probe(nbytes):
     print(json.dumps({"copy_probe_bytes": nbytes}))
 
 
-def measured_traffic(workload, mode, n_bins):
-    """HBM bytes per decode launch from committed rocprofv3 counter runs, if they
-    were taken on the current decode source and the same plan; else None."""
+def measured_traffic(workload, mode=None, n_bins=None, path=TRAFFIC_FILE, src=DECODE_SRC):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they were
+    taken on the current kernel source and the same workload (and plan); else None."""
     try:
-        rec = json.load(open(TRAFFIC_FILE))
+        rec = json.load(open(path))
     except (OSError, ValueError):
         return None
-    if (rec.get("source_sha") != source_sha() or rec.get("workload") != workload or rec.get("mode") != mode
+    if (rec.get("source_sha") != source_sha(src) or rec.get("workload") != workload or rec.get("mode") != mode
             or rec.get("n_bins") != n_bins):
         return None
     return rec.get("hbm_bytes_per_launch")
@@ -253,7 +255,9 @@ def bench_prefill(args):
                    "flops_per_step": flops, "step": "chunk attention over the compressed history, then the "
                    "chunk's K/V compressed into the reserved pages", "parallelism": "single GPU"},
         "roofline": {"bound": "mfma", "achieved": round(pre_tflops, 2), "peak": MFMA_BF16_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(pre_tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "unit": "TFLOP/s", "frac": round(pre_tflops / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "traffic": measured_traffic(wl.name, path=PREFILL_TRAFFIC_FILE, src=PREFILL_SRC),
+                     "min_hbm_bytes_per_launch": s.min_hbm_bytes(),
                      "kernel": "tg_prefill_kernel", "avg_launch_us": round(pre_ms * 1e3, 2),
                      "algorithmic_flops_per_launch": flops},
         "compress": {"bound": "hbm", "achieved": round(comp_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",

@@ -297,6 +297,15 @@ class PrefillSession:
     def run(self, stream=None):
         tg.tg_prefill(self.args, stream)
 
+    def min_hbm_bytes(self) -> int:
+        """Bytes one launch must move at least: Q, each KV head's retained history and chunk K/V read once,
+        the output written once."""
+        g, wl = self.wl.geom, self.wl
+        esz = self.q.element_size()
+        B, C, d = wl.batch, wl.chunk_len, g.head_dim
+        hist = int(self.hist[:, self.layer, :].astype(np.int64).sum())
+        return int(esz * d * (2 * B * C * g.num_q_heads + 2 * B * C * g.num_kv_heads + 2 * hist))
+
     def flops(self) -> int:
         """Algorithmic flops: 4*d per (query row, visible key) for q.k and p.v."""
         g, wl = self.wl.geom, self.wl
