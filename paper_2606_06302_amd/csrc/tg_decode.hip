@@ -367,9 +367,11 @@ __device__ __forceinline__ uint32_t lds_address(const void* ptr) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const TG_LDS void*)ptr));
 }
 
-// 16 bytes per lane from global memory into LDS at m0_base + 16 * lane.
+// 16 bytes per lane from global memory into LDS at m0_base + 16 * lane.  A
+// decode step reads every retained K/V byte exactly once, so the loads carry
+// the non-temporal (streaming) policy, at device scope.
 __device__ __forceinline__ void lds_dma16(const void* src, uint32_t m0_base) {
-  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(m0_base) : "memory");
+  asm volatile("global_load_lds_dwordx4 %0, off nt sc1" ::"v"(src), "{m0}"(m0_base) : "memory");
 }
 
 // vmcnt(n) with expcnt/lgkmcnt left alone; the memory clobber keeps LDS reads

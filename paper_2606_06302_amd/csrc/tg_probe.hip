@@ -6,7 +6,8 @@
 // 16-byte vector loads, two (K, V) slab pairs in flight, folds every word
 // into an XOR and stores one checksum word.  Few registers per wave, so many
 // waves per SIMD keep loads in flight.  No arithmetic beyond the XOR and no
-// LDS: the time is the time to stream the bytes.
+// LDS: the time is the time to stream the bytes.  The loads are non-temporal,
+// the cache policy of the decode kernel's page reads.
 #include <hip/hip_runtime.h>
 
 #include "tg_internal.h"
@@ -49,8 +50,8 @@ __global__ __launch_bounds__(kThreads) void tg_read_probe_kernel(ProbeParams p) 
         const u4* vv = p.pool + ((page * 2 + 1) * p.hp + slot) * p.slab_u4;
 #pragma unroll
         for (int j = 0; j < PL; ++j) {
-          v[u][0][j] = k[j * 64 + lane];
-          v[u][1][j] = vv[j * 64 + lane];
+          v[u][0][j] = __builtin_nontemporal_load(k + j * 64 + lane);
+          v[u][1][j] = __builtin_nontemporal_load(vv + j * 64 + lane);
         }
       }
     }
