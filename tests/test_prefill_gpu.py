@@ -108,6 +108,23 @@ def test_prefill_history_lengths_are_clamped_to_the_table():
     _compare(ps, [(b, q) for b in range(wl.batch) for q in range(g.num_q_heads)], "clamped lengths")
 
 
+def test_prefill_long_chunk_sampled():
+    """A 4096-token chunk at gqa 8 (32768 query rows per unit, 128 row tiles, 64 chunk tiles): sampled
+    (request, query head) rows over every chunk position against the oracle."""
+    _gpu()
+    g = Geometry(1, 4, 32, 128, 16, 2)
+    wl = custom(661, g, 2, "bf16", (500, 3000), chunk_len=4096)
+    say(f"prefill long chunk C={wl.chunk_len} gqa={g.gqa} ctx={wl.ctx_len.tolist()}")
+    tables = Tables(wl)
+    pool = torch.from_numpy(poisoned_host_pool(wl, tables)).to(torch.bfloat16).cuda()
+    ps = PrefillSession(wl, tables=tables, fill="host", pool=pool)
+    ps.run()
+    torch.cuda.synchronize()
+    rows = [(0, 0), (0, 13), (1, 31)]
+    rows.append((int(np.argmax(tables.kv_len[:, 0].max(axis=1))), int(np.argmax(tables.kv_len[:, 0].max(axis=0))) * g.gqa))
+    _compare(ps, sorted(set(rows)), "long chunk")
+
+
 def test_prefill_chunk_of_one_matches_decode_path():
     """C = 1: the prefill kernel and the decode kernel see the same keys when the
     decode cache holds the chunk's key; both must match the oracle."""
