@@ -295,3 +295,29 @@ def test_read_probe_checksums():
         want.append(int(x))
     assert out.cpu().numpy().view(np.uint32).tolist() == want
     assert n == int(sum(-(-(it["tok_end"] - it["tok_begin"]) // 16) for it in s.plans[0]["items"]))
+
+
+def test_random_shapes_and_plans_sweep():
+    """Seeded sweep: 16 random (dtype, head_dim, KV heads, heads per group, gqa, batch, layers, context range,
+    plan mode, bins, split target) cases, every layer against the oracle, pool rows past the retained
+    lengths poisoned with NaN."""
+    _gpu()
+    rng = np.random.default_rng(4242)
+    for case in range(16):
+        dtype = ["f32", "bf16"][int(rng.integers(2))]
+        d = [64, 128][int(rng.integers(2))]
+        H = [1, 2, 4, 8][int(rng.integers(4))]
+        Hp = [x for x in (1, 2, 4, 8) if H % x == 0][int(rng.integers(len([x for x in (1, 2, 4, 8) if H % x == 0])))]
+        gqa = int(rng.integers(1, 17))
+        B, L = int(rng.integers(1, 5)), int(rng.integers(1, 3))
+        lo = int(rng.integers(1, 400))
+        hi = lo + int(rng.integers(0, 2500))
+        mode = int(rng.integers(0, 4))
+        n_bins, st = int(rng.integers(1, 300)), int(rng.integers(1, 500))
+        g = Geometry(L, H, H * gqa, d, 16, Hp)
+        wl = custom(5000 + case, g, B, dtype, (lo, hi) if hi > lo else lo, kv_scale=0.5)
+        say(f"sweep case {case}: {dtype} d{d} H{H} Hp{Hp} gqa{gqa} B{B} L{L} ctx={wl.ctx_len.tolist()} "
+            f"mode {mode} bins {n_bins} split {st}")
+        s = _small_session(wl, mode=mode, n_bins=n_bins, split_target=st)
+        for l in range(L):
+            compare_layer(s, l, what=f"sweep case {case} layer {l}")

@@ -177,3 +177,27 @@ def test_prefill_block_order_does_not_change_results():
         torch.cuda.synchronize()
         assert torch.equal(ps.out, base)
     _compare(ps, [(b, q) for b in range(wl.batch) for q in range(0, 32, 3)], "scheduled")
+
+
+def test_prefill_random_shapes_sweep():
+    """Seeded sweep: 10 random (gqa, KV heads, heads per group, batch, chunk length, context range) cases,
+    every (request, query head) row against the oracle, NaN past the retained history."""
+    _gpu()
+    rng = np.random.default_rng(777)
+    for case in range(10):
+        gqa = int(rng.integers(1, 17))
+        H = [1, 2, 4, 8][int(rng.integers(4))]
+        Hp = [x for x in (1, 2, 4) if H % x == 0][int(rng.integers(len([x for x in (1, 2, 4) if H % x == 0])))]
+        B = int(rng.integers(1, 4))
+        C = int(rng.integers(1, 301))
+        lo = int(rng.integers(1, 300))
+        hi = lo + int(rng.integers(0, 1500))
+        g = Geometry(1, H, H * gqa, 128, 16, Hp)
+        wl = custom(7000 + case, g, B, "bf16", (lo, hi) if hi > lo else lo, chunk_len=C)
+        say(f"prefill sweep case {case}: gqa{gqa} H{H} Hp{Hp} B{B} C{C} ctx={wl.ctx_len.tolist()}")
+        tables = Tables(wl)
+        pool = torch.from_numpy(poisoned_host_pool(wl, tables)).to(torch.bfloat16).cuda()
+        ps = PrefillSession(wl, tables=tables, fill="host", pool=pool)
+        ps.run()
+        torch.cuda.synchronize()
+        _compare(ps, [(b, q) for b in range(B) for q in range(g.num_q_heads)], f"prefill sweep case {case}")
