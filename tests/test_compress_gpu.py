@@ -165,3 +165,30 @@ def test_compress_config5_chunk_full_size():
             written[pages, :, s, rows] = True
     changed = (pool != before).any(dim=-1)
     assert not bool((changed & ~written).any())
+
+
+def test_compress_random_sweep():
+    """Seeded sweep: 8 random (dtype, head_dim, KV heads, heads per group, batch, chunk length, rows per item,
+    selection ratio) cases, each chunk placed anywhere in its context; the whole pool and the kept lists
+    bit-exact against the oracle."""
+    _gpu()
+    rng = np.random.default_rng(9090)
+    for case in range(8):
+        dtype = ["f32", "bf16"][int(rng.integers(2))]
+        d = [64, 128][int(rng.integers(2))]
+        H = [1, 2, 4, 8][int(rng.integers(4))]
+        Hp = [x for x in (1, 2, 4, 8) if H % x == 0][int(rng.integers(len([x for x in (1, 2, 4, 8) if H % x == 0])))]
+        B = int(rng.integers(1, 5))
+        C = int(rng.integers(1, 2001))
+        R = int(rng.integers(1, 257))
+        g = Geometry(1, H, H * 2, d, 16, Hp)
+        ctx = rng.integers(C, 3 * C + 50, size=B).astype(np.int32)
+        wl = custom(9100 + case, g, B, dtype, ctx, chunk_len=C)
+        toks = rng.integers(0, C + 1, size=B).astype(np.int32)
+        starts = np.array([int(rng.integers(0, c - n + 1)) for c, n in zip(ctx, toks)], dtype=np.int32)
+        sel = np.minimum(1.0, wl.ratio * 1.5) if case % 2 else "reserved"
+        say(f"compress sweep case {case}: {dtype} d{d} H{H} Hp{Hp} B{B} C{C} R{R} "
+            f"{'overflow' if case % 2 else 'reserved'} starts={starts.tolist()} toks={toks.tolist()}")
+        tables = Tables(wl)
+        pool = _pool_for(wl, tables)
+        _run_and_check(wl, tables, pool, starts, toks, sel, R, 0, rng)
