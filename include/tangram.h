@@ -562,8 +562,9 @@ int32_t tg_concat_tables(const tg_geometry* geom, int32_t batch_a, const int64_t
  * vector loads, the entries cut into n_workers contiguous ranges (one wave
  * each); worker w stores the XOR of every 32-bit word it read in out[w].
  * DEVICE pointers: kv_pool, page_ids [n], slots [n] (each < H_p), out
- * [n_workers] uint32.  Slab size must be a multiple of 1 KiB up to 8 KiB
- * (else TG_ERR_UNSUPPORTED).  Errors: TG_ERR_INVALID_ARG, TG_ERR_HIP. */
+ * [n_workers] uint32.  The slab (P * d * sizeof(dtype) bytes) must be 2, 4
+ * or 8 KiB (else TG_ERR_UNSUPPORTED, nothing enqueued).  Errors:
+ * TG_ERR_INVALID_ARG, TG_ERR_HIP. */
 int32_t tg_read_probe(const tg_geometry* geom, int32_t dtype, const void* kv_pool, const int32_t* page_ids,
                       const int32_t* slots, int64_t n, int32_t n_workers, uint32_t* out, void* hip_stream);
 

@@ -265,23 +265,35 @@ def gather_head(pool, b, l, h, t0, t1, *, geom, offsets, pages, group_of, slot_o
 
 # ------------------------------------------------------------ Algorithm 1
 
+def _running_sum(values):
+    """Left-to-right fp64 sum starting from 0.0 (the order fixes the rounding)."""
+    total = 0.0
+    for v in values:
+        total += float(v)
+    return total
+
+
 def split_map(budget, perm, heads_per_group, n_cta):
-    """Algorithm 1: S_{l,i} = max(1, round(Phi_{l,i} / tau_l)), tau_l = Omega_l / N_CTA."""
+    """Algorithm 1 (Section 4.3): a head group gets workgroups in proportion to
+    its share of the layer's total budget, and never fewer than one:
+
+        S_{l,i} = max(1, round(Phi_{l,i} / tau_l)),   tau_l = Omega_l / N_CTA,
+
+    Omega_l = the layer's budgets summed over its heads in index order,
+    Phi_{l,i} = the budgets of group i (heads perm[l][i*H_p .. (i+1)*H_p - 1])
+    summed in that order, all in fp64.  round is half away from zero,
+    floor(x + 0.5), not Python's round-half-to-even.  Budgets lie in (0, 1],
+    so Omega_l > 0.
+    """
     budget = np.asarray(budget, dtype=np.float64)
     L, H = budget.shape
     G = H // heads_per_group
-    S = np.ones((L, G), dtype=np.int64)
+    S = np.zeros((L, G), dtype=np.int64)
     for l in range(L):
-        omega = 0.0
-        for h in range(H):
-            omega += float(budget[l, h])
-        if omega == 0.0:
-            continue
-        tau = omega / n_cta
+        tau = _running_sum(budget[l]) / n_cta
+        in_group_order = [budget[l, int(h)] for h in perm[l]]
         for i in range(G):
-            phi = 0.0
-            for j in range(i * heads_per_group, (i + 1) * heads_per_group):
-                phi += float(budget[l, int(perm[l, j])])
+            phi = _running_sum(in_group_order[i * heads_per_group:(i + 1) * heads_per_group])
             S[l, i] = max(1, math.floor(phi / tau + 0.5))
     return S
 

@@ -16,6 +16,7 @@
 #include <queue>
 #include <string>
 #include <utility>
+#include <numeric>
 #include <vector>
 
 #include "tg_internal.h"
@@ -336,7 +337,14 @@ int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_le
   });
 }
 
-// Algorithm 1, fp64, in the paper's order of operations.
+// Algorithm 1's split map: every group of a layer gets workgroups in
+// proportion to its share of the layer's summed budget, at least one,
+//   S[l][g] = max(1, round(Phi[l][g] / tau[l])),  tau[l] = Omega[l] / n_cta,
+// where Omega[l] sums the layer's budgets (heads in index order) and Phi[l][g]
+// the budgets of group g's heads (in the clustering's order), all in fp64.
+// round() is half away from zero (floor(x + 0.5) for x > 0), so the counts of a
+// layer can add up to slightly more or less than n_cta.  Budgets are validated
+// to lie in (0, 1], so Omega > 0 and tau > 0.
 int32_t tg_split_map(const tg_geometry* geom, const double* budget, const int32_t* perm, int32_t n_cta, int32_t* S) {
   if (int32_t rc = tg::check_geometry(geom)) return rc;
   if (!budget || !perm || !S) return fail(TG_ERR_INVALID_ARG, "NULL array");
@@ -346,26 +354,25 @@ int32_t tg_split_map(const tg_geometry* geom, const double* budget, const int32_
     if (!tg::ratio_ok(budget[i])) return fail(TG_ERR_INVALID_ARG, "budget[%lld] outside (0,1]", (long long)i);
     if (perm[i] < 0 || perm[i] >= H) return fail(TG_ERR_INVALID_ARG, "perm[%lld] out of range", (long long)i);
   }
+  std::vector<uint8_t> hit(H);
   for (int l = 0; l < L; ++l) {
-    std::vector<uint8_t> hit(H, 0);
+    std::fill(hit.begin(), hit.end(), 0);
     for (int j = 0; j < H; ++j) {
       if (hit[perm[(int64_t)l * H + j]]) return fail(TG_ERR_INVALID_ARG, "perm of layer %d is not a permutation", l);
       hit[perm[(int64_t)l * H + j]] = 1;
     }
   }
+  // a left-to-right fp64 sum (the order fixes the rounding)
+  auto add_up = [](auto first, auto last) { return std::accumulate(first, last, 0.0); };
+  std::vector<double> sorted(H);
   for (int l = 0; l < L; ++l) {
     const double* bl = budget + (int64_t)l * H;
-    int32_t* Sl = S + (int64_t)l * G;
-    double omega = 0.0;
-    for (int h = 0; h < H; ++h) omega += bl[h];
-    for (int i = 0; i < G; ++i) Sl[i] = 1;
-    if (omega == 0.0) continue;
-    const double tau = omega / (double)n_cta;
-    for (int i = 0; i < G; ++i) {
-      double phi = 0.0;
-      for (int j = i * Hp; j < (i + 1) * Hp; ++j) phi += bl[perm[(int64_t)l * H + j]];
-      const double s = std::floor(phi / tau + 0.5);
-      Sl[i] = s < 1.0 ? 1 : (int32_t)s;
+    const int32_t* pl = perm + (int64_t)l * H;
+    const double tau = add_up(bl, bl + H) / (double)n_cta;
+    for (int j = 0; j < H; ++j) sorted[j] = bl[pl[j]];   // budgets in group order
+    for (int g = 0; g < G; ++g) {
+      const double share = add_up(sorted.begin() + g * Hp, sorted.begin() + (g + 1) * Hp) / tau;
+      S[(int64_t)l * G + g] = (int32_t)std::max(1.0, std::floor(share + 0.5));
     }
   }
   return TG_OK;

@@ -75,8 +75,9 @@ extern "C" int32_t tg_read_probe(const tg_geometry* geom, int32_t dtype, const v
   if (int32_t rc = tg::check_geometry(geom)) return rc;
   if (dtype != TG_F32 && dtype != TG_BF16) return tg::fail(TG_ERR_UNSUPPORTED, "dtype must be f32 or bf16");
   const int64_t slab_bytes = (int64_t)geom->page_size * geom->head_dim * (dtype == TG_F32 ? 4 : 2);
-  if (slab_bytes % 1024 != 0 || slab_bytes > 8192)
-    return tg::fail(TG_ERR_UNSUPPORTED, "slab of %lld bytes: need a multiple of 1 KiB up to 8 KiB", (long long)slab_bytes);
+  // the kernel is instantiated for slabs of 2, 4 and 8 KiB (2, 4 or 8 16-byte loads per lane)
+  if (slab_bytes != 2048 && slab_bytes != 4096 && slab_bytes != 8192)
+    return tg::fail(TG_ERR_UNSUPPORTED, "slab of %lld bytes: need 2, 4 or 8 KiB", (long long)slab_bytes);
   if (n < 0 || n_workers < 1) return tg::fail(TG_ERR_INVALID_ARG, "n < 0 or n_workers < 1");
   if (n > 0 && (!kv_pool || !page_ids || !slots)) return tg::fail(TG_ERR_INVALID_ARG, "NULL device pointer");
   if (!out) return tg::fail(TG_ERR_INVALID_ARG, "out is NULL");
@@ -91,7 +92,13 @@ extern "C" int32_t tg_read_probe(const tg_geometry* geom, int32_t dtype, const v
   p.hp = geom->heads_per_group;
   const int blocks = (n_workers + kWavesPerBlock - 1) / kWavesPerBlock;
   const int pl = p.slab_u4 / 64;
-  auto fn = pl == 2 ? tg_read_probe_kernel<2> : pl == 4 ? tg_read_probe_kernel<4> : tg_read_probe_kernel<8>;
+  void (*fn)(ProbeParams) = nullptr;
+  switch (pl) {
+    case 2: fn = tg_read_probe_kernel<2>; break;
+    case 4: fn = tg_read_probe_kernel<4>; break;
+    case 8: fn = tg_read_probe_kernel<8>; break;
+    default: return tg::fail(TG_ERR_UNSUPPORTED, "slab of %lld bytes", (long long)slab_bytes);
+  }
   hipLaunchKernelGGL(fn, dim3(blocks), dim3(kThreads), 0, static_cast<hipStream_t>(hip_stream), p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "probe launch failed: %s", hipGetErrorString(e));

@@ -29,20 +29,23 @@ static void print_i32(const char* key, const int32_t* v, int n) {
   printf("\n");
 }
 
+#define MAX_ITEMS 128
+
 static void print_plan(const char* key, const tg_geometry* geom, const int32_t* kv_len, const int64_t* offsets,
-                       const int32_t* group_of, const int32_t* slot_of, int32_t mode, int32_t split_target) {
-  tg_work_item items[64];
-  int32_t bin_offsets[9], unit_splits[B * H], unit_base[B * H], n_items, n_bins, n_partials;
+                       const int32_t* group_of, const int32_t* slot_of, int32_t mode, int32_t want_bins,
+                       int32_t split_target) {
+  tg_work_item items[MAX_ITEMS];
+  int32_t bin_offsets[MAX_ITEMS + 1], unit_splits[B * H], unit_base[B * H], n_items, n_bins, n_partials;
   /* size query first: no item array */
-  check(tg_build_plan(geom, B, 0, kv_len, offsets, group_of, slot_of, mode, 8, split_target, NULL, NULL, 0,
-                      bin_offsets, 9, unit_splits, unit_base, &n_items, &n_bins, &n_partials),
+  check(tg_build_plan(geom, B, 0, kv_len, offsets, group_of, slot_of, mode, want_bins, split_target, NULL, NULL, 0,
+                      bin_offsets, MAX_ITEMS + 1, unit_splits, unit_base, &n_items, &n_bins, &n_partials),
         "tg_build_plan (size query)");
-  if (n_items > 64 || n_bins != 8) {
+  if (n_items > MAX_ITEMS || n_bins > MAX_ITEMS) {
     fprintf(stderr, "unexpected plan size %d items, %d bins\n", n_items, n_bins);
     exit(1);
   }
-  check(tg_build_plan(geom, B, 0, kv_len, offsets, group_of, slot_of, mode, 8, split_target, NULL, items, 64,
-                      bin_offsets, 9, unit_splits, unit_base, &n_items, &n_bins, &n_partials),
+  check(tg_build_plan(geom, B, 0, kv_len, offsets, group_of, slot_of, mode, want_bins, split_target, NULL, items,
+                      MAX_ITEMS, bin_offsets, MAX_ITEMS + 1, unit_splits, unit_base, &n_items, &n_bins, &n_partials),
         "tg_build_plan");
   printf("%s_items", key);
   for (int i = 0; i < n_items; ++i)
@@ -54,7 +57,10 @@ static void print_plan(const char* key, const tg_geometry* geom, const int32_t* 
   print_i32(k, bin_offsets, n_bins + 1);
   snprintf(k, sizeof k, "%s_unit_splits", key);
   print_i32(k, unit_splits, B * H);
+  snprintf(k, sizeof k, "%s_unit_partial_base", key);
+  print_i32(k, unit_base, B * H);
   printf("%s_num_partials %d\n", key, n_partials);
+  printf("%s_num_bins %d\n", key, n_bins);
 }
 
 int main(void) {
@@ -93,8 +99,10 @@ int main(void) {
   check(tg_split_map(&geom, budget, perm, 8, S), "tg_split_map");
   print_i32("split_map_ncta8", S, L * G);
 
-  print_plan("plan_aot", &geom, kv_len, offsets, group_of, slot_of, TG_PLAN_AOT, 16);
-  print_plan("plan_fill", &geom, kv_len, offsets, group_of, slot_of, TG_PLAN_AOT_FILL, 1);
+  print_plan("plan_aot", &geom, kv_len, offsets, group_of, slot_of, TG_PLAN_AOT, 8, 16);
+  print_plan("plan_fill", &geom, kv_len, offsets, group_of, slot_of, TG_PLAN_AOT_FILL, 8, 1);
+  print_plan("plan_uniform", &geom, kv_len, offsets, group_of, slot_of, TG_PLAN_UNIFORM, 64, 1);
+  print_plan("plan_naive", &geom, kv_len, offsets, group_of, slot_of, TG_PLAN_NAIVE, 64, 1);
 
   /* an error path: H not divisible by H_p */
   const tg_geometry bad = {L, 3, 6, 64, 16, 2};

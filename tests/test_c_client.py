@@ -54,6 +54,25 @@ def test_split_map_and_plans(client_output):
         assert o[f"{key}_num_partials"] == [gold["num_partials"]], key
 
 
+def test_uniform_and_naive_plans(client_output):
+    """The static-split baselines from plain C: UNIFORM at 64 bins and NAIVE, against the hand values."""
+    from test_oracle_pins import uniform_gold_items
+    o = client_output
+    gold = GOLD["plan_uniform_bins64"]
+    assert o["plan_uniform_items"] == _flat(uniform_gold_items(gold))
+    assert o["plan_uniform_bin_offsets"] == list(range(gold["num_bins"] + 1))
+    assert o["plan_uniform_num_bins"] == [gold["num_bins"]]
+    assert o["plan_uniform_unit_splits"] == _flat(gold["unit_splits"])
+    assert o["plan_uniform_unit_partial_base"] == _flat(gold["unit_partial_base"])
+    assert o["plan_uniform_num_partials"] == [gold["num_partials"]]
+    gold = GOLD["plan_naive"]
+    assert o["plan_naive_items"] == _flat(gold["items"])
+    assert o["plan_naive_bin_offsets"] == gold["bin_offsets"]
+    assert o["plan_naive_num_bins"] == [gold["num_bins"]]
+    assert o["plan_naive_unit_partial_base"] == _flat(gold["unit_partial_base"])
+    assert o["plan_naive_num_partials"] == [0]
+
+
 def test_error_code_and_version(client_output):
     assert client_output["bad_geometry"] == [-1]   # TG_ERR_INVALID_ARG
     assert client_output["version"][0] >> 16 == 1

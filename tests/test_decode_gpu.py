@@ -176,16 +176,36 @@ def test_full_size_config_sampled(cfg):
         torch.cuda.empty_cache()
 
 
-def test_full_size_config3_sampled():
+@pytest.mark.parametrize("plan", ["aot", "fill-graph"])
+def test_full_size_config3_sampled(plan):
+    """Config 3 at full size (64 layers, batch 64).  "fill-graph" is exactly what bench.py times: the
+    sequential-fill plan (TG_PLAN_AOT_FILL) on tg_decode_max_ctas bins, the 64 layers' launches captured in a
+    HIP graph; the replays must equal the eager step bit for bit, and sampled (request, KV head) pairs of
+    sampled layers match the oracle.  "aot" is the LPT-binned proportional plan, run eagerly."""
     _gpu()
     wl = config(3)
-    say(f"config 3 full size: 64 layers, B=64")
-    s = DecodeSession(wl)
+    mode = tg.TG_PLAN_AOT if plan == "aot" else tg.TG_PLAN_AOT_FILL
+    n_cta = tg.tg_decode_max_ctas(wl.geom, tg.TG_BF16, 0)
+    say(f"config 3 full size: 64 layers, B=64, plan {plan}, {n_cta} bins")
+    s = DecodeSession(wl, mode=mode)
+    assert s.n_bins == n_cta
     s.run_step()
     torch.cuda.synchronize()
+    if plan == "fill-graph":
+        eager_out, eager_lse = s.out.clone(), s.lse.clone()
+        st = torch.cuda.Stream()
+        graph = s.capture_step(st)
+        for rep in range(2):
+            s.out.zero_()
+            s.lse.zero_()
+            torch.cuda.synchronize()
+            graph.replay()
+            torch.cuda.synchronize()
+            assert torch.equal(s.out, eager_out) and torch.equal(s.lse, eager_lse), rep
+        del eager_out, eager_lse
     rng = np.random.default_rng(33)
     for layer in sorted(rng.choice(64, size=4, replace=False).tolist()):
-        compare_layer(s, layer, pairs=sample_pairs(wl, 10, seed=layer), what=f"config 3 layer {layer}")
+        compare_layer(s, layer, pairs=sample_pairs(wl, 10, seed=layer), what=f"config 3 {plan} layer {layer}")
     del s
     torch.cuda.empty_cache()
 

@@ -5,6 +5,7 @@ ragged per-group page tables (Eq. 4, Sections 4.1 and 4.2.1), Algorithm 1's
 split map and the balanced partition plan, plus the error contract of
 include/tangram.h.
 """
+import ctypes
 import json
 import os
 
@@ -68,6 +69,25 @@ def test_config1_matches_hand_values_and_oracle():
     assert [list(t) for t in _items_as_tuples(fill["items"])] == GOLD["plan_fill_bins8"]["items"]
     assert fill["bin_offsets"].tolist() == GOLD["plan_fill_bins8"]["bin_offsets"]
 
+
+
+def test_uniform_and_naive_plans_config1_hand():
+    """The library's UNIFORM and NAIVE plans equal the hand-derived config-1 values."""
+    from test_oracle_pins import uniform_gold_items
+    wl = config(1)
+    _, gof, sof = tg.tg_cluster_heads(wl.geom, wl.budget)
+    res = tg.tg_reserve(wl.geom, wl.ctx_len, wl.ratio, None, gof, np.arange(100, dtype=np.int32), 100)
+    gold = GOLD["plan_uniform_bins64"]
+    u = tg.tg_build_plan(wl.geom, 2, 0, res["kv_len"], res["pt_offsets"], gof, sof, tg.TG_PLAN_UNIFORM, 64, 1)
+    assert [list(t) for t in _items_as_tuples(u["items"])] == uniform_gold_items(gold)
+    assert u["num_bins"] == gold["num_bins"] and u["bin_offsets"].tolist() == list(range(57))
+    assert u["unit_splits"].tolist() == gold["unit_splits"] and u["num_partials"] == gold["num_partials"]
+    assert u["unit_partial_base"].tolist() == gold["unit_partial_base"]
+    gold = GOLD["plan_naive"]
+    n = tg.tg_build_plan(wl.geom, 2, 0, res["kv_len"], res["pt_offsets"], gof, sof, tg.TG_PLAN_NAIVE, 64, 1)
+    assert [list(t) for t in _items_as_tuples(n["items"])] == gold["items"]
+    assert n["bin_offsets"].tolist() == gold["bin_offsets"] and n["num_partials"] == 0
+    assert n["unit_partial_base"].tolist() == gold["unit_partial_base"]
 
 @pytest.mark.parametrize("cfg", [1, 2, 4, 5])
 def test_workload_configs_bit_exact(cfg):
@@ -450,6 +470,24 @@ def test_append_launch_validation_on_host():
         with pytest.raises(tg.TangramError) as e:
             tg.tg_append(args)
         assert e.value.code == tg.TG_ERR_INVALID_ARG, kw
+
+
+def test_read_probe_slab_sizes_checked_on_host():
+    """tg_read_probe runs only the 2, 4 and 8 KiB slab kernels: every other slab size is refused before
+    anything is enqueued, and an accepted size goes on to the remaining argument checks (here a zero
+    worker count), so nothing is launched either way."""
+    def call(d, dtype, page_size=16, n_workers=0):
+        g = tg._geom(Geometry(1, 2, 2, d, page_size, 2))
+        return tg._lib.tg_read_probe(ctypes.byref(g), dtype, None, None, None, 0, n_workers, None, None)
+
+    for d, dtype in ((32, tg.TG_BF16), (96, tg.TG_BF16), (160, tg.TG_BF16), (48, tg.TG_F32), (80, tg.TG_F32),
+                     (112, tg.TG_F32), (256, tg.TG_F32), (512, tg.TG_BF16), (8, tg.TG_F32)):
+        assert call(d, dtype) == tg.TG_ERR_UNSUPPORTED, (d, dtype)      # 1, 3, 5, 3, 5, 7, 16, 16 KiB, 512 B
+    for d, dtype in ((64, tg.TG_BF16), (128, tg.TG_BF16), (256, tg.TG_BF16), (32, tg.TG_F32), (64, tg.TG_F32),
+                     (128, tg.TG_F32)):
+        assert call(d, dtype) == tg.TG_ERR_INVALID_ARG, (d, dtype)      # 2, 4, 8 KiB: on to n_workers
+    assert call(128, tg.TG_BF16, page_size=8) == tg.TG_ERR_INVALID_ARG  # 8 rows of 256 B = 2 KiB
+    assert call(128, tg.TG_BF16, page_size=12) == tg.TG_ERR_UNSUPPORTED
 
 
 @settings(max_examples=40, deadline=None)

@@ -234,6 +234,49 @@ def test_fill_plan_config1_hand():
     assert plan["unit_splits"].tolist() == gold["unit_splits"] and plan["num_partials"] == gold["num_partials"]
 
 
+def uniform_gold_items(gold):
+    """The hand-derived UNIFORM plan's items, spelled out from its per-head chunk bounds."""
+    items = []
+    for b in range(2):
+        for h in range(4):
+            bounds = gold["chunk_bounds"][f"head{h}"]
+            pt_base, slot = gold["table_and_slot"][b][h]
+            base = gold["unit_partial_base"][b][h]
+            for c in range(len(bounds) - 1):
+                items.append([pt_base, b, h, slot, bounds[c], bounds[c + 1], base + c])
+    return items
+
+
+def test_uniform_plan_config1_hand():
+    """Static uniform splits (the straggler baseline): 8 splits per unit capped by its pages, one bin per
+    chunk; a floor-for-ceil slip in the split count or a chunk-boundary slip changes these values."""
+    gold = GOLD["plan_uniform_bins64"]
+    _, _, _, plan = _cfg1_plan(mode=oracle.MODE_UNIFORM, n_bins=gold["n_bins"])
+    assert plan["unit_splits"].tolist() == gold["unit_splits"]
+    assert plan["unit_partial_base"].tolist() == gold["unit_partial_base"]
+    assert plan["num_partials"] == gold["num_partials"] == 56
+    assert plan["bin_offsets"].tolist() == list(range(gold["num_bins"] + 1))
+    assert plan["bin_load"].tolist() == gold["bin_load"]
+    assert [list(it) for it in plan["items"]] == uniform_gold_items(gold)
+    # n_bins just above a multiple of the unit count: the ceiling gives one more split per unit
+    _, _, _, plan9 = _cfg1_plan(mode=oracle.MODE_UNIFORM, n_bins=57)
+    assert plan9["unit_splits"].tolist() == [[8, 8, 8, 4], [8, 8, 8, 4]]
+    _, _, _, plan7 = _cfg1_plan(mode=oracle.MODE_UNIFORM, n_bins=9)
+    assert plan7["unit_splits"].tolist() == [[2, 2, 2, 2], [2, 2, 2, 2]]
+
+
+def test_naive_plan_config1_hand():
+    gold = GOLD["plan_naive"]
+    for n_bins in (1, 8, 64):          # the bin count is not an input of the naive split
+        _, _, _, plan = _cfg1_plan(mode=oracle.MODE_NAIVE, n_bins=n_bins)
+        assert [list(it) for it in plan["items"]] == gold["items"]
+        assert plan["bin_offsets"].tolist() == gold["bin_offsets"]
+        assert plan["unit_splits"].tolist() == gold["unit_splits"]
+        assert plan["unit_partial_base"].tolist() == gold["unit_partial_base"]
+        assert plan["num_partials"] == gold["num_partials"] == 0
+        assert plan["bin_load"].tolist() == gold["bin_load"]
+
+
 def test_plan_reduces_to_algorithm1():
     """One request, P=1 and lengths exactly B*N: the executed split counts are
     Algorithm 1's split map with H_p = 1."""

@@ -125,17 +125,45 @@ def test_prefill_long_chunk_sampled():
     _compare(ps, sorted(set(rows)), "long chunk")
 
 
-def test_prefill_chunk_of_one_matches_decode_path():
-    """C = 1: the prefill kernel and the decode kernel see the same keys when the
-    decode cache holds the chunk's key; both must match the oracle."""
+@pytest.mark.parametrize("plan", ["fill", "aot"])
+def test_prefill_chunk_of_one_matches_decode_path(plan):
+    """C = 1: one chunk row of chunked prefill (Section 2.2.1) sees exactly what the split-KV decode path
+    (Section 2.2.3) sees once the chunk's key and value are the cache's next entry.  The prefill kernel runs
+    over the history; then tg_append writes the chunk's K and V as entry kv_len of every head (into a row that
+    holds NaN until then) and the decode kernel, on an open-ended plan, attends over kv_len + 1 entries with the
+    same queries.  Both outputs match the oracle and each other within the bf16 tolerance."""
     _gpu()
+    from paper_2606_06302_amd import tangram as tg
+    from paper_2606_06302_amd.runner import DecodeSession
     g = Geometry(1, 8, 32, 128, 16, 2)
     wl = custom(612, g, 4, "bf16", (100, 900), chunk_len=1)
-    tables = Tables(wl)
-    ps = PrefillSession(wl, tables=tables, fill="host")
+    tables = Tables(wl, headroom=np.ones(wl.batch, dtype=np.int32))
+    pool = torch.from_numpy(poisoned_host_pool(wl, tables)).to(torch.bfloat16).cuda()
+    say(f"C=1 vs decode ({plan}): ctx={wl.ctx_len.tolist()}")
+    ps = PrefillSession(wl, tables=tables, fill="host", pool=pool)
     ps.run()
     torch.cuda.synchronize()
-    _compare(ps, [(b, q) for b in range(4) for q in range(32)], "C=1")
+    rows = [(b, q) for b in range(wl.batch) for q in range(g.num_q_heads)]
+    _compare(ps, rows, "C=1 prefill")
+
+    mode = tg.TG_PLAN_AOT_FILL if plan == "fill" else tg.TG_PLAN_AOT
+    q = ps.q[:, 0].unsqueeze(0).contiguous()                     # [L=1][B][Hq][d]
+    ds = DecodeSession(wl, tables=tables, mode=mode, n_bins=29, split_target=40, fill="host", pool=pool, q=q,
+                       open_end=True)
+    ds.enable_append(k_tok=ps.k_new[:, 0].unsqueeze(0).contiguous(), v_tok=ps.v_new[:, 0].unsqueeze(0).contiguous())
+    ds.run_decode_step()                                         # append, then attend
+    torch.cuda.synchronize()
+    assert int(ds.full.item()) == 0
+    assert np.array_equal(ds.live_len.cpu().numpy(), tables.kv_len + 1)
+    # the decode over kv_len + 1 entries against the oracle (the pool as the append left it)
+    f = lambda x: x.float().cpu().numpy().astype(np.float64)
+    t = tables
+    O, _ = oracle.decode_attention(f(q[0]), f(ds.pool), 0, geom=g, batch=wl.batch, kv_len=t.kv_len + 1,
+                                   offsets=t.pt_offsets, pages=t.pt_pages, group_of=t.group_of, slot_of=t.slot_of)
+    dec = f(ds.out[0])
+    check_close(dec.reshape(-1, g.head_dim), O.reshape(-1, g.head_dim), "bf16", "C=1 decode vs oracle")
+    pre = f(ps.out[:, 0])
+    check_close(dec.reshape(-1, g.head_dim), pre.reshape(-1, g.head_dim), "bf16", "C=1 decode vs prefill")
 
 
 def test_prefill_config5_full_size_sampled():
