@@ -287,6 +287,25 @@ typedef struct {
 size_t  tg_decode_workspace_bytes(const tg_geometry* geom, int32_t batch, int32_t num_partials);
 int32_t tg_decode(const tg_decode_args* args, void* hip_stream);
 
+/* 3b. tg_decode without a workspace, for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Same arguments, kernels and results as tg_decode, except
+ * that args->workspace and args->workspace_bytes are ignored: the split
+ * partials go to a static device array of TG_DECODE_NOALLOC_MAX_BYTES bytes
+ * that the library holds on every device it runs on until the process ends.
+ * The call itself allocates nothing (no hipMalloc, hipFree or allocating
+ * library routine); the first call on a device looks up that device's copy
+ * of the array (hipGetSymbolAddress), so the device of hip_stream must be the
+ * current device.  All calls on one device share the array and it keeps the
+ * last call's contents: calls that overlap in time on one device (other
+ * streams, other threads) race and must be ordered by the caller.
+ * Errors: those of tg_decode; TG_ERR_BUFFER_TOO_SMALL when the plan's
+ * partials need more than TG_DECODE_NOALLOC_MAX_BYTES
+ * (tg_decode_workspace_bytes(geom, batch, num_partials) > the maximum; checked
+ * on the host, nothing enqueued); TG_ERR_HIP if the lookup fails. */
+enum { TG_DECODE_NOALLOC_MAX_BYTES = 16 << 20 };
+int32_t tg_decode_noalloc(const tg_decode_args* args, void* hip_stream);
+
 /* 3a. decode-token append (device): one decode step's new token of one layer,
  * written after every KV head's current entries (the cache grows by one token
  * per head per step; Section 2.2, decode, on the ragged layout of Section

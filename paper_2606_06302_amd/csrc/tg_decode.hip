@@ -22,6 +22,7 @@
 #include <array>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <utility>
 
 #include "tg_device.h"
@@ -734,36 +735,40 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 }  // namespace
 
-extern "C" {
+// ---------------------------------------------------------------------------
+// Static scratch of tg_decode_noalloc: the split partials of one call, for
+// callers that cannot allocate device memory.  Every device the library runs
+// on holds its own copy of this array until the process ends.  In host code
+// `scratch` is only a stand-in symbol: its device address is looked up once
+// per device (hipGetSymbolAddress, with that device current) and that address
+// is what the kernels get.
+static __device__ __align__(256) unsigned char scratch[TG_DECODE_NOALLOC_MAX_BYTES];
 
-size_t tg_decode_workspace_bytes(const tg_geometry* geom, int32_t batch, int32_t num_partials) {
-  if (!geom || geom->num_kv_heads < 1 || geom->num_q_heads < geom->num_kv_heads || num_partials < 0 || batch < 0)
-    return 0;
-  const size_t gqa = (size_t)(geom->num_q_heads / geom->num_kv_heads);
-  const size_t d = (size_t)geom->head_dim;
-  // fp32 partial outputs, then their lse
-  return align256((size_t)num_partials * gqa * d * sizeof(float)) +
-         align256((size_t)num_partials * gqa * sizeof(float));
-}
+namespace {
 
-int32_t tg_decode_max_ctas(const tg_geometry* geom, int32_t dtype, int32_t device, int32_t* n_cta) {
-  if (!n_cta) return tg::fail(TG_ERR_INVALID_ARG, "n_cta is NULL");
-  if (int32_t rc = check_decode_shape(geom, dtype)) return rc;
-  DecodeFn fn = pick_decode(dtype, geom->head_dim, geom->num_q_heads / geom->num_kv_heads);
-  int cus = 0, per_cu = 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess)
-    return tg::fail(TG_ERR_HIP, "hipDeviceGetAttribute failed for device %d", device);
-  int prev = 0;
-  if (hipGetDevice(&prev) != hipSuccess) return tg::fail(TG_ERR_HIP, "hipGetDevice failed");
-  if (prev != device && hipSetDevice(device) != hipSuccess) return tg::fail(TG_ERR_HIP, "hipSetDevice failed");
-  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fn), kBlock, 0);
-  if (prev != device) (void)hipSetDevice(prev);
-  if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "occupancy query failed: %s", hipGetErrorString(e));
-  *n_cta = per_cu * cus * workers_per_wg(dtype, geom->head_dim, geom->num_q_heads / geom->num_kv_heads);
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int32_t scratch_address(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return tg::fail(TG_ERR_HIP, "hipGetDevice failed");
+  if (dev < 0 || dev >= kMaxDevices) return tg::fail(TG_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return tg::fail(TG_ERR_HIP, "hipGetSymbolAddress(scratch) failed on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
   return TG_OK;
 }
 
-int32_t tg_decode(const tg_decode_args* a, void* hip_stream) {
+// tg_decode with the partials' memory passed in: ws (ws_bytes bytes) stands for
+// the caller's workspace.
+int32_t decode_impl(const tg_decode_args* a, void* ws_ptr, size_t ws_bytes, void* hip_stream) {
   if (!a) return tg::fail(TG_ERR_INVALID_ARG, "args is NULL");
   if (int32_t rc = check_decode_shape(&a->geom, a->dtype)) return rc;
   const tg_geometry& g = a->geom;
@@ -774,12 +779,12 @@ int32_t tg_decode(const tg_decode_args* a, void* hip_stream) {
   if (a->num_partials > 0 && (!a->unit_splits || !a->unit_partial_base))
     return tg::fail(TG_ERR_INVALID_ARG, "split plan needs unit_splits and unit_partial_base");
   const size_t need = tg_decode_workspace_bytes(&g, a->batch, a->num_partials);
-  if (a->num_partials > 0 && (!a->workspace || a->workspace_bytes < need))
-    return tg::fail(TG_ERR_BUFFER_TOO_SMALL, "workspace holds %zu bytes, need %zu", a->workspace_bytes, need);
+  if (a->num_partials > 0 && (!ws_ptr || ws_bytes < need))
+    return tg::fail(TG_ERR_BUFFER_TOO_SMALL, "workspace holds %zu bytes, need %zu", ws_bytes, need);
   const int gqa = g.num_q_heads / g.num_kv_heads;
   const int esz = a->dtype == TG_F32 ? 4 : 2;
   const size_t o_bytes = align256((size_t)a->num_partials * gqa * g.head_dim * 4);
-  char* ws = static_cast<char*>(a->workspace);
+  char* ws = static_cast<char*>(ws_ptr);
   DecodeParams p;
   p.q = a->q;
   p.pool = static_cast<const u4*>(a->kv_pool);
@@ -822,6 +827,57 @@ int32_t tg_decode(const tg_decode_args* a, void* hip_stream) {
     if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "merge launch failed: %s", hipGetErrorString(e));
   }
   return TG_OK;
+}
+
+
+}  // namespace
+
+extern "C" {
+
+size_t tg_decode_workspace_bytes(const tg_geometry* geom, int32_t batch, int32_t num_partials) {
+  if (!geom || geom->num_kv_heads < 1 || geom->num_q_heads < geom->num_kv_heads || num_partials < 0 || batch < 0)
+    return 0;
+  const size_t gqa = (size_t)(geom->num_q_heads / geom->num_kv_heads);
+  const size_t d = (size_t)geom->head_dim;
+  // fp32 partial outputs, then their lse
+  return align256((size_t)num_partials * gqa * d * sizeof(float)) +
+         align256((size_t)num_partials * gqa * sizeof(float));
+}
+
+int32_t tg_decode_max_ctas(const tg_geometry* geom, int32_t dtype, int32_t device, int32_t* n_cta) {
+  if (!n_cta) return tg::fail(TG_ERR_INVALID_ARG, "n_cta is NULL");
+  if (int32_t rc = check_decode_shape(geom, dtype)) return rc;
+  DecodeFn fn = pick_decode(dtype, geom->head_dim, geom->num_q_heads / geom->num_kv_heads);
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess)
+    return tg::fail(TG_ERR_HIP, "hipDeviceGetAttribute failed for device %d", device);
+  int prev = 0;
+  if (hipGetDevice(&prev) != hipSuccess) return tg::fail(TG_ERR_HIP, "hipGetDevice failed");
+  if (prev != device && hipSetDevice(device) != hipSuccess) return tg::fail(TG_ERR_HIP, "hipSetDevice failed");
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(fn), kBlock, 0);
+  if (prev != device) (void)hipSetDevice(prev);
+  if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "occupancy query failed: %s", hipGetErrorString(e));
+  *n_cta = per_cu * cus * workers_per_wg(dtype, geom->head_dim, geom->num_q_heads / geom->num_kv_heads);
+  return TG_OK;
+}
+
+int32_t tg_decode(const tg_decode_args* a, void* hip_stream) {
+  if (!a) return tg::fail(TG_ERR_INVALID_ARG, "args is NULL");
+  return decode_impl(a, a->workspace, a->workspace_bytes, hip_stream);
+}
+
+int32_t tg_decode_noalloc(const tg_decode_args* a, void* hip_stream) {
+  if (!a) return tg::fail(TG_ERR_INVALID_ARG, "args is NULL");
+  if (int32_t rc = check_decode_shape(&a->geom, a->dtype)) return rc;
+  if (a->batch < 1 || a->num_partials < 0) return tg::fail(TG_ERR_INVALID_ARG, "batch must be >= 1, num_partials >= 0");
+  const size_t need = tg_decode_workspace_bytes(&a->geom, a->batch, a->num_partials);
+  if (need > (size_t)TG_DECODE_NOALLOC_MAX_BYTES)
+    return tg::fail(TG_ERR_BUFFER_TOO_SMALL,
+                    "tg_decode_noalloc: %d partials need %zu bytes of scratch, the static scratch holds %d",
+                    a->num_partials, need, (int)TG_DECODE_NOALLOC_MAX_BYTES);
+  void* ws = nullptr;
+  if (int32_t rc = scratch_address(&ws)) return rc;
+  return decode_impl(a, ws, (size_t)TG_DECODE_NOALLOC_MAX_BYTES, hip_stream);
 }
 
 }  // extern "C"

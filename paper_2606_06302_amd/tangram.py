@@ -115,6 +115,7 @@ _SIGS = {
                              _P, _P, _P]),
     "tg_decode_workspace_bytes": (_sz, [_G, _i32, _i32]),
     "tg_decode": (_i32, [C.POINTER(tg_decode_args), _P]),
+    "tg_decode_noalloc": (_i32, [C.POINTER(tg_decode_args), _P]),
     "tg_append": (_i32, [C.POINTER(tg_append_args), _P]),
     "tg_prefill_workspace_bytes": (_sz, [C.POINTER(tg_prefill_args)]),
     "tg_prefill": (_i32, [C.POINTER(tg_prefill_args), _P]),
@@ -280,6 +281,14 @@ def make_decode_args(geom, batch, dtype, q, kv_pool, pt_pages, items, bin_offset
 
 def tg_decode(args: tg_decode_args, stream=None):
     _check(_lib.tg_decode(C.byref(args), _stream(stream)), "tg_decode")
+
+
+TG_DECODE_NOALLOC_MAX_BYTES = 16 << 20
+
+
+def tg_decode_noalloc(args: tg_decode_args, stream=None):
+    """tg_decode with the partials in the library's static per-device scratch (args.workspace ignored)."""
+    _check(_lib.tg_decode_noalloc(C.byref(args), _stream(stream)), "tg_decode_noalloc")
 
 
 def make_prefill_args(geom, batch, chunk_len, layer, dtype, q, k_new, v_new, kv_pool, pt_pages, pt_offsets,
