@@ -657,7 +657,8 @@ def main():
             torch.cuda.synchronize()
             lay_ms += np.array([a.elapsed_time(b) for a, b in evs])
         lay_ms /= nrep
-        busy = s.worker_busy(stream)   # an extra untimed step with per-worker stamps
+        timeline = s.worker_timeline(stream)   # an extra untimed step with per-worker stamps
+        busy = [(r["busy_max"], r["busy_mean"]) for r in timeline]
         # streaming-read ceiling of the same access pattern: the probe reads exactly the page slabs the
         # decode reads on a sample of layers, with the same number of workers and no arithmetic
         probe_layers = s.layers[:: max(1, len(s.layers) // 8)]
@@ -711,6 +712,8 @@ def main():
         "plan_build_us": round(s.plan_build_us, 1),
         "load_imbalance_planned": round(planned_imbalance, 4),
         "load_imbalance_measured": round(measured_imbalance, 4),
+        "worker_timeline_us": {k: round(float(np.median([r[k] for r in timeline])), 2)
+                               for k in ("span", "ramp", "tail", "busy_max", "busy_mean")},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic,

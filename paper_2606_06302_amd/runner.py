@@ -204,9 +204,10 @@ class DecodeSession:
             self.run_step(stream)
         return graph
 
-    def worker_busy(self, stream=None):
-        """Runs one step with per-worker start/end stamps (s_memrealtime ticks) and returns, per
-        layer, (max, mean) of the busy time over the workers that had work, in microseconds."""
+    def worker_timeline(self, stream=None):
+        """Runs one step with per-worker start/end stamps (s_memrealtime ticks) and returns, per layer,
+        a dict over the workers that had work, in microseconds: busy_max and busy_mean (end - start),
+        ramp (last start - first start), tail (last end - first end), span (last end - first start)."""
         res = []
         for l in self.layers:
             dp = self.dplans[l]
@@ -215,11 +216,18 @@ class DecodeSession:
             args.timestamps = ts.data_ptr()
             tg.tg_decode(args, stream)
             torch.cuda.synchronize()
-            t = ts.view(-1, 2).cpu().numpy()
-            busy = (t[:, 1] - t[:, 0]).astype(np.float64) / REALTIME_HZ * 1e6
-            busy = busy[np.diff(self.plans[l]["bin_offsets"]) > 0]
-            res.append((float(busy.max()), float(busy.mean())))
+            t = ts.view(-1, 2).cpu().numpy()[np.diff(self.plans[l]["bin_offsets"]) > 0].astype(np.float64)
+            us = 1e6 / REALTIME_HZ
+            busy = (t[:, 1] - t[:, 0]) * us
+            res.append(dict(busy_max=float(busy.max()), busy_mean=float(busy.mean()),
+                            ramp=float(t[:, 0].max() - t[:, 0].min()) * us,
+                            tail=float(t[:, 1].max() - t[:, 1].min()) * us,
+                            span=float(t[:, 1].max() - t[:, 0].min()) * us))
         return res
+
+    def worker_busy(self, stream=None):
+        """Per layer, (max, mean) of the workers' busy time in microseconds (see worker_timeline)."""
+        return [(r["busy_max"], r["busy_mean"]) for r in self.worker_timeline(stream)]
 
     def layer_slabs(self, l):
         """(page id, slot) of every page slab layer l's plan reads, in item order: the decode's reads
