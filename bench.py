@@ -548,6 +548,8 @@ def main():
     ap.add_argument("--split-target", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of a HIP graph replay")
+    ap.add_argument("--fused-merge", action="store_true",
+                    help="merge split units inside the decode launch (merge_counters) instead of a second launch")
     ap.add_argument("--calibrate-xcd", action="store_true",
                     help="rebuild the fill plans with per-XCD bin weights measured in one stamped step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -602,7 +604,8 @@ def main():
         t0_ = Tables(wl)
         tables = Tables(wl, free_pages=np.arange(t0_.pool_pages, dtype=np.int32), pool_pages=t0_.pool_pages)
     s = DecodeSession(wl, tables=tables, mode=mode, n_bins=args.n_bins or None,
-                      split_target=args.split_target or None, fill="host" if args.config == 1 else "device")
+                      split_target=args.split_target or None, fill="host" if args.config == 1 else "device",
+                      fused_merge=args.fused_merge)
     torch.cuda.synchronize()
     log(f"[bench] setup {time.perf_counter() - t0:.1f} s: pool {s.t.pool_pages} pages "
         f"({s.pool.numel() * s.pool.element_size() / 1e9:.1f} GB), n_bins {s.n_bins}, "
@@ -699,6 +702,7 @@ def main():
                    "heads_per_group": g.heads_per_group, "plan": args.mode, "n_bins": s.n_bins,
                    "split_target": s.split_target, "kv_bytes_per_step": kv_bytes_step,
                    "free_order": args.free_order, "launch": "eager" if args.no_graph else "hip graph",
+                   "merge": "in the decode launch" if args.fused_merge else "second launch",
                    "bin_weights": None if xcd_speed is None else "per-XCD speed from one stamped step "
                                   + str(np.round(xcd_speed, 3).tolist()),
                    "parallelism": "single GPU"},

@@ -231,9 +231,10 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
  * executed as the work items of a tg_build_plan partition: worker k of the
  * decode launch (one wave in the bf16 head_dim-128 kernel, one workgroup
  * otherwise) runs the items of bin k; an item with out_idx >= 0
- * writes an fp32 partial (o, lse) to the workspace, and a second launch on the
- * same stream (only when num_partials > 0) merges the partials of every split
- * unit with a log-sum-exp merge.
+ * writes an fp32 partial (o, lse) to the workspace, and the partials of every
+ * split unit are combined with a log-sum-exp merge: inside the decode launch
+ * when merge_counters is given (bf16, head_dim 128), otherwise by a second
+ * launch on the same stream (only when num_partials > 0).
  * All pointers below are DEVICE pointers:
  *   q        [B][Hq][d] dtype
  *   kv_pool  [pool_pages][2][H_p][P][d] dtype (layout in the file header)
@@ -257,6 +258,14 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
  *   live_len [B][L][H] int32 or NULL, with layer: current lengths for items
  *            of a TG_PLAN_OPEN_END plan (an open item with live_len NULL runs
  *            to its table's capacity).
+ *   merge_counters [B][H] int32 or NULL: arrival counters that let the bf16
+ *            head_dim-128 kernel merge split units inside its own launch (the
+ *            split piece that finishes last merges its unit), so no second
+ *            launch is needed.  They must be zero before the first call; every
+ *            call leaves them zero, and calls that share them must not overlap
+ *            in time.  NULL, or any other dtype / head_dim: the merge runs as a
+ *            second launch on the same stream.  The results are the same
+ *            either way, bit for bit.
  * Supported: dtype TG_F32 or TG_BF16, head_dim 64 or 128, page_size 16,
  * gqa 1..16 (else TG_ERR_UNSUPPORTED).  hip_stream is a hipStream_t (NULL =
  * default stream).  Returns TG_ERR_HIP if a launch fails. */
@@ -282,6 +291,7 @@ typedef struct {
   uint64_t* timestamps;
   const int32_t* live_len;
   int32_t layer;
+  int32_t* merge_counters;
 } tg_decode_args;
 
 size_t  tg_decode_workspace_bytes(const tg_geometry* geom, int32_t batch, int32_t num_partials);
@@ -293,6 +303,10 @@ int32_t tg_decode(const tg_decode_args* args, void* hip_stream);
  * that args->workspace and args->workspace_bytes are ignored: the split
  * partials go to a static device array of TG_DECODE_NOALLOC_MAX_BYTES bytes
  * that the library holds on every device it runs on until the process ends.
+ * args->merge_counters is ignored too: the array also holds the in-launch
+ * merge's counters (64 KiB, up to 16384 (request, KV head) units; larger
+ * batches merge in a second launch), so the partials get
+ * TG_DECODE_NOALLOC_MAX_BYTES - 64 KiB.
  * The call itself allocates nothing (no hipMalloc, hipFree or allocating
  * library routine); the first call on a device looks up that device's copy
  * of the array (hipGetSymbolAddress), so the device of hip_stream must be the
@@ -300,8 +314,8 @@ int32_t tg_decode(const tg_decode_args* args, void* hip_stream);
  * last call's contents: calls that overlap in time on one device (other
  * streams, other threads) race and must be ordered by the caller.
  * Errors: those of tg_decode; TG_ERR_BUFFER_TOO_SMALL when the plan's
- * partials need more than TG_DECODE_NOALLOC_MAX_BYTES
- * (tg_decode_workspace_bytes(geom, batch, num_partials) > the maximum; checked
+ * partials need more than TG_DECODE_NOALLOC_MAX_BYTES - 64 KiB
+ * (tg_decode_workspace_bytes(geom, batch, num_partials) > that; checked
  * on the host, nothing enqueued); TG_ERR_HIP if the lookup fails. */
 enum { TG_DECODE_NOALLOC_MAX_BYTES = 16 << 20 };
 int32_t tg_decode_noalloc(const tg_decode_args* args, void* hip_stream);

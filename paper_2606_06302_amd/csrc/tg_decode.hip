@@ -116,6 +116,7 @@ struct DecodeParams {
   int32_t live_stride;
   float scale_log2;          // sm_scale * log2(e)
   float scale;               // sm_scale
+  int32_t* merge_counters;   // [B*H] arrival counters of the in-launch merge, or NULL
 };
 
 // An open-ended item (tok_end = -capacity) runs to the head's live length,
@@ -404,6 +405,11 @@ __device__ __forceinline__ tg_work_item load_item(const TG_CONST tg_work_item* s
   return r;
 }
 
+// two fp32 values as one 64-bit word (lo first, as they sit in memory)
+__device__ __forceinline__ uint64_t pack_f32x2(float lo, float hi) {
+  return (uint64_t)__float_as_uint(lo) | ((uint64_t)__float_as_uint(hi) << 32);
+}
+
 __device__ __forceinline__ f32x4 mfma_qk(const u4& a, const u4& b, const f32x4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0,
                                                  0);
@@ -628,6 +634,20 @@ __global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, 
                                     uint32_t(f32_to_bf16(o[2])) | (uint32_t(f32_to_bf16(o[3])) << 16));
         }
         if (p.lse && rb == 0) p.lse[(int64_t)item.b * p.num_q_heads + qh] = lse_nat;
+      } else if (p.merge_counters) {
+        // read in this launch by whichever worker merges the unit, maybe on
+        // another XCD: device-scope stores, written through to where every
+        // XCD's device-scope loads read
+        uint64_t* prow = reinterpret_cast<uint64_t*>(p.part_o + ((int64_t)item.out_idx * G + col) * D + 4 * rb);
+#pragma unroll
+        for (int mm = 0; mm < 8; ++mm) {
+          const f32x4 o = acc[mm] * inv;
+          __hip_atomic_store(prow + mm * 8, pack_f32x2(o[0], o[1]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(prow + mm * 8 + 1, pack_f32x2(o[2], o[3]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        if (rb == 0)
+          __hip_atomic_store(p.part_lse + (int64_t)item.out_idx * G + col, lse_nat, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
       } else {
         f32x4* prow = reinterpret_cast<f32x4*>(p.part_o + ((int64_t)item.out_idx * G + col) * D + 4 * rb);
 #pragma unroll
@@ -638,7 +658,87 @@ __global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, 
     pi = 0;
     if (++it == it_end) break;
   }
-  wait_vmcnt<0>();
+  wait_vmcnt<0>();   // every page and every partial of this worker is complete
+
+  // In-launch log-sum-exp merge (split-KV decoding, Section 2.2.3).  Each split
+  // piece this worker ran counts itself on its unit's arrival counter; the
+  // piece that arrives last merges the unit's partials and resets the counter
+  // for the next call.  The partials were written with device-scope stores and
+  // are complete (the wait above) before the worker's increments; the merging
+  // worker reads them with device-scope loads issued after its increment
+  // returned.  This is the ordering a release/acquire pair gives for data
+  // written and read by device-scope atomics, without the writeback and
+  // invalidation of a whole L2 that a fence for ordinary data needs.
+  if (p.merge_counters) {
+    const TG_CONST int32_t* const unit_splits = (const TG_CONST int32_t*)p.unit_splits;
+    const TG_CONST int32_t* const unit_base = (const TG_CONST int32_t*)p.unit_partial_base;
+    // the split items of the bin, up to kBatch at a time: all their arrivals
+    // go out before the first result is waited for, so a worker pays one
+    // round trip for them, not one per item
+    constexpr int kBatch = 4;
+    int it2 = it_begin;
+    while (it2 < it_end) {
+      int su[kBatch], nb = 0;   // item indices of this batch's split items
+      for (; it2 < it_end && nb < kBatch; ++it2)
+        if (items[it2].out_idx >= 0) su[nb++] = it2;
+      if (nb == 0) break;
+      int arrived[kBatch];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        arrived[j] = 0;
+        if (j < nb && lane == 0) {
+          const int u = items[su[j]].b * p.num_kv_heads + items[su[j]].kv_head;
+          arrived[j] = __hip_atomic_fetch_add(p.merge_counters + u, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        if (j >= nb) break;
+        const int b = items[su[j]].b, h = items[su[j]].kv_head;
+        const int u = b * p.num_kv_heads + h;
+        const int s = unit_splits[u], base = unit_base[u];
+        if (__builtin_amdgcn_readfirstlane(arrived[j]) != s - 1) continue;
+        if (col < G) {
+          float mr = -INFINITY, L = 0.f;
+          f32x4 A[8];
+#pragma unroll
+          for (int mm = 0; mm < 8; ++mm) A[mm] = f32x4{0.f, 0.f, 0.f, 0.f};
+          for (int i = 0; i < s; ++i) {
+            const int64_t pidx = (int64_t)base + i;
+            const float li = __hip_atomic_load(p.part_lse + pidx * G + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            const uint64_t* prow = reinterpret_cast<const uint64_t*>(p.part_o + (pidx * G + col) * D + 4 * rb);
+            f32x4 oi[8];
+#pragma unroll
+            for (int mm = 0; mm < 8; ++mm) {
+              const uint64_t lo = __hip_atomic_load(prow + mm * 8, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              const uint64_t hi = __hip_atomic_load(prow + mm * 8 + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              oi[mm] = f32x4{__uint_as_float((uint32_t)lo), __uint_as_float((uint32_t)(lo >> 32)),
+                             __uint_as_float((uint32_t)hi), __uint_as_float((uint32_t)(hi >> 32))};
+            }
+            // the same running-max recurrence, in the same order, as tg_merge_kernel
+            const float mn = fmaxf(mr, li);
+            const float a = __expf(mr - mn), w = __expf(li - mn);
+            L = fmaf(L, a, w);
+#pragma unroll
+            for (int mm = 0; mm < 8; ++mm)
+#pragma unroll
+              for (int q = 0; q < 4; ++q) A[mm][q] = fmaf(A[mm][q], a, w * oi[mm][q]);
+            mr = mn;
+          }
+          const int qh = h * G + col;
+          uint2* orow =
+              reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + ((int64_t)b * p.num_q_heads + qh) * D + 4 * rb);
+#pragma unroll
+          for (int mm = 0; mm < 8; ++mm)
+            orow[mm * 4] =
+                make_uint2(uint32_t(f32_to_bf16(A[mm][0] / L)) | (uint32_t(f32_to_bf16(A[mm][1] / L)) << 16),
+                           uint32_t(f32_to_bf16(A[mm][2] / L)) | (uint32_t(f32_to_bf16(A[mm][3] / L)) << 16));
+          if (p.lse && rb == 0) p.lse[(int64_t)b * p.num_q_heads + qh] = mr + logf(L);
+        }
+        if (lane == 0) __hip_atomic_store(p.merge_counters + u, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
   if (p.timestamps && lane == 0) {   // one lane, vector stores
     p.timestamps[2 * bin] = t_start;
     p.timestamps[2 * bin + 1] = __builtin_amdgcn_s_memrealtime();
@@ -747,6 +847,7 @@ static __device__ __align__(256) unsigned char scratch[TG_DECODE_NOALLOC_MAX_BYT
 namespace {
 
 constexpr int kMaxDevices = 64;
+constexpr size_t kScratchCounters = 64 << 10;   // merge arrival counters: up to 16384 (request, KV head) units
 std::mutex g_scratch_mu;
 void* g_scratch_ptr[kMaxDevices] = {};
 
@@ -808,6 +909,10 @@ int32_t decode_impl(const tg_decode_args* a, void* ws_ptr, size_t ws_bytes, void
     return tg::fail(TG_ERR_INVALID_ARG, "layer %d out of range", a->layer);
   p.live = a->live_len ? a->live_len + (int64_t)a->layer * g.num_kv_heads : nullptr;
   p.live_stride = g.num_layers * g.num_kv_heads;
+  // the bf16 head_dim-128 kernel merges split units inside its launch when the
+  // caller passes arrival counters; every other case merges in a second launch
+  const bool fused_merge = a->merge_counters && a->num_partials > 0 && a->dtype == TG_BF16 && g.head_dim == 128;
+  p.merge_counters = fused_merge ? a->merge_counters : nullptr;
   p.scale = a->sm_scale != 0.f ? a->sm_scale : 1.0f / std::sqrt((float)g.head_dim);
   p.scale_log2 = p.scale * kLog2e;
   if (a->num_items == 0) return TG_OK;
@@ -818,7 +923,7 @@ int32_t decode_impl(const tg_decode_args* a, void* ws_ptr, size_t ws_bytes, void
                      a->bin_offsets, p.pool);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
-  if (a->num_partials > 0) {
+  if (a->num_partials > 0 && !fused_merge) {
     MergeFn mf = pick_merge(a->dtype, g.head_dim);
     hipLaunchKernelGGL(mf, dim3(a->batch * g.num_kv_heads, (gqa * g.head_dim + kBlock - 1) / kBlock), dim3(kBlock), 0,
                        st, a->unit_splits,
@@ -871,13 +976,19 @@ int32_t tg_decode_noalloc(const tg_decode_args* a, void* hip_stream) {
   if (int32_t rc = check_decode_shape(&a->geom, a->dtype)) return rc;
   if (a->batch < 1 || a->num_partials < 0) return tg::fail(TG_ERR_INVALID_ARG, "batch must be >= 1, num_partials >= 0");
   const size_t need = tg_decode_workspace_bytes(&a->geom, a->batch, a->num_partials);
-  if (need > (size_t)TG_DECODE_NOALLOC_MAX_BYTES)
+  if (need > (size_t)TG_DECODE_NOALLOC_MAX_BYTES - kScratchCounters)
     return tg::fail(TG_ERR_BUFFER_TOO_SMALL,
-                    "tg_decode_noalloc: %d partials need %zu bytes of scratch, the static scratch holds %d",
-                    a->num_partials, need, (int)TG_DECODE_NOALLOC_MAX_BYTES);
+                    "tg_decode_noalloc: %d partials need %zu bytes of scratch, the static scratch holds %zu",
+                    a->num_partials, need, (size_t)TG_DECODE_NOALLOC_MAX_BYTES - kScratchCounters);
   void* ws = nullptr;
   if (int32_t rc = scratch_address(&ws)) return rc;
-  return decode_impl(a, ws, (size_t)TG_DECODE_NOALLOC_MAX_BYTES, hip_stream);
+  // the scratch starts with kScratchCounters bytes of merge arrival counters
+  // (zero at load; every call leaves them zero), then the partials
+  tg_decode_args b = *a;
+  char* base = static_cast<char*>(ws);
+  const bool counters_fit = (size_t)a->batch * a->geom.num_kv_heads * sizeof(int32_t) <= kScratchCounters;
+  b.merge_counters = counters_fit ? reinterpret_cast<int32_t*>(base) : nullptr;
+  return decode_impl(&b, base + kScratchCounters, (size_t)TG_DECODE_NOALLOC_MAX_BYTES - kScratchCounters, hip_stream);
 }
 
 }  // extern "C"

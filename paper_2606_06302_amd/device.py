@@ -50,10 +50,11 @@ def upload_plan(geom, batch, plan: dict, device) -> DevicePlan:
 
 
 def bind_decode(dp: DevicePlan, geom, batch, dtype, q, kv_pool, pt_pages, out, lse=None, sm_scale=0.0,
-                live_len=None, layer=0):
-    """Packs (and stores on dp) the tg_decode_args for this layer."""
+                live_len=None, layer=0, merge_counters=None):
+    """Packs (and stores on dp) the tg_decode_args for this layer; merge_counters (int32 [B*H] zeros,
+    shared by calls on one stream) selects the in-launch merge."""
     dp.args = tg.make_decode_args(geom, batch, dtype, q, kv_pool, pt_pages, dp.items, dp.bin_offsets,
                                   dp.host["num_bins"], dp.host["num_items"], dp.unit_splits,
                                   dp.unit_partial_base, dp.host["num_partials"], out, lse, sm_scale,
-                                  dp.workspace, live_len=live_len, layer=layer)
+                                  dp.workspace, live_len=live_len, layer=layer, merge_counters=merge_counters)
     return dp.args

@@ -59,7 +59,8 @@ class DecodeSession:
     """Pool, queries, outputs and per-layer plans of one decode workload."""
 
     def __init__(self, wl, tables: Tables = None, mode=tg.TG_PLAN_AOT, n_bins=None, split_target=None,
-                 fill="device", pool=None, q=None, want_lse=True, device="cuda", layers=None, open_end=False):
+                 fill="device", pool=None, q=None, want_lse=True, device="cuda", layers=None, open_end=False,
+                 fused_merge=False):
         from workloads import S_POOL, S_Q, device_normal_, host_pool, host_q_decode, page_elems
         g = wl.geom
         self.wl, self.device = wl, device
@@ -97,6 +98,10 @@ class DecodeSession:
             self.q = torch.empty(L, B, g.num_q_heads, g.head_dim, dtype=self.dtype, device=device)
             device_normal_(self.q, wl, S_Q, wl.q_scale)
         self.out = torch.zeros(L, B, g.num_q_heads, g.head_dim, dtype=self.dtype, device=device)
+        # arrival counters of the in-launch merge (zero; every call leaves them zero), shared by the layers'
+        # calls, which run one after the other on a stream; None: the merge is a second launch
+        self.merge_counters = (torch.zeros(B * g.num_kv_heads, dtype=torch.int32, device=device)
+                               if fused_merge else None)
         self.lse = torch.zeros(L, B, g.num_q_heads, dtype=torch.float32, device=device) if want_lse else None
         self._bind()
 
@@ -121,7 +126,8 @@ class DecodeSession:
         g, B = self.wl.geom, self.wl.batch
         for l in self.layers:
             bind_decode(self.dplans[l], g, B, self.tg_dtype, self.q[l], self.pool, self.t.d_pt_pages, self.out[l],
-                        None if self.lse is None else self.lse[l], live_len=self.live_len, layer=l)
+                        None if self.lse is None else self.lse[l], live_len=self.live_len, layer=l,
+                        merge_counters=self.merge_counters)
 
     def item_tokens(self, l):
         """Tokens of every item of layer l's plan; open-ended items count up to the lengths the

@@ -291,6 +291,38 @@ def test_split_map_plan_vs_oracle():
         compare_layer(s, l, what=f"split map layer {l}")
 
 
+@pytest.mark.parametrize("gqa,mode,n_bins,st", [(8, 3, 64, 1), (8, 0, 512, 4096), (16, 0, 300, 900), (3, 3, 97, 1),
+                                                (1, 4, 128, 1), (8, 3, 1, 1), (5, 0, 2000, 8000)])
+def test_fused_merge_matches_two_launch_merge_bitwise(gqa, mode, n_bins, st):
+    """The in-launch merge (each split piece counts itself on its unit's counter; the piece that arrives last
+    merges) gives bit for bit the outputs and LSEs of the separate merge launch, including plans that cut units
+    into dozens of pieces, on repeated calls (the counters are back at zero after each); both match the oracle."""
+    _gpu()
+    g = Geometry(2, 8, 8 * gqa, 128, 16, 2)
+    wl = custom(7300 + gqa + n_bins, g, 5, "bf16", (100, 8000), kv_scale=0.5)
+    tables = Tables(wl)
+    pool = torch.from_numpy(poisoned_host_pool(wl, tables)).to(torch.bfloat16).cuda()
+    kw = dict(tables=tables, mode=mode, n_bins=n_bins, split_target=st, fill="host", pool=pool)
+    if mode == tg.TG_PLAN_SPLIT_MAP:
+        kw["n_bins"] = n_bins
+    fused = DecodeSession(wl, fused_merge=True, **kw)
+    assert fused.merge_counters is not None
+    twol = DecodeSession(wl, fused_merge=False, q=fused.q, **kw)
+    splits = [int(fused.plans[l]["unit_splits"].max()) for l in fused.layers]
+    say(f"fused merge gqa {gqa} mode {mode} bins {n_bins}: partials "
+        f"{[fused.plans[l]['num_partials'] for l in fused.layers]}, most splits per unit {splits}")
+    twol.run_step()
+    for rep in range(3):
+        fused.out.fill_(float("nan"))
+        fused.lse.fill_(float("nan"))
+        fused.run_step()
+        torch.cuda.synchronize()
+        assert torch.equal(fused.out, twol.out) and torch.equal(fused.lse, twol.lse), rep
+        assert int(fused.merge_counters.abs().sum().item()) == 0
+    for l in fused.layers:
+        compare_layer(fused, l, what=f"fused merge layer {l}")
+
+
 def test_read_probe_checksums():
     """The streaming-read probe reads exactly the slabs the decode reads: every worker's XOR checksum equals
     the host's over the same (page, slot) K and V slabs."""
