@@ -303,9 +303,10 @@ int32_t tg_decode(const tg_decode_args* args, void* hip_stream);
  * that args->workspace and args->workspace_bytes are ignored: the split
  * partials go to a static device array of TG_DECODE_NOALLOC_MAX_BYTES bytes
  * that the library holds on every device it runs on until the process ends.
- * args->merge_counters is ignored too: the array also holds the in-launch
- * merge's counters (64 KiB, up to 16384 (request, KV head) units; larger
- * batches merge in a second launch), so the partials get
+ * A non-NULL args->merge_counters selects the in-launch merge as in
+ * tg_decode, but the counters used are the array's own (its first 64 KiB,
+ * for up to 16384 (request, KV head) units; larger batches merge in a second
+ * launch), not the pointer passed; the partials get the remaining
  * TG_DECODE_NOALLOC_MAX_BYTES - 64 KiB.
  * The call itself allocates nothing (no hipMalloc, hipFree or allocating
  * library routine); the first call on a device looks up that device's copy
@@ -370,7 +371,7 @@ int32_t tg_append(const tg_append_args* args, void* hip_stream);
  * TG_PREFILL_TILE keys.  The result does not depend on block_order.
  * A history length outside [0, pages of the head's table * page_size] is
  * clamped to that range on the device.
- * Supported: dtype TG_BF16, head_dim 128, page_size 16, gqa 1..16,
+ * Supported: dtype TG_BF16, head_dim 64 or 128, page_size 16, gqa 1..16,
  * chunk_len >= 1.  The kernel needs no workspace (workspace may be NULL). */
 typedef struct {
   tg_geometry geom;

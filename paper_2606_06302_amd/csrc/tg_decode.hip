@@ -987,7 +987,7 @@ int32_t tg_decode_noalloc(const tg_decode_args* a, void* hip_stream) {
   tg_decode_args b = *a;
   char* base = static_cast<char*>(ws);
   const bool counters_fit = (size_t)a->batch * a->geom.num_kv_heads * sizeof(int32_t) <= kScratchCounters;
-  b.merge_counters = counters_fit ? reinterpret_cast<int32_t*>(base) : nullptr;
+  b.merge_counters = a->merge_counters && counters_fit ? reinterpret_cast<int32_t*>(base) : nullptr;
   return decode_impl(&b, base + kScratchCounters, (size_t)TG_DECODE_NOALLOC_MAX_BYTES - kScratchCounters, hip_stream);
 }
 

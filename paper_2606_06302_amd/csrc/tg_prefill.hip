@@ -63,8 +63,6 @@ typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
 #define TG_CONST __attribute__((address_space(4)))
 #define TG_LDS __attribute__((address_space(3)))
 
-constexpr int kD = 128;              // head_dim
-constexpr int kChunks = kD / 8;      // 16-byte chunks per row
 constexpr int kPage = 16;
 constexpr int kWaves = 8;
 constexpr int kBlock = 64 * kWaves;
@@ -75,11 +73,28 @@ constexpr int kTile = 64;                      // keys per tile = 4 pages
 static_assert(kRows == TG_PREFILL_ROWS && kTile == TG_PREFILL_TILE, "tg_prefill_schedule costs these tiles");
 constexpr int kRing = 4;                       // LDS tile buffers
 static_assert(kRing >= 2 && kRing <= 4, "the wait below covers up to two tiles in flight after the current one");
-constexpr int kTileBytes = 2 * kTile * kD * 2; // K + V
 constexpr int kDmaRows = kTile / kWaves;       // key rows each wave fetches per tile
-constexpr int kDmaInst = kDmaRows / 4;         // 1 KiB instructions per K or V slab and wave
-constexpr int kDmaPerTile = 2 * kDmaInst;
 constexpr float kSlack = 8.0f;
+
+// Shape constants of the kernel for head_dim D (64 or 128).  A key row is
+// 2*D bytes = kChunks 16-byte chunks; one 1 KiB DMA instruction (64 lanes x
+// 16 bytes) moves kRowsPerDma rows.  LDS swizzles: chunk c of key row r of a
+// tile sits at position c ^ k_swz(r) in the K tile and c ^ v_swz(r) in the V
+// tile (r taken mod 16, which is also the row within its page), chosen so
+// that the q.k operand reads and the transposed V reads are bank-conflict free.
+template <int D>
+struct Shape {
+  static_assert(D == 64 || D == 128, "head_dim 64 or 128");
+  static constexpr int kChunks = D / 8;
+  static constexpr int kRowsPerDma = 64 / kChunks;
+  static constexpr int kDmaInst = kDmaRows / kRowsPerDma;   // 1 KiB instructions per K or V slab and wave
+  static constexpr int kDmaPerTile = 2 * kDmaInst;
+  static constexpr int kTileBytes = 2 * kTile * D * 2;      // K + V
+  static constexpr int kK = D / 16;                         // 16-deep k steps of q.k
+  static constexpr int kDB = D / 32;                        // 32-dim blocks of the output
+  __device__ static constexpr int k_swz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+  __device__ static constexpr int v_swz(int r) { return D == 128 ? 4 * (r & 3) : 2 * (r & 3); }
+};
 
 struct PrefillParams {
   const uint16_t* q;        // [B][C][Hq][d]
@@ -131,8 +146,12 @@ __device__ __forceinline__ u2v lds_read_tr16(const void* ptr) {
   return __builtin_bit_cast(u2v, __builtin_amdgcn_ds_read_tr16_b64_v4bf16((TG_LDS bf16x4_vs*)ptr));
 }
 
+template <int D>
 __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
-  __shared__ u4 ring[kRing][2][kTile * kChunks];   // [slot][K, V][key row * 16 + chunk position]
+  using S = Shape<D>;
+  constexpr int kChunks = S::kChunks, kDmaInst = S::kDmaInst, kDmaPerTile = S::kDmaPerTile;
+  constexpr int kTileBytes = S::kTileBytes, kRowsPerDma = S::kRowsPerDma;
+  __shared__ u4 ring[kRing][2][kTile * kChunks];   // [slot][K, V][key row * kChunks + chunk position]
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -180,16 +199,16 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
   const int hf = lane >> 5;
   int my_i[kCB];
   bool row_ok[kCB];
-  u4 qb[kCB][8];
+  u4 qb[kCB][S::kK];
 #pragma unroll
   for (int cb = 0; cb < kCB; ++cb) {
     const int r = row0 + wave * kRowsPerWave + cb * 32 + (lane & 31);
     row_ok[cb] = r < rows_total;
     my_i[cb] = row_ok[cb] ? r / gqa : 0;
     const int j = row_ok[cb] ? r % gqa : 0;
-    const u4* qp = reinterpret_cast<const u4*>(p.q + (((int64_t)b * C + my_i[cb]) * Hq + h * gqa + j) * kD);
+    const u4* qp = reinterpret_cast<const u4*>(p.q + (((int64_t)b * C + my_i[cb]) * Hq + h * gqa + j) * D);
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) qb[cb][kk] = row_ok[cb] ? qp[kk * 2 + hf] : u4(0u);
+    for (int kk = 0; kk < S::kK; ++kk) qb[cb][kk] = row_ok[cb] ? qp[kk * 2 + hf] : u4(0u);
   }
   // Settle the query loads here, once: the compiler's wait-count pass cannot
   // see the inline-assembly LDS DMAs, so a load still pending at the loop
@@ -199,15 +218,15 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
 #pragma unroll
   for (int cb = 0; cb < kCB; ++cb)
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk) asm volatile("" : "+v"(qb[cb][kk]));
+    for (int kk = 0; kk < S::kK; ++kk) asm volatile("" : "+v"(qb[cb][kk]));
   const int wave_i_max = min(C - 1, (min(row0 + wave * kRowsPerWave + kRowsPerWave, rows_total) - 1) / gqa);
   const int wave_i_min = min(C - 1, (row0 + wave * kRowsPerWave) / gqa);
 
   // DMA of this wave's share (key rows kDmaRows*w .. kDmaRows*(w+1)-1) of tile
   // t into ring slot s
   const uint32_t ring_lds = lds_address(&ring[0][0][0]);
-  const int rl = lane >> 4;   // row within a 4-row DMA instruction
-  const int pos = lane & 15;  // chunk position within the row
+  const int rl = lane / kChunks;   // row within a DMA instruction
+  const int pos = lane % kChunks;  // chunk position within the row
   const int rb0 = (wave * kDmaRows) % kPage;   // first row of the share within its page
   auto issue = [&](int t, int s) {
     const uint32_t dst = ring_lds + (uint32_t)s * kTileBytes + (uint32_t)wave * (kDmaRows * kChunks * 16);
@@ -219,9 +238,9 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
       const u4* vb = p.pool + ((id * 2 + 1) * p.heads_per_group + slot) * (kPage * kChunks);
 #pragma unroll
       for (int j = 0; j < kDmaInst; ++j) {
-        const int r = rb0 + j * 4 + rl;   // key row within the page (== tile row mod 16)
-        lds_dma16(kb + r * kChunks + (pos ^ r), dst + j * 1024);
-        lds_dma16(vb + r * kChunks + (pos ^ (4 * (r & 3))), dst + kTile * kChunks * 16 + j * 1024);
+        const int r = rb0 + j * kRowsPerDma + rl;   // key row within the page (== tile row mod 16)
+        lds_dma16(kb + r * kChunks + (pos ^ S::k_swz(r)), dst + j * 1024);
+        lds_dma16(vb + r * kChunks + (pos ^ S::v_swz(r)), dst + kTile * kChunks * 16 + j * 1024);
       }
     } else {
       const int c0 = (t - n_hist_tiles) * kTile + wave * kDmaRows;   // first chunk key of the share
@@ -229,22 +248,22 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
       const u4* vb = p.v_new + h * kChunks;
 #pragma unroll
       for (int j = 0; j < kDmaInst; ++j) {
-        const int r = j * 4 + rl;
+        const int r = j * kRowsPerDma + rl;
         const int c = min(c0 + r, C - 1);   // rows past the chunk repeat its last key (masked later)
         const int rr = rb0 + r;             // tile row mod 16
         const int64_t roff = ((int64_t)b * C + c) * p.num_kv_heads * kChunks;
-        lds_dma16(kb + roff + (pos ^ rr), dst + j * 1024);
-        lds_dma16(vb + roff + (pos ^ (4 * (rr & 3))), dst + kTile * kChunks * 16 + j * 1024);
+        lds_dma16(kb + roff + (pos ^ S::k_swz(rr)), dst + j * 1024);
+        lds_dma16(vb + roff + (pos ^ S::v_swz(rr)), dst + kTile * kChunks * 16 + j * 1024);
       }
     }
   };
 
-  f32x16 acc[kCB][4];
+  f32x16 acc[kCB][S::kDB];
   float m[kCB], l[kCB];
 #pragma unroll
   for (int cb = 0; cb < kCB; ++cb) {
 #pragma unroll
-    for (int d = 0; d < 4; ++d) acc[cb][d] = f32x16(0.f);
+    for (int d = 0; d < S::kDB; ++d) acc[cb][d] = f32x16(0.f);
     m[cb] = -INFINITY;
     l[cb] = 0.f;
   }
@@ -276,7 +295,7 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
       u4* vq = &ring[t % kRing][1][wave * kDmaRows * kChunks];
 #pragma unroll
       for (int j = 0; j < kDmaInst; ++j)
-        if (t * kTile + wave * kDmaRows + j * 4 + rl >= hist) vq[j * 64 + lane] = u4(0u);
+        if (t * kTile + wave * kDmaRows + j * kRowsPerDma + rl >= hist) vq[j * 64 + lane] = u4(0u);
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     }
     barrier();   // tile t complete in LDS; every wave is done with tile t-1
@@ -302,26 +321,26 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
       // all eight K operands of the block, and the V^T operands of its p.v
       // products (they do not depend on p), are requested before the first
       // product, so their LDS latency hides under q.k and the softmax
-      u4 ka[8];
+      u4 ka[S::kK];
 #pragma unroll
-      for (int kk = 0; kk < 8; ++kk)
-        ka[kk] = *reinterpret_cast<const u4*>(kt + krow * 256 + (((kk * 2 + hf) ^ (krow & 15)) << 4));
-      u4 va[2][4];
+      for (int kk = 0; kk < S::kK; ++kk)
+        ka[kk] = *reinterpret_cast<const u4*>(kt + krow * (2 * D) + (((kk * 2 + hf) ^ S::k_swz(krow)) << 4));
+      u4 va[2][S::kDB];
 #pragma unroll
       for (int q16 = 0; q16 < 2; ++q16) {
         const int g0 = kb * 32 + q16 * 16 + 4 * hf;    // tile row of the A operand's first key
         const int r0 = g0 + tr_key, r1 = g0 + 8 + tr_key;  // source rows of the two transposed reads
 #pragma unroll
-        for (int db = 0; db < 4; ++db) {
+        for (int db = 0; db < S::kDB; ++db) {
           const int c = 4 * db + tr_chunk;
-          const u2v lo = lds_read_tr16(vt + r0 * 256 + ((c ^ (4 * (r0 & 3))) << 4) + tr_half * 8);
-          const u2v hi = lds_read_tr16(vt + r1 * 256 + ((c ^ (4 * (r1 & 3))) << 4) + tr_half * 8);
+          const u2v lo = lds_read_tr16(vt + r0 * (2 * D) + ((c ^ S::v_swz(r0)) << 4) + tr_half * 8);
+          const u2v hi = lds_read_tr16(vt + r1 * (2 * D) + ((c ^ S::v_swz(r1)) << 4) + tr_half * 8);
           va[q16][db] = u4{lo.x, lo.y, hi.x, hi.y};
         }
       }
       __builtin_amdgcn_sched_barrier(0);   // keep the reads ahead of the products
 #pragma unroll
-      for (int kk = 0; kk < 8; ++kk)
+      for (int kk = 0; kk < S::kK; ++kk)
 #pragma unroll
         for (int cb = 0; cb < kCB; ++cb) sc[cb] = mfma(ka[kk], qb[cb][kk], sc[cb]);
       // only the block holding the end of the history and the chunk blocks
@@ -352,7 +371,7 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
           m[cb] = m_new;
           l[cb] *= alpha;
 #pragma unroll
-          for (int d = 0; d < 4; ++d) acc[cb][d] *= alpha;
+          for (int d = 0; d < S::kDB; ++d) acc[cb][d] *= alpha;
         }
         const float mcs = m[cb] * cs;
         uint32_t pw[8];
@@ -370,7 +389,7 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
 #pragma unroll
       for (int q16 = 0; q16 < 2; ++q16)
 #pragma unroll
-        for (int db = 0; db < 4; ++db)
+        for (int db = 0; db < S::kDB; ++db)
 #pragma unroll
           for (int cb = 0; cb < kCB; ++cb) acc[cb][db] = mfma(va[q16][db], pb[cb][q16], acc[cb][db]);
     }
@@ -384,9 +403,9 @@ __global__ void __launch_bounds__(kBlock) tg_prefill_kernel(PrefillParams p) {
     const int r = row0 + wave * kRowsPerWave + cb * 32 + (lane & 31);
     const int i = r / gqa, j = r % gqa;
     const float inv = 1.f / lt;
-    uint16_t* orow = p.out + (((int64_t)b * C + i) * Hq + h * gqa + j) * kD;
+    uint16_t* orow = p.out + (((int64_t)b * C + i) * Hq + h * gqa + j) * D;
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
+    for (int db = 0; db < S::kDB; ++db)
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
         const int dv = db * 32 + 8 * r4 + 4 * hf;
@@ -411,7 +430,8 @@ int32_t tg_prefill(const tg_prefill_args* a, void* hip_stream) {
   const tg_geometry& g = a->geom;
   if (int32_t rc = tg::check_geometry(&g)) return rc;
   if (a->dtype != TG_BF16) return tg::fail(TG_ERR_UNSUPPORTED, "prefill supports bf16 only");
-  if (g.head_dim != kD) return tg::fail(TG_ERR_UNSUPPORTED, "prefill supports head_dim 128 only (got %d)", g.head_dim);
+  if (g.head_dim != 64 && g.head_dim != 128)
+    return tg::fail(TG_ERR_UNSUPPORTED, "prefill supports head_dim 64 or 128 (got %d)", g.head_dim);
   if (g.page_size != kPage) return tg::fail(TG_ERR_UNSUPPORTED, "prefill supports page_size 16 only");
   const int gqa = g.num_q_heads / g.num_kv_heads;
   if (gqa < 1 || gqa > 16) return tg::fail(TG_ERR_UNSUPPORTED, "prefill supports 1..16 query heads per KV head");
@@ -441,12 +461,13 @@ int32_t tg_prefill(const tg_prefill_args* a, void* hip_stream) {
   p.heads_per_group = g.heads_per_group;
   p.gqa = gqa;
   p.row_tiles = (a->chunk_len * gqa + kRows - 1) / kRows;
-  const float scale = a->sm_scale != 0.f ? a->sm_scale : 1.0f / std::sqrt((float)kD);
+  const float scale = a->sm_scale != 0.f ? a->sm_scale : 1.0f / std::sqrt((float)g.head_dim);
   p.scale_log2 = scale * kLog2e;
   const int units = a->batch * g.num_kv_heads;
   if (a->block_order && a->num_blocks < 1) return tg::fail(TG_ERR_INVALID_ARG, "block_order needs num_blocks >= 1");
   const int blocks = a->block_order ? a->num_blocks : 8 * ((units + 7) / 8) * p.row_tiles;
-  hipLaunchKernelGGL(tg_prefill_kernel, dim3(blocks), dim3(kBlock), 0, static_cast<hipStream_t>(hip_stream), p);
+  auto kernel = g.head_dim == 128 ? tg_prefill_kernel<128> : tg_prefill_kernel<64>;
+  hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kBlock), 0, static_cast<hipStream_t>(hip_stream), p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "prefill launch failed: %s", hipGetErrorString(e));
   return TG_OK;

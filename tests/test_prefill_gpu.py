@@ -48,14 +48,15 @@ def _compare(ps, rows, what):
     return check_close(g.reshape(-1, g.shape[-1]), r.reshape(-1, r.shape[-1]), "bf16", what)
 
 
+@pytest.mark.parametrize("d", [128, 64])
 @pytest.mark.parametrize("gqa,C,Hp,ctx", [(4, 40, 2, 300), (1, 33, 1, 100), (3, 70, 2, (20, 600)), (8, 128, 4, 1000),
                                           (16, 9, 2, 50), (2, 1, 1, 64), (5, 200, 1, (1, 2000))])
-def test_prefill_small_vs_oracle(gqa, C, Hp, ctx):
+def test_prefill_small_vs_oracle(gqa, C, Hp, ctx, d):
     _gpu()
     H = 4 if Hp != 1 else 2
-    g = Geometry(1, H, H * gqa, 128, 16, Hp)
-    wl = custom(500 + gqa * 7 + C, g, 3, "bf16", ctx, chunk_len=C)
-    say(f"prefill gqa={gqa} C={C} Hp={Hp} ctx={wl.ctx_len.tolist()}")
+    g = Geometry(1, H, H * gqa, d, 16, Hp)
+    wl = custom(500 + gqa * 7 + C + d, g, 3, "bf16", ctx, chunk_len=C)
+    say(f"prefill d={d} gqa={gqa} C={C} Hp={Hp} ctx={wl.ctx_len.tolist()}")
     tables = Tables(wl)
     pool = torch.from_numpy(poisoned_host_pool(wl, tables)).to(torch.bfloat16).cuda()
     ps = PrefillSession(wl, tables=tables, fill="host", pool=pool)
@@ -65,11 +66,12 @@ def test_prefill_small_vs_oracle(gqa, C, Hp, ctx):
     _compare(ps, rows, f"gqa {gqa} C {C}")
 
 
-def test_prefill_short_and_empty_histories():
+@pytest.mark.parametrize("d", [128, 64])
+def test_prefill_short_and_empty_histories(d):
     """Histories shorter than the reservation, down to none at all (a prompt's first chunk): heads with 0,
     1, 15, 16, 17 and 63 retained rows and one with its whole reservation, NaN in every pool row past them."""
     _gpu()
-    g = Geometry(1, 8, 32, 128, 16, 2)
+    g = Geometry(1, 8, 32, d, 16, 2)
     wl = custom(640, g, 3, "bf16", (200, 900), chunk_len=77)
     tables = Tables(wl)
     pool = torch.from_numpy(poisoned_host_pool(wl, tables)).to(torch.bfloat16).cuda()
@@ -208,7 +210,7 @@ def test_prefill_block_order_does_not_change_results():
 
 
 def test_prefill_random_shapes_sweep():
-    """Seeded sweep: 10 random (gqa, KV heads, heads per group, batch, chunk length, context range) cases,
+    """Seeded sweep: 10 random (head_dim, gqa, KV heads, heads per group, batch, chunk length, context range) cases,
     every (request, query head) row against the oracle, NaN past the retained history."""
     _gpu()
     rng = np.random.default_rng(777)
@@ -220,9 +222,10 @@ def test_prefill_random_shapes_sweep():
         C = int(rng.integers(1, 301))
         lo = int(rng.integers(1, 300))
         hi = lo + int(rng.integers(0, 1500))
-        g = Geometry(1, H, H * gqa, 128, 16, Hp)
+        d = [64, 128][int(rng.integers(2))]
+        g = Geometry(1, H, H * gqa, d, 16, Hp)
         wl = custom(7000 + case, g, B, "bf16", (lo, hi) if hi > lo else lo, chunk_len=C)
-        say(f"prefill sweep case {case}: gqa{gqa} H{H} Hp{Hp} B{B} C{C} ctx={wl.ctx_len.tolist()}")
+        say(f"prefill sweep case {case}: d{d} gqa{gqa} H{H} Hp{Hp} B{B} C{C} ctx={wl.ctx_len.tolist()}")
         tables = Tables(wl)
         pool = torch.from_numpy(poisoned_host_pool(wl, tables)).to(torch.bfloat16).cuda()
         ps = PrefillSession(wl, tables=tables, fill="host", pool=pool)

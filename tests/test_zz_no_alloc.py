@@ -23,21 +23,21 @@ def _gpu():
         pytest.skip("no GPU")
 
 
-def _session(wl, mode, n_bins):
+def _session(wl, mode, n_bins, fused=False):
     tables = Tables(wl)
     dt = {"f32": torch.float32, "bf16": torch.bfloat16}[wl.dtype]
     pool = torch.from_numpy(poisoned_host_pool(wl, tables)).to(dt).cuda()
     return DecodeSession(wl, tables=tables, mode=mode, n_bins=n_bins, split_target=2 * n_bins, fill="host",
-                         pool=pool)
+                         pool=pool, fused_merge=fused)
 
 
-@pytest.mark.parametrize("dtype,d,gqa", [("bf16", 128, 8), ("f32", 64, 3)])
-def test_noalloc_matches_workspace_decode_twice(dtype, d, gqa):
+@pytest.mark.parametrize("dtype,d,gqa,fused", [("bf16", 128, 8, False), ("f32", 64, 3, False), ("bf16", 128, 8, True)])
+def test_noalloc_matches_workspace_decode_twice(dtype, d, gqa, fused):
     _gpu()
     big = custom(8801 + d, Geometry(2, 8, 8 * gqa, d, 16, 2), 6, dtype, (300, 6000), kv_scale=0.5)
     small = custom(8802 + d, Geometry(1, 4, 4 * gqa, d, 16, 2), 2, dtype, (20, 900), kv_scale=0.5)
     for wl, n_bins in ((big, 160), (small, 24)):          # the second call: a smaller input
-        s = _session(wl, tg.TG_PLAN_AOT_FILL, n_bins)
+        s = _session(wl, tg.TG_PLAN_AOT_FILL, n_bins, fused)
         parts = [s.plans[l]["num_partials"] for l in s.layers]
         say(f"noalloc {dtype} d{d} gqa{gqa}: B={wl.batch} L={wl.geom.num_layers} partials {parts}")
         assert max(parts) > 0
