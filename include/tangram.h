@@ -476,11 +476,13 @@ int32_t tg_compress_plan(const tg_geometry* geom, int32_t batch, int32_t layer, 
                          tg_compress_item* items, int32_t item_capacity, int32_t* keep_count,
                          int32_t* write_begin, int32_t* num_items);
 
-/* 5b. tg_compress (device): runs a tg_compress_plan as two launches on
- * hip_stream.  The select launch takes one workgroup per (b, h): it ranks the
- * chunk's entries and writes the indices of Top(keep_count[b][h]) to kept[].
- * The copy launch takes one workgroup per item: it copies the K and V rows of
- * ranks [rank_begin, rank_end) into their pages.
+/* 5b. tg_compress (device): runs a tg_compress_plan on hip_stream.  For
+ * chunk_len > 1024 it takes two launches: the select launch takes one
+ * workgroup per (b, h), ranks the chunk's entries and writes the indices of
+ * Top(keep_count[b][h]) to kept[]; the copy launch takes one workgroup per
+ * item and copies the K and V rows of ranks [rank_begin, rank_end) into their
+ * pages.  Shorter chunks take one launch in which every item's workgroup
+ * ranks its unit itself and copies its own ranks.  The results are the same.
  * DEVICE pointers:
  *   k_new, v_new [B][C][H][d] dtype: the chunk's K and V before compression
  *   scores  [B][H][C] float32: importance of every chunk entry (from the

@@ -2,13 +2,16 @@
 // per-head Top(count) selection over a chunk's importance scores and the
 // scatter of the kept K and V rows into the head's reserved ragged pages.
 //
-// Two launches on the caller's stream:
+// Chunks of up to kFusedMaxChunk tokens take one launch: every work item's
+// workgroup ranks its unit's chunk in LDS and copies its own ranks.  Longer
+// chunks take two launches on the caller's stream:
 //   select - one workgroup of 256 threads per (request, KV head) unit:
 //     1. the unit's n scores become order-preserving 32-bit keys in LDS
 //        (larger score = larger key; -0 maps to +0; NaN maps to 0, below all);
-//     2. a most-significant-digit-first radix select (four 8-bit passes, one
-//        LDS histogram per wave) finds the count-th largest key T and how many
-//        entries equal to T are kept (the lowest-index ones);
+//     2. a most-significant-digit-first radix select (up to four 8-bit
+//        passes, one LDS histogram per wave) finds the count-th largest key T
+//        and how many entries equal to T are kept (the lowest-index ones); it
+//        stops early once the chosen digit's whole bucket is kept;
 //     3. each wave walks its quarter of the tokens 64 at a time; ballots of
 //        the "kept" and "equal to T" predicates and lane-prefix bit counts
 //        give every kept entry its rank in token order, written to kept[].
@@ -25,9 +28,10 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
 constexpr int kBins = 256;           // one radix digit of 8 bits; == kThreads
-constexpr int kUnroll = 4;           // rows in flight per thread in the copy
+constexpr int kUnroll = 4;           // rows in flight per thread in the copy launch
 constexpr int kBatch = 8;            // score loads / LDS key reads in flight per thread
 constexpr int kGroups = 4;           // 64-token groups per batch of the ranking walk
+constexpr int kFusedMaxChunk = 1024; // chunks up to this many tokens are compressed in one launch
 
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
@@ -99,14 +103,17 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
   return (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-__global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectParams p) {
-  extern __shared__ uint32_t keys[];             // [n] keys of the unit's scores
+// Top(count) of one unit's chunk scores: the kept chunk indices in ascending
+// order go to kept[] (global, when write_out) and, when kept_lds is not NULL,
+// to kept_lds[0 .. count) as well.  Called by a whole workgroup of kThreads
+// threads; keys is LDS room for C keys.  Returns count.
+__device__ __forceinline__ int select_unit(const SelectParams& p, int64_t unit, uint32_t* keys, int32_t* kept_lds,
+                                           bool write_out = true) {
   __shared__ uint32_t hist[kWaves][kBins];
   __shared__ int32_t wave_cnt[2][kWaves];
-  __shared__ uint32_t pick[2];
+  __shared__ uint32_t pick[3];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t unit = blockIdx.x;
   const int b = (int)(unit / p.H);
   // the first batch of scores is requested before the counts arrive: it
   // covers chunk entries that exist whatever chunk_tokens says
@@ -119,7 +126,7 @@ __global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectPara
   }
   const int n = min(max(((const TG_CONST int32_t*)p.chunk_tokens)[b], 0), p.C);
   const int count = min(max(((const TG_CONST int32_t*)p.keep_count)[unit], 0), n);
-  if (count == 0) return;                        // the whole workgroup leaves together
+  if (count == 0) return 0;                      // the whole workgroup leaves together
   const bool keep_all = count >= n;
 
 #pragma unroll
@@ -147,8 +154,12 @@ __global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectPara
   }
   __syncthreads();
 
-  // radix select: thr = the count-th largest key, need = entries equal to thr
-  // that are kept
+  // radix select over the digits from the top: after each pass, thr holds the
+  // digits of the count-th largest key found so far (mask marks them) and
+  // need = how many keys with that prefix are kept.  When the whole bucket of
+  // the chosen prefix is kept (need == its size), the lower digits cannot
+  // change the kept set and the walk stops: the kept keys are then those whose
+  // prefix is larger than thr's, or equal to it.
   uint32_t thr = 0, mask = 0;
   int need = count;
   if (!keep_all) {
@@ -185,6 +196,7 @@ __global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectPara
           if (run < need && run + c[j] >= need) {
             pick[0] = 255u - 4u * lane - j;
             pick[1] = (uint32_t)(need - run);
+            pick[2] = (uint32_t)(run + c[j] == need);   // the bucket is kept whole
           }
           run += c[j];
         }
@@ -193,6 +205,7 @@ __global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectPara
       thr |= pick[0] << shift;
       mask |= 0xffu << shift;
       need = (int)pick[1];
+      if (pick[2]) break;
     }
   }
 
@@ -206,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectPara
 #pragma unroll
     for (int u = 0; u < kGroups; ++u) {
       const int t = base + 64 * u + lane;
-      kk[u] = t < t_end ? keys[t] : 0u;
+      kk[u] = t < t_end ? keys[t] & mask : 0u;
     }
 #pragma unroll
     for (int u = 0; u < kGroups; ++u) {
@@ -232,7 +245,7 @@ __global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectPara
 #pragma unroll
     for (int u = 0; u < kGroups; ++u) {
       const int t = base + 64 * u + lane;
-      kk[u] = t < t_end ? keys[t] : 0u;
+      kk[u] = t < t_end ? keys[t] & mask : 0u;
     }
 #pragma unroll
     for (int u = 0; u < kGroups; ++u) {
@@ -242,20 +255,30 @@ __global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectPara
       const uint64_t eq_mask = __ballot(eq);
       const bool keep = valid && (keep_all || kk[u] > thr || (eq && run_eq + lanes_below(eq_mask) < need));
       const uint64_t keep_mask = __ballot(keep);
-      if (keep) out[run_kept + lanes_below(keep_mask)] = t;
+      if (keep) {
+        const int r = run_kept + lanes_below(keep_mask);
+        if (write_out) out[r] = t;
+        if (kept_lds) kept_lds[r] = t;
+      }
       run_eq += __popcll(eq_mask);
       run_kept += __popcll(keep_mask);
     }
   }
+  return count;
 }
 
-__global__ __launch_bounds__(kThreads) void tg_compress_copy_kernel(CopyParams p) {
-  const tg_compress_item it = load_item((const TG_CONST tg_compress_item*)p.items + blockIdx.x);
+__global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectParams p) {
+  extern __shared__ uint32_t keys[];             // [C] keys of the unit's scores
+  select_unit(p, blockIdx.x, keys, nullptr);
+}
+
+// Copies the K and V rows of ranks [r0, r0 + rows) of one unit: rank j's
+// chunk index is tok(j); it goes to the head's entry cursor + j.  Called by a
+// whole workgroup, kUnroll rows in flight per thread.
+template <int kUnroll, typename TokFn>
+__device__ __forceinline__ void copy_rows(const CopyParams& p, const tg_compress_item& it, int r0, int rows,
+                                          TokFn tok) {
   const int tid = threadIdx.x;
-  const int r0 = max(it.rank_begin, 0);
-  const int r1 = min(min(it.rank_end, min(it.count, p.C)), r0 + TG_COMPRESS_MAX_ROWS);
-  const int rows = r1 - r0;
-  const int32_t* src_tok = p.kept + ((int64_t)it.b * p.H + it.kv_head) * p.C + r0;
   const int lpr = p.row_u4;
   const int rpp = kThreads / lpr;               // rows per pass of the workgroup
   const int sub = tid % lpr, rsel = tid / lpr;
@@ -263,30 +286,55 @@ __global__ __launch_bounds__(kThreads) void tg_compress_copy_kernel(CopyParams p
   const int64_t src0 = ((int64_t)it.b * p.C * p.H + it.kv_head) * lpr + sub;
   const int64_t v_plane = (int64_t)p.Hp * p.P * lpr;  // V rows of a page follow its K rows
   for (int base = 0; base < rows; base += kUnroll * rpp) {
+    // every load of the batch (K row, V row, destination page id) goes out
+    // before the first result is used, so a batch costs one memory round trip
+    // (straight-line: rows past the end load the last row again and store nothing)
     u4 kk[kUnroll], vv[kUnroll];
-    int64_t dst[kUnroll];
+    int32_t page[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int j = base + u * rpp + rsel;
-      if (j < rows) {
-        const int t = min(max(src_tok[j], 0), p.C - 1);   // in range by construction; clamped for safety
-        const int64_t src = src0 + t * tok_stride;
-        kk[u] = p.k_new[src];
-        vv[u] = p.v_new[src];
-        const int pos = it.cursor + r0 + j;
-        const int64_t page = p.pt_pages[it.pt_base + pos / p.P];
-        dst[u] = ((page * 2 * p.Hp + it.slot) * p.P + pos % p.P) * lpr + sub;
-      }
+      const int j = min(base + u * rpp + rsel, rows - 1);
+      const int t = min(max(tok(j), 0), p.C - 1);   // in range by construction; clamped for safety
+      const int64_t src = src0 + t * tok_stride;
+      kk[u] = p.k_new[src];
+      vv[u] = p.v_new[src];
+      page[u] = p.pt_pages[it.pt_base + (it.cursor + r0 + j) / p.P];
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int j = base + u * rpp + rsel;
       if (j < rows) {
-        p.pool[dst[u]] = kk[u];
-        p.pool[dst[u] + v_plane] = vv[u];
+        const int pos = it.cursor + r0 + j;
+        const int64_t dst = (((int64_t)page[u] * 2 * p.Hp + it.slot) * p.P + pos % p.P) * lpr + sub;
+        p.pool[dst] = kk[u];
+        p.pool[dst + v_plane] = vv[u];
       }
     }
   }
+}
+
+__global__ __launch_bounds__(kThreads) void tg_compress_copy_kernel(CopyParams p) {
+  const tg_compress_item it = load_item((const TG_CONST tg_compress_item*)p.items + blockIdx.x);
+  const int r0 = max(it.rank_begin, 0);
+  const int r1 = min(min(it.rank_end, min(it.count, p.C)), r0 + TG_COMPRESS_MAX_ROWS);
+  const int32_t* src_tok = p.kept + ((int64_t)it.b * p.H + it.kv_head) * p.C + r0;
+  copy_rows<kUnroll>(p, it, r0, r1 - r0, [&](int j) { return src_tok[j]; });
+}
+
+// Short chunks in one launch: every work item's workgroup ranks its unit's
+// chunk itself (into LDS; the unit's first item also writes kept[]) and
+// copies its own ranks.  A unit's selection runs once per item, which at short
+// chunks costs less than the second launch and the round trip of the kept
+// indices through global memory that the two-launch form pays.
+__global__ __launch_bounds__(kThreads) void tg_compress_fused_kernel(SelectParams sp, CopyParams p) {
+  extern __shared__ uint32_t lds[];             // [C] keys, then [C] kept chunk indices
+  const tg_compress_item it = load_item((const TG_CONST tg_compress_item*)p.items + blockIdx.x);
+  int32_t* kept_lds = reinterpret_cast<int32_t*>(lds + p.C);
+  const int count = select_unit(sp, (int64_t)it.b * p.H + it.kv_head, lds, kept_lds, it.rank_begin == 0);
+  __syncthreads();
+  const int r0 = max(it.rank_begin, 0);
+  const int r1 = min(min(it.rank_end, min(count, min(it.count, p.C))), r0 + TG_COMPRESS_MAX_ROWS);
+  copy_rows<kUnroll>(p, it, r0, r1 - r0, [&](int j) { return kept_lds[r0 + j]; });
 }
 
 }  // namespace
@@ -308,22 +356,6 @@ extern "C" int32_t tg_compress(const tg_compress_args* a, void* hip_stream) {
     return tg::fail(TG_ERR_INVALID_ARG, "NULL device pointer");
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   SelectParams s;
-  s.scores = reinterpret_cast<const uint32_t*>(a->scores);
-  s.chunk_tokens = a->chunk_tokens;
-  s.keep_count = a->keep_count;
-  s.kept = a->kept;
-  s.H = g.num_kv_heads;
-  s.C = a->chunk_len;
-  const size_t lds = (size_t)a->chunk_len * sizeof(uint32_t);
-  static_assert(kBins == kThreads, "one histogram bin per thread");
-  if (lds > 32768) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(tg_compress_select_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress LDS attribute: %s", hipGetErrorString(e));
-  }
-  hipLaunchKernelGGL(tg_compress_select_kernel, dim3(a->batch * g.num_kv_heads), dim3(kThreads), lds, stream, s);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress select launch failed: %s", hipGetErrorString(e));
   CopyParams c;
   c.k_new = static_cast<const u4*>(a->k_new);
   c.v_new = static_cast<const u4*>(a->v_new);
@@ -336,6 +368,29 @@ extern "C" int32_t tg_compress(const tg_compress_args* a, void* hip_stream) {
   c.Hp = g.heads_per_group;
   c.P = g.page_size;
   c.row_u4 = g.head_dim * (a->dtype == TG_F32 ? 4 : 2) / 16;
+  s.scores = reinterpret_cast<const uint32_t*>(a->scores);
+  s.chunk_tokens = a->chunk_tokens;
+  s.keep_count = a->keep_count;
+  s.kept = a->kept;
+  s.H = g.num_kv_heads;
+  s.C = a->chunk_len;
+  static_assert(kBins == kThreads, "one histogram bin per thread");
+  if (a->chunk_len <= kFusedMaxChunk) {
+    const size_t lds2 = 2 * (size_t)a->chunk_len * sizeof(uint32_t);   // keys + kept indices
+    hipLaunchKernelGGL(tg_compress_fused_kernel, dim3(a->num_items), dim3(kThreads), lds2, stream, s, c);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress launch failed: %s", hipGetErrorString(e));
+    return TG_OK;
+  }
+  const size_t lds = (size_t)a->chunk_len * sizeof(uint32_t);
+  if (lds > 32768) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(tg_compress_select_kernel),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress LDS attribute: %s", hipGetErrorString(e));
+  }
+  hipLaunchKernelGGL(tg_compress_select_kernel, dim3(a->batch * g.num_kv_heads), dim3(kThreads), lds, stream, s);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress select launch failed: %s", hipGetErrorString(e));
   hipLaunchKernelGGL(tg_compress_copy_kernel, dim3(a->num_items), dim3(kThreads), 0, stream, c);
   e = hipGetLastError();
   if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress copy launch failed: %s", hipGetErrorString(e));
