@@ -301,13 +301,22 @@ int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_le
     if (!pt_pages) return TG_OK;  // size query: nothing consumed, free list not examined
     if (k > num_free) return fail(TG_ERR_OUT_OF_PAGES, "reservation needs %lld pages, %lld free", (long long)k, (long long)num_free);
     if (pt_capacity < k) return fail(TG_ERR_BUFFER_TOO_SMALL, "pt_pages holds %lld, need %lld", (long long)pt_capacity, (long long)k);
-    // the consumed ids must be distinct pages of the pool: chunks checked in
-    // parallel against one atomic bitmap; on any failure a sequential pass
-    // reports the first offending entry, so the message does not depend on timing
-    std::unique_ptr<uint64_t[]> seen(new uint64_t[(size_t)(pool_pages + 63) / 64]());
-    const int nthreads = host_threads(k);
+    // the consumed ids must be distinct pages of the pool.  Each thread marks
+    // its chunk of the list in a bitmap of its own (plain stores: no atomics,
+    // no cache lines shared between threads); then the pool's id range is cut
+    // among the threads and each one ORs the bitmaps' words of its range
+    // together, flagging any bit set in two of them.  The bitmaps take
+    // threads * pool_pages / 8 bytes, kept within 256 MiB by using fewer
+    // threads.  On any failure a sequential pass reports the first offending
+    // entry, so the message does not depend on timing.
+    const int64_t words = (pool_pages + 63) / 64;
+    const int64_t map_cap = std::max<int64_t>(1, (int64_t(256) << 20) / std::max<int64_t>(8, words * 8));
+    const int nthreads = (int)std::min<int64_t>(host_threads(k), map_cap);
+    std::unique_ptr<uint64_t[]> maps(new uint64_t[(size_t)(nthreads * words)]);
     std::vector<uint8_t> bad((size_t)nthreads, 0);
     parallel_chunks(k, nthreads, [&](int w, int64_t lo, int64_t hi) {
+      uint64_t* m = maps.get() + (size_t)w * words;
+      std::memset(m, 0, (size_t)words * sizeof(uint64_t));
       for (int64_t i = lo; i < hi; ++i) {
         const int32_t p = free_pages[i];
         if (p < 0 || p >= pool_pages) {
@@ -315,12 +324,27 @@ int32_t tg_reserve(const tg_geometry* geom, int32_t batch, const int32_t* ctx_le
           return;
         }
         const uint64_t bit = 1ull << (p & 63);
-        if (__atomic_fetch_or(&seen[p >> 6], bit, __ATOMIC_RELAXED) & bit) {
+        if (m[p >> 6] & bit) {
           bad[w] = 1;
           return;
         }
+        m[p >> 6] |= bit;
       }
-  });
+    });
+    if (std::find(bad.begin(), bad.end(), 1) == bad.end() && nthreads > 1)
+      parallel_chunks(words, nthreads, [&](int w, int64_t lo, int64_t hi) {
+        for (int64_t j = lo; j < hi; ++j) {
+          uint64_t acc = 0;
+          for (int t = 0; t < nthreads; ++t) {
+            const uint64_t x = maps[(size_t)t * words + j];
+            if (acc & x) {
+              bad[w] = 1;
+              return;
+            }
+            acc |= x;
+          }
+        }
+      });
   if (std::find(bad.begin(), bad.end(), 1) != bad.end()) {
     std::vector<uint8_t> once((size_t)pool_pages, 0);
     for (int64_t i = 0; i < k; ++i) {

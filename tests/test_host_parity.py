@@ -195,6 +195,36 @@ def test_bad_page_ids_rejected(free):
     assert e.value.code == tg.TG_ERR_INVALID_ARG
 
 
+@pytest.mark.parametrize("threads", ["1", "4", "8"])
+def test_page_id_check_across_host_threads(threads, monkeypatch):
+    """600 000 consumed pages, so the id check runs on several host threads, each marking its chunk of the
+    list in a bitmap of its own: a repeat inside one chunk, a repeat across two chunks and an id outside the
+    pool must all be rejected, and a valid permutation must be taken as is."""
+    monkeypatch.setenv("TG_HOST_THREADS", threads)
+    geom = Geometry(1, 1, 1, 64, 16, 1)
+    n = 600_000
+    ctx, ratio = np.array([16 * n], np.int32), np.ones((1, 1, 1))
+    gof = np.zeros((1, 1), np.int32)
+    pool = n + 5000
+    free = np.random.default_rng(5).permutation(pool).astype(np.int32)
+    res = tg.tg_reserve(geom, ctx, ratio, None, gof, free, pool)
+    assert res["pages_needed"] == n and np.array_equal(res["pt_pages"], free[:n])
+    for i, j in ((3, 7), (5, n - 2), (n // 2 - 1, n // 2 + 1)):
+        bad = free.copy()
+        bad[j] = bad[i]
+        with pytest.raises(tg.TangramError) as e:
+            tg.tg_reserve(geom, ctx, ratio, None, gof, bad, pool)
+        assert e.value.code == tg.TG_ERR_INVALID_ARG and "twice" in tg.tg_last_error(), (i, j)
+    ok = free.copy()
+    ok[n] = ok[0]              # a repeat beyond the consumed prefix is never examined
+    assert np.array_equal(tg.tg_reserve(geom, ctx, ratio, None, gof, ok, pool)["pt_pages"], free[:n])
+    out = free.copy()
+    out[n - 1] = pool
+    with pytest.raises(tg.TangramError) as e:
+        tg.tg_reserve(geom, ctx, ratio, None, gof, out, pool)
+    assert e.value.code == tg.TG_ERR_INVALID_ARG and "outside the pool" in tg.tg_last_error()
+
+
 def test_plan_rejects_length_beyond_table():
     wl = config(1)
     perm, gof, sof = tg.tg_cluster_heads(wl.geom, wl.budget)
