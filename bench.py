@@ -63,6 +63,13 @@ def copy_probe(nbytes):
     print(json.dumps({"copy_probe_bytes": nbytes}))
 
 
+def compress_kernel_name(chunk_len):
+    from paper_2606_06302_amd import tangram as tg
+    if chunk_len <= tg.TG_COMPRESS_ONE_LAUNCH_MAX_CHUNK:
+        return "tg_compress (one launch: each item selects its unit and copies its ranks)"
+    return "tg_compress (select + copy launches)"
+
+
 def measured_traffic(workload, mode=None, n_bins=None, path=TRAFFIC_FILE, src=DECODE_SRC):
     """HBM bytes per launch from committed rocprofv3 counter runs, if they were
     taken on the current kernel source and the same workload (and plan); else None."""
@@ -261,7 +268,7 @@ def bench_prefill(args):
                      "kernel": "tg_prefill_kernel", "avg_launch_us": round(pre_ms * 1e3, 2),
                      "algorithmic_flops_per_launch": flops},
         "compress": {"bound": "hbm", "achieved": round(comp_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(comp_gbs / HBM_PEAK_GBS, 4), "kernel": "tg_compress (select + copy launches)",
+                     "frac": round(comp_gbs / HBM_PEAK_GBS, 4), "kernel": compress_kernel_name(C),
                      "avg_launch_us": round(comp_ms * 1e3, 2), "algorithmic_bytes_per_launch": comp_bytes,
                      "kept_rows": int(cs.plan["keep_count"].sum()), "work_items": cs.plan["num_items"]},
         "cpu_baseline": None,
@@ -315,7 +322,7 @@ def bench_compress(args):
                       "work_items": cs.plan["num_items"], "parallelism": "single GPU"},
            "roofline": {"bound": "hbm", "achieved": round(gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": round(gbs / HBM_PEAK_GBS, 4), "traffic": None,
-                        "kernel": "tg_compress (select + copy launches)", "avg_launch_us": round(us, 2),
+                        "kernel": compress_kernel_name(C), "avg_launch_us": round(us, 2),
                         "algorithmic_bytes_per_launch": nbytes},
            "cpu_baseline": None}
     if not args.no_cpu_baseline:

@@ -467,7 +467,7 @@ typedef struct {
   int32_t rank_end;
 } tg_compress_item;   /* 40 bytes */
 
-enum { TG_COMPRESS_MAX_CHUNK = 16384, TG_COMPRESS_MAX_ROWS = 256 };
+enum { TG_COMPRESS_MAX_CHUNK = 16384, TG_COMPRESS_MAX_ROWS = 256, TG_COMPRESS_ONE_LAUNCH_MAX_CHUNK = 1024 };
 
 int32_t tg_compress_plan(const tg_geometry* geom, int32_t batch, int32_t layer, int32_t chunk_len,
                          const int32_t* chunk_start, const int32_t* chunk_tokens, const double* ratio,
@@ -477,7 +477,7 @@ int32_t tg_compress_plan(const tg_geometry* geom, int32_t batch, int32_t layer, 
                          int32_t* write_begin, int32_t* num_items);
 
 /* 5b. tg_compress (device): runs a tg_compress_plan on hip_stream.  For
- * chunk_len > 1024 it takes two launches: the select launch takes one
+ * chunk_len > TG_COMPRESS_ONE_LAUNCH_MAX_CHUNK (1024) it takes two launches: the select launch takes one
  * workgroup per (b, h), ranks the chunk's entries and writes the indices of
  * Top(keep_count[b][h]) to kept[]; the copy launch takes one workgroup per
  * item and copies the K and V rows of ranks [rank_begin, rank_end) into their

@@ -31,7 +31,7 @@ constexpr int kBins = 256;           // one radix digit of 8 bits; == kThreads
 constexpr int kUnroll = 4;           // rows in flight per thread in the copy launch
 constexpr int kBatch = 8;            // score loads / LDS key reads in flight per thread
 constexpr int kGroups = 4;           // 64-token groups per batch of the ranking walk
-constexpr int kFusedMaxChunk = 1024; // chunks up to this many tokens are compressed in one launch
+constexpr int kFusedMaxChunk = TG_COMPRESS_ONE_LAUNCH_MAX_CHUNK; // chunks up to this many tokens are compressed in one launch
 
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 

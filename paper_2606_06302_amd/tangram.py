@@ -32,7 +32,7 @@ COMPRESS_ITEM_DTYPE = np.dtype([("pt_base", "<i8"), ("b", "<i4"), ("kv_head", "<
                                 ("n_valid", "<i4"), ("cursor", "<i4"), ("count", "<i4"), ("rank_begin", "<i4"),
                                 ("rank_end", "<i4")])
 assert COMPRESS_ITEM_DTYPE.itemsize == 40
-TG_COMPRESS_MAX_CHUNK, TG_COMPRESS_MAX_ROWS = 16384, 256
+TG_COMPRESS_MAX_CHUNK, TG_COMPRESS_MAX_ROWS, TG_COMPRESS_ONE_LAUNCH_MAX_CHUNK = 16384, 256, 1024
 
 
 class TangramError(RuntimeError):

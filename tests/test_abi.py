@@ -56,8 +56,8 @@ def test_c_struct_layouts_match_the_binding(tmp_path):
         lines.append(f'printf("{name} %zu\\n", sizeof({name}));')
         for f in dt.names:
             lines.append(f'printf("{name}.{f} %zu\\n", offsetof({name}, {f}));')
-    lines.append('printf("TG_COMPRESS_MAX_CHUNK %d\\nTG_COMPRESS_MAX_ROWS %d\\n", TG_COMPRESS_MAX_CHUNK, '
-                 'TG_COMPRESS_MAX_ROWS);')
+    lines.append('printf("TG_COMPRESS_MAX_CHUNK %d\\nTG_COMPRESS_MAX_ROWS %d\\nTG_COMPRESS_ONE_LAUNCH_MAX_CHUNK %d\\n", '
+                 'TG_COMPRESS_MAX_CHUNK, TG_COMPRESS_MAX_ROWS, TG_COMPRESS_ONE_LAUNCH_MAX_CHUNK);')
     lines.append("return 0; }")
     src = tmp_path / "layout.c"
     src.write_text("\n".join(lines))
@@ -75,3 +75,4 @@ def test_c_struct_layouts_match_the_binding(tmp_path):
             assert int(got[f"{name}.{f}"]) == dt.fields[f][1], (name, f)
     assert int(got["TG_COMPRESS_MAX_CHUNK"]) == tg.TG_COMPRESS_MAX_CHUNK
     assert int(got["TG_COMPRESS_MAX_ROWS"]) == tg.TG_COMPRESS_MAX_ROWS
+    assert int(got["TG_COMPRESS_ONE_LAUNCH_MAX_CHUNK"]) == tg.TG_COMPRESS_ONE_LAUNCH_MAX_CHUNK
