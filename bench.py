@@ -18,6 +18,7 @@ divided by the measured step time.
     python bench.py --compress-chunk C     # chunk compression alone, chunk of C tokens
     python bench.py --memory               # host only: memory reclaimed per paging scheme
     python bench.py --plan-reuse           # planning cost vs decode step, 28 to 80 layers
+    python bench.py --tail-analysis        # decode layer tail: per-worker speed, per-XCD speed, weights
     python bench.py --lifecycle            # host only: calibration, reservation threads, release
     python bench.py --copy-probe BYTES     # plain copy kernel, for counter calibration
 """
@@ -367,6 +368,86 @@ def compress_cpu_baseline(cs, seconds, seed=10):
             "gpu_matches_oracle": ok}
 
 
+def bench_tail(args):
+    """Where the decode layer's tail comes from (sequential-fill plan, HIP-graph step): per-worker
+    stamps give every worker's pages per microsecond; their repeatability between two stamped runs,
+    their spread over the 8 XCDs, and the step time after re-planning with per-bin or per-XCD bin
+    weights taken from one stamped step."""
+    import torch
+    sys.path.insert(0, ROOT)
+    from paper_2606_06302_amd import tangram as tg
+    from paper_2606_06302_amd.runner import REALTIME_HZ, DecodeSession
+    from workloads import config
+    wl = config(args.config)
+    s = DecodeSession(wl, mode=tg.TG_PLAN_AOT_FILL, fill="device")
+    stream = torch.cuda.Stream()
+    kv = s.t.kv_bytes()
+    us = 1e6 / REALTIME_HZ
+
+    def step_gbs(n=30):
+        with torch.cuda.stream(stream):
+            graph = s.capture_step(stream)
+            for _ in range(3):
+                graph.replay()
+            stream.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(n):
+                graph.replay()
+            e1.record(stream)
+            stream.synchronize()
+        return kv / (e0.elapsed_time(e1) / n * 1e-3) / 1e9
+
+    def stamped():
+        """per layer: relative speed per bin (NaN for empty bins), span and mean busy time (us)"""
+        speed, span, busy = {}, [], []
+        for l in s.layers:
+            t = s.stamp_layer(l, stream)
+            pages = s.bin_pages(l)
+            b = np.maximum(t[:, 1] - t[:, 0], 1)
+            sp = np.where(pages > 0, pages / b, np.nan)
+            speed[l] = sp / np.nanmean(sp)
+            span.append((t[:, 1].max() - t[:, 0].min()) * us)
+            busy.append(b[pages > 0].mean() * us)
+        return speed, float(np.mean(span)), float(np.mean(busy))
+
+    def row(name):
+        gbs = step_gbs()
+        sp, span, busy = stamped()
+        log(f"[bench] {name}: {gbs:.1f} GB/s; mean layer span {span:.1f} us, mean worker busy {busy:.1f} us")
+        return {"plan": name, "GBps": round(gbs, 1), "layer_span_us": round(span, 1),
+                "worker_busy_us": round(busy, 1), "busy_over_span": round(busy / span, 4)}, sp
+
+    step_gbs(5)
+    rows = []
+    r, sp0 = row("equal bins")
+    rows.append(r)
+    sp1, _, _ = stamped()
+    xcd = (np.arange(s.n_bins) // 4) % 8
+    corr = [np.corrcoef(sp0[l][np.isfinite(sp0[l])], sp1[l][np.isfinite(sp1[l])])[0, 1] for l in s.layers]
+    per_xcd = np.array([[np.nanmean(sp0[l][xcd == k]) for k in range(8)] for l in s.layers])
+    cv = [np.nanstd(sp0[l]) for l in s.layers]
+    within = [np.nanstd(sp0[l] / per_xcd[i][xcd]) for i, l in enumerate(s.layers)]
+    s.set_bin_weights({l: np.maximum(1, np.round(1000 * np.nan_to_num(sp0[l], nan=1.0))).astype(np.int32)
+                       for l in s.layers})
+    r, _ = row("per-bin weights from one stamped step")
+    rows.append(r)
+    s.set_bin_weights({l: np.maximum(1, np.round(1000 * per_xcd[i][xcd] / per_xcd[i].mean())).astype(np.int32)
+                       for i, l in enumerate(s.layers)})
+    r, _ = row("per-layer per-XCD weights from one stamped step")
+    rows.append(r)
+    out = {"metric": "decode layer tail analysis (per-worker stamps)", "data": "synthetic",
+           "config": {"workload": wl.name, "plan": "fill", "n_bins": s.n_bins, "launch": "hip graph"},
+           "speed_cv_median": round(float(np.median(cv)), 4),
+           "speed_cv_within_xcd_median": round(float(np.median(within)), 4),
+           "speed_corr_between_runs_median": round(float(np.median(corr)), 3),
+           "per_xcd_speed_mean": [round(float(v), 3) for v in per_xcd.mean(0) / per_xcd.mean()],
+           "per_xcd_speed_min": [round(float(v), 3) for v in (per_xcd / per_xcd.mean(1, keepdims=True)).min(0)],
+           "per_xcd_speed_max": [round(float(v), 3) for v in (per_xcd / per_xcd.mean(1, keepdims=True)).max(0)],
+           "rows": rows}
+    print(json.dumps(out), flush=True)
+
+
 def bench_memory(args):
     """Memory reclaimed by ragged paging (host, integer; no GPU): KV slots each scheme allocates for the
     same retained lengths, per heads-per-group and grouping, and the block-table build time."""
@@ -566,6 +647,8 @@ def main():
     ap.add_argument("--compress-chunk", type=int, default=0,
                     help="time only the compression of a chunk of this many tokens (config 5's requests)")
     ap.add_argument("--rows-per-item", type=int, default=0)
+    ap.add_argument("--tail-analysis", action="store_true",
+                    help="per-worker stamps of the fill plan: speed spread, per-XCD speed, re-planning with weights")
     ap.add_argument("--plan-reuse", action="store_true",
                     help="planning cost against the decode step (append + attention) for 28 to 80 layers")
     ap.add_argument("--lifecycle", action="store_true",
@@ -597,6 +680,8 @@ def main():
         return bench_compress(args)
     if args.plan_reuse:
         return bench_plan_reuse(args)
+    if args.tail_analysis:
+        return bench_tail(args)
     if args.config == 5:
         return bench_prefill(args)
     mode = {"aot": tg.TG_PLAN_AOT, "fill": tg.TG_PLAN_AOT_FILL, "naive": tg.TG_PLAN_NAIVE,

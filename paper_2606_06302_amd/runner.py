@@ -114,6 +114,8 @@ class DecodeSession:
             # Algorithm 1 on the static budgets with N_CTA = n_bins: one row of S per layer
             S = tg.tg_split_map(g, self.wl.budget, self.t.perm, self.n_bins)
             weights = {l: S[l] for l in self.layers}
+        elif isinstance(self.bin_weights, dict):
+            weights = self.bin_weights
         else:
             weights = {l: self.bin_weights for l in self.layers}
         self.plans = {l: tg.tg_build_plan(g, B, l, self.t.kv_len, self.t.pt_offsets, self.t.group_of,
@@ -147,26 +149,14 @@ class DecodeSession:
         pages = np.zeros(classes)
         busy = np.zeros(classes)
         for l in self.layers:
-            dp = self.dplans[l]
-            nb = dp.host["num_bins"]
-            ts = torch.zeros(2 * nb, dtype=torch.int64, device=self.device)
-            args = tg.tg_decode_args.from_buffer_copy(dp.args)
-            args.timestamps = ts.data_ptr()
-            tg.tg_decode(args, stream)
-            torch.cuda.synchronize()
-            t = ts.view(-1, 2).cpu().numpy()
-            npages = -(-self.item_tokens(l) // self.wl.geom.page_size)
-            bo = self.plans[l]["bin_offsets"]
-            per_bin = np.add.reduceat(npages, bo[:-1]) if len(npages) else np.zeros(nb)
-            per_bin[np.diff(bo) == 0] = 0
-            cls = (np.arange(nb) // 4) % classes
+            t = self.stamp_layer(l, stream)
+            per_bin = self.bin_pages(l)
+            cls = (np.arange(len(per_bin)) // 4) % classes
             np.add.at(pages, cls, per_bin)
-            np.add.at(busy, cls, (t[:, 1] - t[:, 0]).astype(np.float64))
+            np.add.at(busy, cls, t[:, 1] - t[:, 0])
         speed = pages / np.maximum(busy, 1)
         speed = speed / speed.mean()
-        self.bin_weights = np.round(1000 * speed[(np.arange(self.n_bins) // 4) % classes]).astype(np.int32)
-        self._build_plans()
-        self._bind()
+        self.set_bin_weights(np.round(1000 * speed[(np.arange(self.n_bins) // 4) % classes]).astype(np.int32))
         return speed
 
     def enable_append(self, k_tok=None, v_tok=None):
@@ -210,19 +200,41 @@ class DecodeSession:
             self.run_step(stream)
         return graph
 
+    def stamp_layer(self, l, stream=None):
+        """Runs layer l's decode once with per-worker stamps: [n_bins][2] start / end s_memrealtime
+        ticks (REALTIME_HZ), as float64 on the host."""
+        dp = self.dplans[l]
+        ts = torch.zeros(2 * dp.host["num_bins"], dtype=torch.int64, device=self.device)
+        args = tg.tg_decode_args.from_buffer_copy(dp.args)
+        args.timestamps = ts.data_ptr()
+        tg.tg_decode(args, stream)
+        torch.cuda.synchronize()
+        return ts.view(-1, 2).cpu().numpy().astype(np.float64)
+
+    def bin_pages(self, l):
+        """Pages every bin of layer l's plan reads (0 for empty bins)."""
+        nb = self.plans[l]["bin_offsets"].shape[0] - 1
+        npages = -(-self.item_tokens(l) // self.wl.geom.page_size)
+        bo = self.plans[l]["bin_offsets"]
+        per_bin = np.add.reduceat(npages, bo[:-1]).astype(np.float64) if len(npages) else np.zeros(nb)
+        per_bin[np.diff(bo) == 0] = 0
+        return per_bin
+
+    def set_bin_weights(self, weights):
+        """Rebuilds the sequential-fill plans with bin weights: one int32 array for every layer, a
+        dict of per-layer arrays, or None for equal bins."""
+        assert self.mode == tg.TG_PLAN_AOT_FILL, "bin weights apply to the sequential-fill plan"
+        self.bin_weights = weights
+        self._build_plans()
+        self._bind()
+
     def worker_timeline(self, stream=None):
         """Runs one step with per-worker start/end stamps (s_memrealtime ticks) and returns, per layer,
         a dict over the workers that had work, in microseconds: busy_max and busy_mean (end - start),
         ramp (last start - first start), tail (last end - first end), span (last end - first start)."""
         res = []
         for l in self.layers:
-            dp = self.dplans[l]
-            ts = torch.zeros(2 * dp.host["num_bins"], dtype=torch.int64, device=self.device)
-            args = tg.tg_decode_args.from_buffer_copy(dp.args)
-            args.timestamps = ts.data_ptr()
-            tg.tg_decode(args, stream)
-            torch.cuda.synchronize()
-            t = ts.view(-1, 2).cpu().numpy()[np.diff(self.plans[l]["bin_offsets"]) > 0].astype(np.float64)
+            t = self.stamp_layer(l, stream)[np.diff(self.plans[l]["bin_offsets"]) > 0]
             us = 1e6 / REALTIME_HZ
             busy = (t[:, 1] - t[:, 0]) * us
             res.append(dict(busy_max=float(busy.max()), busy_mean=float(busy.mean()),
