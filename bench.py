@@ -64,6 +64,11 @@ def copy_probe(nbytes):
     print(json.dumps({"copy_probe_bytes": nbytes}))
 
 
+def host_cores():
+    """The host's CPU share for the oracle runs: OMP_NUM_THREADS when the environment sets it."""
+    return min(len(os.sched_getaffinity(0)), int(os.environ.get("OMP_NUM_THREADS", "0")) or 10**6)
+
+
 def compress_kernel_name(chunk_len):
     from paper_2606_06302_amd import tangram as tg
     if chunk_len <= tg.TG_COMPRESS_ONE_LAUNCH_MAX_CHUNK:
@@ -155,9 +160,9 @@ def step_stats(run, stream, n, flush):
     return float(np.median(t)), float(np.percentile(t, 10)), float(np.percentile(t, 90))
 
 
-def prefill_cpu_baseline(ps, seconds, seed=9):
+def prefill_cpu_baseline(ps, seconds, seed=9, threads=1):
     """The fp64 oracle's chunked-prefill attention on sampled (request, query head) rows of the same
-    workload, timed on the host with one BLAS thread; TFLOP/s of those rows' algorithmic flops."""
+    workload, timed on the host with `threads` BLAS threads; TFLOP/s of those rows' algorithmic flops."""
     sys.path.insert(0, ROOT)
     from threadpoolctl import threadpool_limits
 
@@ -170,7 +175,7 @@ def prefill_cpu_baseline(ps, seconds, seed=9):
     q, k, v = f(ps.q), f(ps.k_new), f(ps.v_new)
     got = f(ps.out)
     spent, flops, rows, max_abs = 0.0, 0, 0, 0.0
-    with threadpool_limits(limits=1):
+    with threadpool_limits(limits=threads):
         while spent < seconds and rows < 4096:
             b, qh = int(rng.integers(0, wl.batch)), int(rng.integers(0, g.num_q_heads))
             h = qh // g.gqa
@@ -188,9 +193,10 @@ def prefill_cpu_baseline(ps, seconds, seed=9):
             flops += 4 * g.head_dim * (n * C + C * (C + 1) // 2)
             rows += 1
             max_abs = max(max_abs, float(np.abs(got[b, :, qh] - ref[b, :, qh]).max()))
-    return {"value": flops / spent / 1e12, "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
+    return {"value": flops / spent / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": f"{rows} (request, query head) rows of the same chunk, all {C} query positions each, "
-                      f"{flops / 1e9:.2f} GFLOP, {spent:.1f} s, BLAS limited to 1 thread",
+                      f"{flops / 1e9:.2f} GFLOP, {spent:.1f} s, BLAS limited to {threads} thread"
+                      f"{'s' if threads > 1 else ''}",
             "gpu_vs_oracle_max_abs": max_abs}
 
 
@@ -277,6 +283,9 @@ def bench_prefill(args):
     if not args.no_cpu_baseline:
         log(f"[bench] cpu_baseline: oracle on sampled rows (~{args.cpu_seconds:.0f} s)")
         res["cpu_baseline"] = prefill_cpu_baseline(s, args.cpu_seconds)
+        cores = host_cores()
+        if cores > 1:
+            res["cpu_baseline_all_cores"] = prefill_cpu_baseline(s, args.cpu_seconds * 2 / 3, seed=11, threads=cores)
     print(json.dumps(res), flush=True)
 
 
@@ -821,8 +830,7 @@ def main():
     if not args.no_cpu_baseline:
         log(f"[bench] cpu_baseline: oracle on a bounded sample (~{args.cpu_seconds:.0f} s)")
         res["cpu_baseline"] = cpu_baseline(s, args.cpu_seconds, threads=1)
-        # the machine's CPU share: OMP_NUM_THREADS when the environment sets it
-        cores = min(len(os.sched_getaffinity(0)), int(os.environ.get("OMP_NUM_THREADS", "0")) or 10**6)
+        cores = host_cores()
         if cores > 1:
             res["cpu_baseline_all_cores"] = cpu_baseline(s, args.cpu_seconds * 2 / 3, threads=cores, seed=8)
     print(json.dumps(res), flush=True)
