@@ -109,9 +109,10 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
 // threads; keys is LDS room for C keys.  Returns count.
 __device__ __forceinline__ int select_unit(const SelectParams& p, int64_t unit, uint32_t* keys, int32_t* kept_lds,
                                            bool write_out = true) {
-  __shared__ uint32_t hist[kWaves][kBins];
+  // per-wave digit histograms, two buffers: a pass reads one while the
+  // waves build the next pass's in the other, each wave clearing its own
+  __shared__ __align__(16) uint32_t hist[2][kWaves][kBins];
   __shared__ int32_t wave_cnt[2][kWaves];
-  __shared__ uint32_t pick[3];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int b = (int)(unit / p.H);
@@ -129,9 +130,7 @@ __device__ __forceinline__ int select_unit(const SelectParams& p, int64_t unit, 
   if (count == 0) return 0;                      // the whole workgroup leaves together
   const bool keep_all = count >= n;
 
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) hist[w][tid] = 0;
-  __syncthreads();
+  if (!keep_all) *reinterpret_cast<u4*>(&hist[0][wave][4 * lane]) = u4(0u);
   // keys into LDS, kBatch loads in flight per thread; the histogram of the
   // top digit is taken on the way
   for (int t0 = tid; t0 < n; t0 += kBatch * kThreads) {
@@ -148,64 +147,69 @@ __device__ __forceinline__ int select_unit(const SelectParams& p, int64_t unit, 
       if (t < n) {
         const uint32_t key = order_key(v[u]);
         keys[t] = key;
-        if (!keep_all) atomicAdd(&hist[wave][key >> 24], 1u);
+        if (!keep_all) atomicAdd(&hist[0][wave][key >> 24], 1u);
       }
     }
   }
-  __syncthreads();
+  __syncthreads();   // keys and the first histogram complete
 
   // radix select over the digits from the top: after each pass, thr holds the
   // digits of the count-th largest key found so far (mask marks them) and
   // need = how many keys with that prefix are kept.  When the whole bucket of
   // the chosen prefix is kept (need == its size), the lower digits cannot
   // change the kept set and the walk stops: the kept keys are then those whose
-  // prefix is larger than thr's, or equal to it.
+  // prefix is larger than thr's, or equal to it.  Every wave finds the digit
+  // itself, so a pass costs one barrier (after its histogram).
   uint32_t thr = 0, mask = 0;
   int need = count;
   if (!keep_all) {
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      if (shift < 24) {
+    int buf = 0;
+    for (int shift = 24;; shift -= 8) {
+      // lane i owns digits 255-4i .. 252-4i, in descending order
+      int c[4] = {0, 0, 0, 0};
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) hist[w][tid] = 0;
-        __syncthreads();
-        for (int t0 = tid; t0 < n; t0 += kBatch * kThreads) {
-          uint32_t kk[kBatch];
-#pragma unroll
-          for (int u = 0; u < kBatch; ++u) {
-            const int t = t0 + u * kThreads;
-            kk[u] = t < n ? keys[t] : ~thr;    // ~thr never matches thr under mask (mask != 0 here)
-          }
-#pragma unroll
-          for (int u = 0; u < kBatch; ++u)
-            if ((kk[u] & mask) == thr) atomicAdd(&hist[wave][(kk[u] >> shift) & 0xffu], 1u);
-        }
-        __syncthreads();
+      for (int w = 0; w < kWaves; ++w) {
+        const u4 h = *reinterpret_cast<const u4*>(&hist[buf][w][252 - 4 * lane]);
+        c[0] += (int)h.w;
+        c[1] += (int)h.z;
+        c[2] += (int)h.y;
+        c[3] += (int)h.x;
       }
-      if (wave == 0) {
-        // lane i owns digits 255-4i .. 252-4i, in descending order
-        int c[4], s = 0;
+      const int s = c[0] + c[1] + c[2] + c[3];
+      int run = wave_inclusive_sum(s) - s;   // matching keys with a larger digit
+      int f_digit = -1, f_need = 0, f_whole = 0;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int d = 255 - 4 * lane - j;
-          c[j] = (int)(hist[0][d] + hist[1][d] + hist[2][d] + hist[3][d]);
-          s += c[j];
+      for (int j = 0; j < 4; ++j) {
+        if (run < need && run + c[j] >= need) {
+          f_digit = 255 - 4 * lane - j;
+          f_need = need - run;
+          f_whole = run + c[j] == need;       // the bucket is kept whole
         }
-        int run = wave_inclusive_sum(s) - s;  // matching keys with a larger digit
+        run += c[j];
+      }
+      // exactly one lane holds the digit: the count-th largest matching key exists
+      const uint64_t holder = __ballot(f_digit >= 0);
+      const int src = holder ? (int)__builtin_ctzll(holder) : 0;
+      const int digit = __builtin_amdgcn_readlane(f_digit, src);
+      need = __builtin_amdgcn_readlane(f_need, src);
+      thr |= (uint32_t)digit << shift;
+      mask |= 0xffu << shift;
+      if (__builtin_amdgcn_readlane(f_whole, src) || shift == 0) break;
+      // the next digit's histogram over the keys that share the prefix
+      buf ^= 1;
+      *reinterpret_cast<u4*>(&hist[buf][wave][4 * lane]) = u4(0u);
+      for (int t0 = tid; t0 < n; t0 += kBatch * kThreads) {
+        uint32_t kk[kBatch];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          if (run < need && run + c[j] >= need) {
-            pick[0] = 255u - 4u * lane - j;
-            pick[1] = (uint32_t)(need - run);
-            pick[2] = (uint32_t)(run + c[j] == need);   // the bucket is kept whole
-          }
-          run += c[j];
+        for (int u = 0; u < kBatch; ++u) {
+          const int t = t0 + u * kThreads;
+          kk[u] = t < n ? keys[t] : ~thr;    // ~thr never matches thr under mask (mask != 0 here)
         }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+          if ((kk[u] & mask) == thr) atomicAdd(&hist[buf][wave][(kk[u] >> (shift - 8)) & 0xffu], 1u);
       }
       __syncthreads();
-      thr |= pick[0] << shift;
-      mask |= 0xffu << shift;
-      need = (int)pick[1];
-      if (pick[2]) break;
     }
   }
 
@@ -330,11 +334,18 @@ __global__ __launch_bounds__(kThreads) void tg_compress_fused_kernel(SelectParam
   extern __shared__ uint32_t lds[];             // [C] keys, then [C] kept chunk indices
   const tg_compress_item it = load_item((const TG_CONST tg_compress_item*)p.items + blockIdx.x);
   int32_t* kept_lds = reinterpret_cast<int32_t*>(lds + p.C);
-  const int count = select_unit(sp, (int64_t)it.b * p.H + it.kv_head, lds, kept_lds, it.rank_begin == 0);
+  const int64_t unit = (int64_t)it.b * p.H + it.kv_head;
+  const int count = select_unit(sp, unit, lds, kept_lds, false);
   __syncthreads();
   const int r0 = max(it.rank_begin, 0);
   const int r1 = min(min(it.rank_end, min(count, min(it.count, p.C))), r0 + TG_COMPRESS_MAX_ROWS);
   copy_rows<kUnroll>(p, it, r0, r1 - r0, [&](int j) { return kept_lds[r0 + j]; });
+  // the unit's first item publishes the kept indices last: stored before the
+  // barrier above, they would make every wave wait for them there
+  if (it.rank_begin == 0) {
+    int32_t* out = sp.kept + unit * p.C;
+    for (int r = threadIdx.x; r < count; r += kThreads) out[r] = kept_lds[r];
+  }
 }
 
 }  // namespace
