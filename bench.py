@@ -647,8 +647,8 @@ def main():
     ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of a HIP graph replay")
     ap.add_argument("--fused-merge", action="store_true",
                     help="merge split units inside the decode launch (merge_counters) instead of a second launch")
-    ap.add_argument("--calibrate-xcd", action="store_true",
-                    help="rebuild the fill plans with per-XCD bin weights measured in one stamped step")
+    ap.add_argument("--no-calibrate", action="store_true",
+                    help="fill plans with equal bins (default: per-layer per-XCD bin weights from one stamped step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--probe-workers", type=int, default=8192,
                     help="waves of the streaming-read ceiling probe (8 per SIMD by default)")
@@ -719,12 +719,15 @@ def main():
             s.run_step(stream)
         stream.synchronize()
         xcd_speed = None
-        if mode == tg.TG_PLAN_AOT_FILL and args.calibrate_xcd:
-            # ahead-of-time calibration (untimed): one stamped step measures each XCD's pages per
-            # microsecond, and the fill plans are rebuilt with bin weights in proportion
-            xcd_speed = s.calibrate_xcd_weights(stream)
-            log(f"[bench] per-XCD relative speed {np.round(xcd_speed, 3).tolist()}; plans rebuilt")
-            s.run_step(stream)
+        if mode == tg.TG_PLAN_AOT_FILL and not args.no_calibrate:
+            # ahead-of-time calibration (untimed, like the plan build): one stamped step measures
+            # each XCD's pages per microsecond on every layer, and the layers' fill plans are
+            # rebuilt with bin weights in proportion
+            xcd_speed = s.calibrate_xcd_weights(stream, per_layer=True)
+            log(f"[bench] per-XCD relative speed (mean over layers) "
+                f"{np.round(xcd_speed.mean(0), 3).tolist()}; plans rebuilt")
+            for _ in range(2):
+                s.run_step(stream)
             stream.synchronize()
         log(f"[bench] warmup {args.warmup} steps done")
         # whole-step timing: the 64 layers' launches captured once in a HIP graph (or eager)
@@ -804,8 +807,8 @@ def main():
                    "split_target": s.split_target, "kv_bytes_per_step": kv_bytes_step,
                    "free_order": args.free_order, "launch": "eager" if args.no_graph else "hip graph",
                    "merge": "in the decode launch" if args.fused_merge else "second launch",
-                   "bin_weights": None if xcd_speed is None else "per-XCD speed from one stamped step "
-                                  + str(np.round(xcd_speed, 3).tolist()),
+                   "bin_weights": None if xcd_speed is None else "per-layer per-XCD speed from one stamped "
+                                  "step (mean over layers " + str(np.round(xcd_speed.mean(0), 3).tolist()) + ")",
                    "parallelism": "single GPU"},
         "us_per_step": round((med if flush else ms_per_step) * 1e3, 1),
         "stream_ceiling": {"value": round(probe_bytes / (t_probe * 1e-3) / 1e9, 1), "unit": "GB/s",

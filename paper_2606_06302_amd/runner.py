@@ -140,23 +140,36 @@ class DecodeSession:
         end[open_] = self.t.kv_len[items["b"][open_], l, items["kv_head"][open_]]
         return end - items["tok_begin"]
 
-    def calibrate_xcd_weights(self, stream=None, classes=8):
+    def calibrate_xcd_weights(self, stream=None, classes=8, per_layer=False):
         """Measures every worker's pages per microsecond over one stamped step and rebuilds the
         sequential-fill plans with bin weights in proportion to the speed of the worker's class.
         Worker k runs in workgroup k // 4; workgroups are dispatched round-robin over the
-        `classes` XCDs, so class = (k // 4) % classes.  Returns the per-class relative speeds."""
+        `classes` XCDs, so class = (k // 4) % classes.  With per_layer, each layer gets the speeds
+        its own stamps show (the pattern differs from layer to layer); else one set pooled over the
+        layers.  Returns the relative speeds: [classes], or [layers][classes] with per_layer."""
         assert self.mode == tg.TG_PLAN_AOT_FILL, "bin weights apply to the sequential-fill plan"
-        pages = np.zeros(classes)
-        busy = np.zeros(classes)
-        for l in self.layers:
+        pages = np.zeros((len(self.layers), classes))
+        busy = np.zeros((len(self.layers), classes))
+        for i, l in enumerate(self.layers):
             t = self.stamp_layer(l, stream)
             per_bin = self.bin_pages(l)
             cls = (np.arange(len(per_bin)) // 4) % classes
-            np.add.at(pages, cls, per_bin)
-            np.add.at(busy, cls, t[:, 1] - t[:, 0])
-        speed = pages / np.maximum(busy, 1)
-        speed = speed / speed.mean()
-        self.set_bin_weights(np.round(1000 * speed[(np.arange(self.n_bins) // 4) % classes]).astype(np.int32))
+            np.add.at(pages[i], cls, per_bin)
+            np.add.at(busy[i], cls, t[:, 1] - t[:, 0])
+
+        def relative(p, b):
+            sp = np.where(b > 0, p / np.maximum(b, 1), np.nan)
+            sp = sp / np.nanmean(sp) if np.isfinite(sp).any() else np.ones_like(sp)
+            return np.nan_to_num(sp, nan=1.0)
+
+        cls = (np.arange(self.n_bins) // 4) % classes
+        if per_layer:
+            speed = np.stack([relative(pages[i], busy[i]) for i in range(len(self.layers))])
+            self.set_bin_weights({l: np.maximum(1, np.round(1000 * speed[i][cls])).astype(np.int32)
+                                  for i, l in enumerate(self.layers)})
+        else:
+            speed = relative(pages.sum(0), busy.sum(0))
+            self.set_bin_weights(np.maximum(1, np.round(1000 * speed[cls])).astype(np.int32))
         return speed
 
     def enable_append(self, k_tok=None, v_tok=None):
@@ -262,12 +275,17 @@ class DecodeSession:
         return pages, slots
 
     def bin_load_stats(self, l):
-        """Planned token load per bin: (max, mean)."""
+        """Planned time per bin, as token load divided by the bin's relative weight (1 without bin
+        weights, so plain tokens): (max, mean)."""
         p = self.plans[l]
         lens = self.item_tokens(l)
         bo = p["bin_offsets"]
-        loads = np.zeros(len(bo) - 1, dtype=np.int64)
+        loads = np.zeros(len(bo) - 1, dtype=np.float64)
         np.add.at(loads, np.repeat(np.arange(len(bo) - 1), np.diff(bo)), lens)
+        w = self.bin_weights.get(l) if isinstance(self.bin_weights, dict) else self.bin_weights
+        if w is not None and self.mode == tg.TG_PLAN_AOT_FILL:
+            w = np.asarray(w, dtype=np.float64)
+            loads = loads / (w / w.mean())
         return float(loads.max()), float(loads.mean())
 
 

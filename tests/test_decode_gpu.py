@@ -260,16 +260,18 @@ def test_graph_replay_matches_eager_bitwise():
         assert torch.equal(s.out, ref_out), rep
 
 
-def test_xcd_calibrated_fill_plan_matches_oracle():
-    """The per-XCD calibration rebuilds the fill plan with bin weights; the new
-    plan still computes the same attention (oracle) as the unweighted one."""
+@pytest.mark.parametrize("per_layer", [False, True])
+def test_xcd_calibrated_fill_plan_matches_oracle(per_layer):
+    """The per-XCD calibration rebuilds the fill plan with bin weights (one set, or
+    one per layer as the benchmark uses); the new plan still computes the same
+    attention (oracle) as the unweighted one."""
     _gpu()
     g = Geometry(2, 8, 64, 128, 16, 2)
     wl = custom(2468, g, 6, "bf16", (300, 5000), kv_scale=0.5)
     s = _small_session(wl, mode=3, n_bins=128)
     ref = s.out.clone()
-    speed = s.calibrate_xcd_weights()
-    assert speed.shape == (8,) and np.all(speed > 0) and s.bin_weights is not None
+    speed = s.calibrate_xcd_weights(per_layer=per_layer)
+    assert speed.shape == ((2, 8) if per_layer else (8,)) and np.all(speed > 0) and s.bin_weights is not None
     s.run_step()
     torch.cuda.synchronize()
     for l in range(2):
