@@ -2,6 +2,7 @@
 from __future__ import annotations
 
 import math
+import os
 import sys
 
 import numpy as np
@@ -120,3 +121,9 @@ def sample_pairs(wl, n, seed):
 
 def math_isclose(a, b):
     return math.isclose(a, b, rel_tol=1e-6)
+
+
+def sweep_cases(default):
+    """Case count of a seeded random sweep: `default`, or TG_SWEEP_CASES for a longer campaign (the first
+    `default` cases are the same either way)."""
+    return int(os.environ.get("TG_SWEEP_CASES", default))

@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import compare_layer, say
+from gpu_helpers import compare_layer, say, sweep_cases
 from workloads import Geometry, config, custom, host_pool, host_scores
 
 pytestmark = pytest.mark.gpu
@@ -173,7 +173,7 @@ def test_compress_random_sweep():
     bit-exact against the oracle."""
     _gpu()
     rng = np.random.default_rng(9090)
-    for case in range(8):
+    for case in range(sweep_cases(8)):
         dtype = ["f32", "bf16"][int(rng.integers(2))]
         d = [64, 128][int(rng.integers(2))]
         H = [1, 2, 4, 8][int(rng.integers(4))]

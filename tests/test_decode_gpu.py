@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_helpers import compare_layer, poisoned_host_pool, sample_pairs, say
+from gpu_helpers import compare_layer, poisoned_host_pool, sample_pairs, say, sweep_cases
 from workloads import Geometry, config, custom
 
 pytestmark = pytest.mark.gpu
@@ -357,7 +357,7 @@ def test_random_shapes_and_plans_sweep():
     lengths poisoned with NaN."""
     _gpu()
     rng = np.random.default_rng(4242)
-    for case in range(16):
+    for case in range(sweep_cases(16)):
         dtype = ["f32", "bf16"][int(rng.integers(2))]
         d = [64, 128][int(rng.integers(2))]
         H = [1, 2, 4, 8][int(rng.integers(4))]

@@ -4,7 +4,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import check_close, poisoned_host_pool, say
+from gpu_helpers import check_close, poisoned_host_pool, say, sweep_cases
 from workloads import Geometry, config, custom
 
 pytestmark = pytest.mark.gpu
@@ -214,7 +214,7 @@ def test_prefill_random_shapes_sweep():
     every (request, query head) row against the oracle, NaN past the retained history."""
     _gpu()
     rng = np.random.default_rng(777)
-    for case in range(10):
+    for case in range(sweep_cases(10)):
         gqa = int(rng.integers(1, 17))
         H = [1, 2, 4, 8][int(rng.integers(4))]
         Hp = [x for x in (1, 2, 4) if H % x == 0][int(rng.integers(len([x for x in (1, 2, 4) if H % x == 0])))]
