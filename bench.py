@@ -432,7 +432,7 @@ def bench_tail(args):
     r, sp0 = row("equal bins")
     rows.append(r)
     sp1, _, _ = stamped()
-    xcd = (np.arange(s.n_bins) // 4) % 8
+    xcd = (np.arange(s.n_bins) // s.workers_per_wg()) % 8
     corr = [np.corrcoef(sp0[l][np.isfinite(sp0[l])], sp1[l][np.isfinite(sp1[l])])[0, 1] for l in s.layers]
     per_xcd = np.array([[np.nanmean(sp0[l][xcd == k]) for k in range(8)] for l in s.layers])
     cv = [np.nanstd(sp0[l]) for l in s.layers]

@@ -140,11 +140,18 @@ class DecodeSession:
         end[open_] = self.t.kv_len[items["b"][open_], l, items["kv_head"][open_]]
         return end - items["tok_begin"]
 
+    def workers_per_wg(self):
+        """Bins (workers) per workgroup of the decode kernel the library picks for this session:
+        four waves, each its own worker, in the bf16 head-dim-128 kernel; one otherwise."""
+        g = self.wl.geom
+        return 4 if (self.tg_dtype == tg.TG_BF16 and g.head_dim == 128) else 1
+
     def calibrate_xcd_weights(self, stream=None, classes=8, per_layer=False):
         """Measures every worker's pages per microsecond over one stamped step and rebuilds the
         sequential-fill plans with bin weights in proportion to the speed of the worker's class.
-        Worker k runs in workgroup k // 4; workgroups are dispatched round-robin over the
-        `classes` XCDs, so class = (k // 4) % classes.  With per_layer, each layer gets the speeds
+        Worker k runs in workgroup k // w (w = workers_per_wg(): 4 for the bf16 head-dim-128 kernel,
+        else 1); workgroups are dispatched round-robin over the `classes` XCDs, so class =
+        (k // w) % classes.  With per_layer, each layer gets the speeds
         its own stamps show (the pattern differs from layer to layer); else one set pooled over the
         layers.  Returns the relative speeds: [classes], or [layers][classes] with per_layer."""
         assert self.mode == tg.TG_PLAN_AOT_FILL, "bin weights apply to the sequential-fill plan"
@@ -153,7 +160,7 @@ class DecodeSession:
         for i, l in enumerate(self.layers):
             t = self.stamp_layer(l, stream)
             per_bin = self.bin_pages(l)
-            cls = (np.arange(len(per_bin)) // 4) % classes
+            cls = (np.arange(len(per_bin)) // self.workers_per_wg()) % classes
             np.add.at(pages[i], cls, per_bin)
             np.add.at(busy[i], cls, t[:, 1] - t[:, 0])
 
@@ -162,7 +169,7 @@ class DecodeSession:
             sp = sp / np.nanmean(sp) if np.isfinite(sp).any() else np.ones_like(sp)
             return np.nan_to_num(sp, nan=1.0)
 
-        cls = (np.arange(self.n_bins) // 4) % classes
+        cls = (np.arange(self.n_bins) // self.workers_per_wg()) % classes
         if per_layer:
             speed = np.stack([relative(pages[i], busy[i]) for i in range(len(self.layers))])
             self.set_bin_weights({l: np.maximum(1, np.round(1000 * speed[i][cls])).astype(np.int32)
