@@ -499,9 +499,12 @@ def bench_memory(args):
 
 def bench_plan_reuse(args):
     """Planning cost against the decode step (the analog of the paper's Table 1) for four model shapes.
-    One decode step = for every layer, the new token's K/V appended (tg_append) and attention over the
-    cache (tg_decode).  The ahead-of-time open-ended plans are built once, before the first step, and
-    serve every step; a planner run at every step would cost plan_build_ms (host) + plan_upload_ms."""
+    One decode step = for every layer, the new token's K/V appended and attention over the cache: step_ms
+    with tg_append, tg_decode and its merge launch (three launches per layer), fused_append_step_ms with the
+    append inside the decode launch (tg_decode's append_k / append_v), one_launch_step_ms with the append
+    and the merge inside it (merge_counters too).  Each form runs the same steps from the same live lengths.
+    The ahead-of-time open-ended plans are built once, before the first step, and serve every step; a
+    planner run at every step would cost plan_build_ms (host) + plan_upload_ms."""
     import torch
     from paper_2606_06302_amd import tangram as tg
     from paper_2606_06302_amd.device import upload_plan
@@ -528,26 +531,43 @@ def bench_plan_reuse(args):
         torch.cuda.synchronize()
         upload_ms = (time.perf_counter() - t0) * 1e3
         stream = torch.cuda.Stream()
-        with torch.cuda.stream(stream):
-            for _ in range(warmup):
-                s.run_decode_step(stream)
-            stream.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            for _ in range(steps):
-                s.run_decode_step(stream)
-            e1.record(stream)
-            torch.cuda.synchronize()
-        step_ms = e0.elapsed_time(e1) / steps
-        assert int(s.full.item()) == 0, "decode headroom exhausted"
+
+        live0 = s.live_len.clone()
+
+        def timed_steps():
+            s.live_len.copy_(live0)   # every form appends the same tokens at the same places
+            with torch.cuda.stream(stream):
+                for _ in range(warmup):
+                    s.run_decode_step(stream)
+                stream.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(steps):
+                    s.run_decode_step(stream)
+                e1.record(stream)
+                torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / steps
+
+        step_ms = timed_steps()
         kv = int(s.live_len.sum().item()) * 2 * g.head_dim * 2
+        s.enable_append(fused=True)
+        fused_ms = timed_steps()
+        counters = torch.zeros(wl.batch * g.num_kv_heads, dtype=torch.int32, device="cuda")
+        for a in s.append_decode_args.values():
+            a.merge_counters = counters.data_ptr()
+        one_ms = timed_steps()
+        assert int(s.full.item()) == 0, "decode headroom exhausted"
         rows.append({"model": name, "layers": g.num_layers, "q_heads": g.num_q_heads, "kv_heads": g.num_kv_heads,
-                     "batch": wl.batch, "step_ms": round(step_ms, 3), "kv_GB_per_step": round(kv / 1e9, 2),
+                     "batch": wl.batch, "step_ms": round(step_ms, 3), "fused_append_step_ms": round(fused_ms, 3),
+                     "one_launch_step_ms": round(one_ms, 3),
+                     "kv_GB_per_step": round(kv / 1e9, 2),
                      "kv_GBps": round(kv / (step_ms * 1e-3) / 1e9, 1),
                      "plan_build_ms": round(plan_ms, 3), "plan_upload_ms": round(upload_ms, 3),
                      "replan_share": round((plan_ms + upload_ms) / (plan_ms + upload_ms + step_ms), 4),
                      "aot_plan_share": 0.0})
-        log(f"[bench]   step {step_ms:.3f} ms ({rows[-1]['kv_GBps']} GB/s), plan {plan_ms:.2f} ms + upload "
+        log(f"[bench]   step {step_ms:.3f} ms ({rows[-1]['kv_GBps']} GB/s), append in decode {fused_ms:.3f} ms, "
+            f"append and merge in decode {one_ms:.3f} ms, "
+            f"plan {plan_ms:.2f} ms + upload "
             f"{upload_ms:.2f} ms")
         del s, t, plans
         torch.cuda.empty_cache()

@@ -237,7 +237,8 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
  * launch on the same stream (only when num_partials > 0).
  * All pointers below are DEVICE pointers:
  *   q        [B][Hq][d] dtype
- *   kv_pool  [pool_pages][2][H_p][P][d] dtype (layout in the file header)
+ *   kv_pool  [pool_pages][2][H_p][P][d] dtype (layout in the file header);
+ *            written only at the rows the append below stores
  *   pt_pages CSR page ids (device copy of tg_reserve's output)
  *   items [num_items], bin_offsets [n_bins+1], unit_splits [B][H],
  *   unit_partial_base [B][H]: device copies of tg_build_plan's output
@@ -257,7 +258,7 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
  *            equal stamps.
  *   live_len [B][L][H] int32 or NULL, with layer: current lengths for items
  *            of a TG_PLAN_OPEN_END plan (an open item with live_len NULL runs
- *            to its table's capacity).
+ *            to its table's capacity).  Written only by the append below.
  *   merge_counters [B][H] int32 or NULL: arrival counters that let the bf16
  *            head_dim-128 kernel merge split units inside its own launch (the
  *            split piece that finishes last merges its unit), so no second
@@ -266,15 +267,31 @@ int32_t tg_build_plan(const tg_geometry* geom, int32_t batch, int32_t layer, con
  *            in time.  NULL, or any other dtype / head_dim: the merge runs as a
  *            second launch on the same stream.  The results are the same
  *            either way, bit for bit.
+ *   append_k, append_v [B][H][d] dtype, or both NULL: this step's new token
+ *            of every (b, h), appended inside the launch (needs live_len and a
+ *            TG_PLAN_OPEN_END plan, whose one open item per unit does it).
+ *            The open item of (b, h) reads n = live_len[b][layer][h] and the
+ *            capacity cap of its table.  If tok_begin <= n < cap, it attends
+ *            over entries [tok_begin, n] with entry n taken from the token
+ *            rows, stores those rows as entry n of the cache (the row tg_append
+ *            writes) and sets live_len[b][layer][h] to n + 1.  Otherwise it
+ *            stores nothing, sets *append_full (when not NULL) to 1 and runs
+ *            as without the append.  While every live length is at least the
+ *            kv_len the plan was built for (the lengths only grow), one call
+ *            gives what tg_append followed by tg_decode gives, bit for bit
+ *            (out, lse, cache rows, live_len), in one launch instead of two.
+ *   append_full: one int32 the caller clears, or NULL.
  * Supported: dtype TG_F32 or TG_BF16, head_dim 64 or 128, page_size 16,
  * gqa 1..16 (else TG_ERR_UNSUPPORTED).  hip_stream is a hipStream_t (NULL =
- * default stream).  Returns TG_ERR_HIP if a launch fails. */
+ * default stream).  Returns TG_ERR_INVALID_ARG when only one of append_k /
+ * append_v is given or the append has no live_len, TG_ERR_HIP if a launch
+ * fails. */
 typedef struct {
   tg_geometry geom;
   int32_t batch;
   int32_t dtype;
   const void* q;
-  const void* kv_pool;
+  void* kv_pool;
   const int32_t* pt_pages;
   const tg_work_item* items;
   const int32_t* bin_offsets;
@@ -289,9 +306,12 @@ typedef struct {
   void* workspace;
   size_t workspace_bytes;
   uint64_t* timestamps;
-  const int32_t* live_len;
+  int32_t* live_len;
   int32_t layer;
   int32_t* merge_counters;
+  const void* append_k;
+  const void* append_v;
+  int32_t* append_full;
 } tg_decode_args;
 
 size_t  tg_decode_workspace_bytes(const tg_geometry* geom, int32_t batch, int32_t num_partials);

@@ -3,19 +3,26 @@
 // One decode step of one layer over Tangram's ragged cache (Section 4.2 of
 // arXiv 2606.06302): every KV head h of request b keeps its own number of
 // retained rows, stored in the pages of its head group.  The host partition
-// (tg_build_plan, Algorithm 1's proportional rule) cuts every (b, h) into
-// page-aligned chunks and places them on n_bins persistent workgroups; the
-// kernel runs bin k on workgroup k.  A chunk of a split unit writes an fp32
-// partial (o, lse) and tg_merge_kernel, launched right after on the same
-// stream, combines the partials of every split unit with a log-sum-exp merge
-// (split-KV decoding, Section 2.2.3).  The merge is a separate launch on
-// purpose: making one workgroup's partials visible to another inside a launch
-// needs agent-scope fences, which on MI355X write back and invalidate the
-// whole L2 of an XCD and cost more than half of the kernel's bandwidth.
+// (tg_build_plan, Algorithm 1's proportional rule or the sequential fill)
+// cuts every (b, h) into page-aligned chunks and places them on n_bins bins;
+// worker k of the launch runs bin k (a wave in the matrix-core kernel, a
+// workgroup in the generic one).  A chunk of a split unit writes an fp32
+// partial (o, lse), and the partials of every split unit are combined with a
+// log-sum-exp merge (split-KV decoding, Section 2.2.3): by tg_merge_kernel,
+// launched right after on the same stream, or, with arrival counters, inside
+// the matrix-core launch by the piece that finishes last.  The in-launch merge
+// orders partials and counters with device-scope stores, loads and atomics
+// only: a fence for ordinary stores would write back and invalidate the whole
+// L2 of an XCD.
 //
-// Both kernels deal the pages of an item round-robin to the 4 waves of the
-// workgroup; every wave keeps its own online-softmax state and the states are
-// merged through LDS at the end of the item.  The wave index is made
+// Open-ended items (the chunk that ends a unit in a plan built for several
+// steps) run to the unit's live length, and can append the step's new token
+// themselves: the row is taken from the token buffer instead of the pool,
+// then stored into the pool, and the live length advanced, at the item's end.
+//
+// The generic kernel deals the pages of an item round-robin to the 4 waves of
+// the workgroup; every wave keeps its own online-softmax state and the states
+// are merged through LDS at the end of the item.  The wave index is made
 // wave-uniform (readfirstlane) so that all item/page bookkeeping is scalar.
 #include <hip/hip_runtime.h>
 
@@ -117,16 +124,35 @@ struct DecodeParams {
   float scale_log2;          // sm_scale * log2(e)
   float scale;               // sm_scale
   int32_t* merge_counters;   // [B*H] arrival counters of the in-launch merge, or NULL
+  // in-launch decode-token append (open items only), or append_k == NULL
+  const u4* append_k;        // [B][H] token rows, 16-byte chunks
+  const u4* append_v;
+  u4* pool_w;                // the pool, written at the appended rows only
+  int32_t* live_w;           // = live, written by the open items
+  int32_t* append_full;      // set when a unit cannot take its token, or NULL
 };
 
-// An open-ended item (tok_end = -capacity) runs to the head's live length,
+// An open-ended item (tok_end = -capacity) runs to the head's live length n,
 // kept within [tok_begin + 1, capacity]; without live lengths, to capacity.
-__device__ __forceinline__ int resolve_end(int tok_begin, int tok_end, int b, int h, const int32_t* live,
-                                           int live_stride) {
-  if (tok_end >= 0) return tok_end;
+// With the in-launch append, an open item with tok_begin <= n < capacity
+// takes the new token as entry n and runs to n + 1 (*arow = n); otherwise
+// *arow = -1, and -2 for an open item that cannot take the token.
+__device__ __forceinline__ int resolve_open(int tok_begin, int tok_end, int n, bool append, int* arow) {
   const int cap = -tok_end;
-  const int n = live ? live[(int64_t)b * live_stride + h] : cap;
+  if (append && n >= tok_begin && n < cap) {
+    *arow = n;
+    return n + 1;
+  }
+  *arow = append ? -2 : -1;
   return min(max(n, tok_begin + 1), cap);
+}
+
+__device__ __forceinline__ int resolve_end(int tok_begin, int tok_end, int b, int h, const DecodeParams& p,
+                                           int* arow) {
+  *arow = -1;
+  if (tok_end >= 0) return tok_end;
+  const int n = p.live ? p.live[(int64_t)b * p.live_stride + h] : -tok_end;
+  return resolve_open(tok_begin, tok_end, n, p.append_k != nullptr, arow);
 }
 
 __device__ __forceinline__ int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
@@ -204,8 +230,10 @@ __global__ void __launch_bounds__(kBlock) tg_decode_kernel(DecodeParams p, const
 
   for (int it = it_begin; it < it_end; ++it) {
     tg_work_item item = items[it];
-    item.tok_end = resolve_end(item.tok_begin, item.tok_end, item.b, item.kv_head, p.live, p.live_stride);
+    int arow;   // entry that takes the appended token, or < 0
+    item.tok_end = resolve_end(item.tok_begin, item.tok_end, item.b, item.kv_head, p, &arow);
     const int qh0 = item.kv_head * GQA;
+    const int64_t toff = ((int64_t)item.b * p.num_kv_heads + item.kv_head) * CPR;   // token row, in chunks
     u4 qv[GQA];
     {
       const u4* qbase = reinterpret_cast<const u4*>(static_cast<const T*>(p.q) +
@@ -237,6 +265,14 @@ __global__ void __launch_bounds__(kBlock) tg_decode_kernel(DecodeParams p, const
           kc[j] = kb[j * 64];
           vc[j] = vb[j * 64];
         }
+      }
+      if (arow >= 0 && pi == npages - 1) {   // the appended entry is the item's last: its row comes from the token
+#pragma unroll
+        for (int j = 0; j < NS; ++j)
+          if (j * TPL + r == (arow & (kPage - 1))) {
+            kc[j] = p.append_k[toff + c];
+            vc[j] = p.append_v[toff + c];
+          }
       }
       const int nvalid = min(kPage, ntok - pi * kPage);
       float s[NS][GQA];
@@ -307,6 +343,18 @@ __global__ void __launch_bounds__(kBlock) tg_decode_kernel(DecodeParams p, const
     }
     __syncthreads();
     finish_item<T, GQA, D>(p, item, sm_m, sm_l, &sm_acc[0][0][0], GQA * D);
+    if (arow >= 0) {   // the token becomes entry arow of the cache; every thread read the length above
+      if (threadIdx.x < 2 * CPR) {
+        const bool is_k = threadIdx.x < CPR;
+        const int ch = threadIdx.x % CPR;
+        const int64_t pg = (int64_t)pt_pages[item.pt_base + arow / kPage] * p.page_chunks;
+        p.pool_w[pg + (is_k ? slab_k : slab_v) + (arow % kPage) * CPR + ch] =
+            is_k ? p.append_k[toff + ch] : p.append_v[toff + ch];
+      }
+      if (threadIdx.x == 0) p.live_w[(int64_t)item.b * p.live_stride + item.kv_head] = arow + 1;
+    } else if (arow == -2 && threadIdx.x == 0 && p.append_full) {
+      *p.append_full = 1;
+    }
     __syncthreads();
   }
   if (p.timestamps && threadIdx.x == 0) {   // one lane, vector stores
@@ -387,7 +435,9 @@ __device__ __forceinline__ void wait_vmcnt() {
 __device__ __forceinline__ void wait_lgkmcnt0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 // field-wise copy: the implicit copy constructor cannot bind a constant-space object
-__device__ __forceinline__ tg_work_item load_item(const TG_CONST tg_work_item* src, const DecodeParams& p) {
+// (live lengths too: the open item that appends writes its length only after
+// its last scalar read of it)
+__device__ __forceinline__ tg_work_item load_item(const TG_CONST tg_work_item* src, const DecodeParams& p, int* arow) {
   tg_work_item r;
   r.pt_base = src->pt_base;
   r.b = src->b;
@@ -396,11 +446,11 @@ __device__ __forceinline__ tg_work_item load_item(const TG_CONST tg_work_item* s
   r.tok_begin = src->tok_begin;
   r.tok_end = src->tok_end;
   r.out_idx = src->out_idx;
+  *arow = -1;
   if (r.tok_end < 0) {
     const TG_CONST int32_t* live = (const TG_CONST int32_t*)p.live;
-    const int cap = -r.tok_end;
-    const int n = live ? live[(int64_t)r.b * p.live_stride + r.kv_head] : cap;
-    r.tok_end = min(max(n, r.tok_begin + 1), cap);
+    const int n = live ? live[(int64_t)r.b * p.live_stride + r.kv_head] : -r.tok_end;
+    r.tok_end = resolve_open(r.tok_begin, r.tok_end, n, p.append_k != nullptr, arow);
   }
   return r;
 }
@@ -472,15 +522,17 @@ __global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, 
   // DMA cursor over every page of every item of the bin; it caches the
   // item's page count, table base, slot and query offset.
   struct Cursor {
-    int it, pi, np, slot;
+    int it, pi, np, slot, arow;
     int64_t pbase, qoff;
   };
   auto enter = [&](Cursor& cu, int it) {
-    const tg_work_item im = load_item(items + it, p);
+    int arow;
+    const tg_work_item im = load_item(items + it, p, &arow);
     cu.it = it;
     cu.pi = 0;
     cu.np = (im.tok_end - im.tok_begin + kPage - 1) / kPage;
     cu.slot = im.slot;
+    cu.arow = arow >= 0 ? arow & (kPage - 1) : -1;   // row of the last page that takes the new token
     cu.pbase = im.pt_base + im.tok_begin / kPage;
     cu.qoff = ((int64_t)im.b * p.num_q_heads + (int64_t)im.kv_head * G) * (D / 8);
   };
@@ -508,6 +560,25 @@ __global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, 
     const u4* kb = base + cu.slot * 256;
     const u4* vb = base + (p.heads_per_group + cu.slot) * 256;
     const uint32_t dst = ring_lds + ring * 8192;
+    if (cu.arow >= 0 && cu.pi == cu.np - 1) {   // the page that takes the new token: that row from the token
+      const int64_t toff = ((int64_t)items[cu.it].b * p.num_kv_heads + items[cu.it].kv_head) * (D / 8);
+      const u4* tk = p.append_k + toff;
+      const u4* tv = p.append_v + toff;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = j * 4 + (lane >> 4);
+        const int pos = lane & 15;
+        lds_dma16(r == cu.arow ? tk + (pos ^ r) : kb + r * 16 + (pos ^ r), dst + j * 1024);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = j * 4 + (lane >> 4);
+        const int pos = lane & 15;
+        const int c = pos ^ ((2 * r) & 15);
+        lds_dma16(r == cu.arow ? tv + c : vb + r * 16 + c, dst + 4096 + j * 1024);
+      }
+      return;
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int r = j * 4 + (lane >> 4);   // token row written by this lane
@@ -541,14 +612,14 @@ __global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, 
   const int v_off = 4096 + v_tok * 256 + (lane & 3) * 8;       // bytes within the page buffer
   const int v_swz = v_tok & 7;
 
-  int it = it_begin, pi = 0, np = 0, ntok = 0, k = 0;
+  int it = it_begin, pi = 0, np = 0, ntok = 0, k = 0, arow = -1;
   tg_work_item item;
   u4 qv[4];
   float m = -INFINITY, l = 0.f;
   f32x4 acc[8];
   for (;;) {
     if (pi == 0) {   // item start: its queries were DMA'd just before its first page
-      item = load_item(items + it, p);
+      item = load_item(items + it, p, &arow);
       ntok = item.tok_end - item.tok_begin;
       np = (ntok + kPage - 1) / kPage;
       if (d_live)
@@ -617,6 +688,24 @@ __global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, 
     }
     ++k;
     if (++pi < np) continue;
+
+    if (arow >= 0) {
+      // the new token becomes entry arow of the cache: its rows are in this
+      // page's LDS buffer (refilled only by the next issue), 16 lanes for K
+      // and 16 for V, stored with ordinary vector stores, which the DMA waits
+      // above only count as extra (later) operations
+      const int r = arow & (kPage - 1);
+      const int64_t pg = (int64_t)pt[item.pt_base + arow / kPage] * p.page_chunks;
+      if (lane < 32) {
+        const int ch = lane & 15;
+        const bool is_k = lane < 16;
+        const u4 row = is_k ? kbuf[r * 16 + (ch ^ r)] : kbuf[256 + r * 16 + (ch ^ ((2 * r) & 15))];
+        p.pool_w[pg + (is_k ? item.slot : p.heads_per_group + item.slot) * 256 + r * 16 + ch] = row;
+      }
+      if (lane == 0) p.live_w[(int64_t)item.b * p.live_stride + item.kv_head] = arow + 1;
+    } else if (arow == -2 && lane == 0 && p.append_full) {
+      *p.append_full = 1;
+    }
 
     // item end: the head's sum over all 16 token rows, then normalise and store
     l = swap32_sum(swap16_sum(l));
@@ -909,6 +998,14 @@ int32_t decode_impl(const tg_decode_args* a, void* ws_ptr, size_t ws_bytes, void
     return tg::fail(TG_ERR_INVALID_ARG, "layer %d out of range", a->layer);
   p.live = a->live_len ? a->live_len + (int64_t)a->layer * g.num_kv_heads : nullptr;
   p.live_stride = g.num_layers * g.num_kv_heads;
+  if ((a->append_k == nullptr) != (a->append_v == nullptr))
+    return tg::fail(TG_ERR_INVALID_ARG, "append_k and append_v go together");
+  if (a->append_k && !a->live_len) return tg::fail(TG_ERR_INVALID_ARG, "the in-launch append needs live_len");
+  p.append_k = static_cast<const u4*>(a->append_k);
+  p.append_v = static_cast<const u4*>(a->append_v);
+  p.pool_w = static_cast<u4*>(a->kv_pool);
+  p.live_w = a->append_k ? a->live_len + (int64_t)a->layer * g.num_kv_heads : nullptr;
+  p.append_full = a->append_full;
   // the bf16 head_dim-128 kernel merges split units inside its launch when the
   // caller passes arrival counters; every other case merges in a second launch
   const bool fused_merge = a->merge_counters && a->num_partials > 0 && a->dtype == TG_BF16 && g.head_dim == 128;

@@ -179,9 +179,11 @@ class DecodeSession:
             self.set_bin_weights(np.maximum(1, np.round(1000 * speed[cls])).astype(np.int32))
         return speed
 
-    def enable_append(self, k_tok=None, v_tok=None):
+    def enable_append(self, k_tok=None, v_tok=None, fused=False):
         """Device buffers for one decode step's new token per layer ([L][B][H][d] K and V) and the
-        tg_append arguments of every layer; run_decode_step then appends before attending."""
+        tg_append arguments of every layer; run_decode_step then appends before attending, with
+        tg_append (two launches per layer) or, when fused, inside the decode launch (tg_decode's
+        append_k / append_v: one launch per layer, the same results bit for bit)."""
         assert self.open_end, "appending needs open-ended plans and live lengths"
         g, B, dev = self.wl.geom, self.wl.batch, self.device
         shape = (g.num_layers, B, g.num_kv_heads, g.head_dim)
@@ -194,6 +196,19 @@ class DecodeSession:
         self.append_args = {l: tg.make_append_args(g, B, l, self.tg_dtype, self.k_tok[l], self.v_tok[l], self.pool,
                                                    self.t.d_pt_pages, self.d_offsets, self.d_group_of,
                                                    self.d_slot_of, self.live_len, self.full) for l in self.layers}
+        self.fused_append = fused
+        self._bind_append()
+
+    def _bind_append(self):
+        # decode args that also append (kept apart from the plain ones, which run_step uses)
+        self.append_decode_args = {}
+        if not getattr(self, "fused_append", False):
+            return
+        for l in self.layers:
+            a = tg.tg_decode_args.from_buffer_copy(self.dplans[l].args)
+            a.append_k, a.append_v = self.k_tok[l].data_ptr(), self.v_tok[l].data_ptr()
+            a.append_full = self.full.data_ptr()
+            self.append_decode_args[l] = a
 
     def append_layer(self, l, stream=None):
         tg.tg_append(self.append_args[l], stream)
@@ -201,8 +216,11 @@ class DecodeSession:
     def run_decode_step(self, stream=None):
         """One decode step: per layer, the new token's K/V appended, then attention over the cache."""
         for l in self.layers:
-            tg.tg_append(self.append_args[l], stream)
-            tg.tg_decode(self.dplans[l].args, stream)
+            if self.fused_append:
+                tg.tg_decode(self.append_decode_args[l], stream)
+            else:
+                tg.tg_append(self.append_args[l], stream)
+                tg.tg_decode(self.dplans[l].args, stream)
 
     def run_layer(self, l, stream=None):
         tg.tg_decode(self.dplans[l].args, stream)
@@ -247,6 +265,7 @@ class DecodeSession:
         self.bin_weights = weights
         self._build_plans()
         self._bind()
+        self._bind_append()
 
     def worker_timeline(self, stream=None):
         """Runs one step with per-worker start/end stamps (s_memrealtime ticks) and returns, per layer,

@@ -54,7 +54,8 @@ class tg_decode_args(C.Structure):
                 ("num_partials", C.c_int32), ("out", C.c_void_p), ("lse", C.c_void_p),
                 ("sm_scale", C.c_float), ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t),
                 ("timestamps", C.c_void_p), ("live_len", C.c_void_p), ("layer", C.c_int32),
-                ("merge_counters", C.c_void_p)]
+                ("merge_counters", C.c_void_p), ("append_k", C.c_void_p), ("append_v", C.c_void_p),
+                ("append_full", C.c_void_p)]
 
 
 class tg_prefill_args(C.Structure):
@@ -270,16 +271,19 @@ def _stream(stream):
 def make_decode_args(geom, batch, dtype, q, kv_pool, pt_pages, items, bin_offsets, n_bins, num_items,
                      unit_splits, unit_partial_base, num_partials, out, lse=None, sm_scale=0.0,
                      workspace=None, timestamps=None, live_len=None, layer=0,
-                     merge_counters=None) -> tg_decode_args:
+                     merge_counters=None, append_k=None, append_v=None, append_full=None) -> tg_decode_args:
     """Packs a tg_decode_args from device tensors (kept alive by the caller); timestamps is an
     int64 device tensor of 2*n_bins entries, or None; live_len an int32 [B][L][H] device tensor of
     current lengths for open-ended plans, or None; merge_counters an int32 [B*H] device tensor of
-    zeros for the in-launch merge, or None for the two-launch merge."""
+    zeros for the in-launch merge, or None for the two-launch merge; append_k / append_v the
+    step's new token rows [B][H][d] for the in-launch append (with live_len), append_full an
+    int32 flag the caller clears."""
     return tg_decode_args(_geom(geom), int(batch), int(dtype), _dptr(q), _dptr(kv_pool), _dptr(pt_pages),
                           _dptr(items), _dptr(bin_offsets), int(n_bins), int(num_items), _dptr(unit_splits),
                           _dptr(unit_partial_base), int(num_partials), _dptr(out), _dptr(lse), float(sm_scale),
                           _dptr(workspace), 0 if workspace is None else workspace.numel() * workspace.element_size(),
-                          _dptr(timestamps), _dptr(live_len), int(layer), _dptr(merge_counters))
+                          _dptr(timestamps), _dptr(live_len), int(layer), _dptr(merge_counters),
+                          _dptr(append_k), _dptr(append_v), _dptr(append_full))
 
 
 def tg_decode(args: tg_decode_args, stream=None):

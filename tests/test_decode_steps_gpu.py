@@ -1,5 +1,6 @@
 """Decode steps through the C ABI: tg_append writes each step's token after every head's entries, and one
-open-ended plan built before the first step serves every later step (tg_decode with live lengths)."""
+open-ended plan built before the first step serves every later step (tg_decode with live lengths).  The same
+steps with the append inside the decode launch (tg_decode's append_k / append_v) give the same bits."""
 import numpy as np
 import pytest
 import torch
@@ -24,13 +25,13 @@ def _f64(t):
     return t.float().cpu().numpy().astype(np.float64)
 
 
-def _session(geom, B, dtype, ctx, T, mode, seed, n_bins=64):
+def _session(geom, B, dtype, ctx, T, mode, seed, n_bins=64, fused=False):
     wl = custom(seed, geom, B, dtype, ctx)
     tables = Tables(wl, headroom=np.full(B, T, dtype=np.int32))
     pool = torch.from_numpy(host_pool(wl, tables.pool_pages)).to(TORCH_DTYPE[dtype]).cuda()
     s = DecodeSession(wl, tables=tables, mode=mode, n_bins=n_bins, split_target=2 * n_bins, fill="host", pool=pool,
                       open_end=True)
-    s.enable_append()
+    s.enable_append(fused=fused)
     return wl, tables, s
 
 
@@ -46,17 +47,18 @@ def _step_inputs(rng, s, dtype):
     return _f64(k), _f64(v)
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["append-launch", "append-in-decode"])
 @pytest.mark.parametrize("geom,dtype,mode", [
     (Geometry(2, 8, 32, 128, 16, 2), "bf16", "fill"),
     (Geometry(2, 8, 40, 128, 16, 2), "bf16", "aot"),
     (Geometry(1, 4, 8, 64, 16, 2), "f32", "fill"),
 ])
-def test_steps_with_one_plan_match_oracle(geom, dtype, mode):
+def test_steps_with_one_plan_match_oracle(geom, dtype, mode, fused):
     _gpu()
     T, B = 37, 4
     m = tg.TG_PLAN_AOT_FILL if mode == "fill" else tg.TG_PLAN_AOT
-    wl, t, s = _session(geom, B, dtype, (20, 900), T, m, 4242 + geom.num_q_heads)
-    say(f"decode steps {geom} {dtype} {mode}: ctx {wl.ctx_len.tolist()}, {T} steps")
+    wl, t, s = _session(geom, B, dtype, (20, 900), T, m, 4242 + geom.num_q_heads, fused=fused)
+    say(f"decode steps {geom} {dtype} {mode} fused={fused}: ctx {wl.ctx_len.tolist()}, {T} steps")
     rng = np.random.default_rng(99)
     ref_pool = _f64(s.pool)
     live = t.kv_len.copy()
@@ -130,3 +132,91 @@ def test_reused_plan_equals_fresh_plan():
                                    pages=t.pt_pages, group_of=t.group_of, slot_of=t.slot_of)
     check_close(reused.reshape(-1, 128), O.reshape(-1, 128), "bf16", "reused plan")
     check_close(_f64(out2).reshape(-1, 128), O.reshape(-1, 128), "bf16", "fresh plan")
+
+
+def _twin_sessions(geom, B, dtype, ctx, mode, seed, headroom, n_bins, merge):
+    """Two sessions on the same tables and equal pools: one appends with tg_append, one inside tg_decode."""
+    wl = custom(seed, geom, B, dtype, ctx)
+    t = Tables(wl, headroom=None if headroom is None else np.full(B, headroom, dtype=np.int32))
+    host = torch.from_numpy(host_pool(wl, t.pool_pages)).to(TORCH_DTYPE[dtype])
+    pair = []
+    for fused in (False, True):
+        s = DecodeSession(wl, tables=t, mode=mode, n_bins=n_bins, split_target=2 * n_bins, fill="host",
+                          pool=host.clone().cuda(), open_end=True, fused_merge=merge)
+        s.enable_append(fused=fused)
+        pair.append(s)
+    return wl, t, pair
+
+
+def _same_bits(a, b):
+    return torch.equal(a.view(torch.int16) if a.dtype == torch.bfloat16 else a.view(torch.int32),
+                       b.view(torch.int16) if b.dtype == torch.bfloat16 else b.view(torch.int32))
+
+
+@pytest.mark.parametrize("geom,dtype,mode,merge", [
+    (Geometry(2, 8, 32, 128, 16, 2), "bf16", "fill", False),   # matrix-core kernel, 4 query heads per KV head
+    (Geometry(2, 8, 32, 128, 16, 2), "bf16", "fill", True),    # ... merging split units in the same launch
+    (Geometry(1, 4, 64, 128, 16, 2), "bf16", "aot", False),    # 16 query heads per KV head (3-page ring)
+    (Geometry(1, 8, 40, 128, 16, 4), "bf16", "aot", True),     # 5 query heads per KV head
+    (Geometry(1, 4, 8, 64, 16, 2), "f32", "fill", False),      # generic kernel, fp32, d 64
+    (Geometry(1, 4, 16, 64, 16, 1), "bf16", "aot", False),     # generic kernel, bf16, d 64
+    (Geometry(1, 2, 4, 128, 16, 2), "f32", "fill", False),     # generic kernel, fp32, d 128
+])
+def test_append_in_decode_is_bitwise_append_then_decode(geom, dtype, mode, merge):
+    """Every step: out, lse, the whole pool and the live lengths equal bit for bit between tg_append +
+    tg_decode and tg_decode with the append (contexts from 1 token, steps across page boundaries)."""
+    _gpu()
+    B, T = 6, 23
+    m = tg.TG_PLAN_AOT_FILL if mode == "fill" else tg.TG_PLAN_AOT
+    wl, t, (sep, fus) = _twin_sessions(geom, B, dtype, (1, 700), m, 808 + geom.num_q_heads, T, 48, merge)
+    say(f"append in decode {geom} {dtype} {mode} merge={merge}: ctx {wl.ctx_len.tolist()}, {T} steps")
+    rng = np.random.default_rng(31)
+    for step in range(1, T + 1):
+        _step_inputs(rng, sep, dtype)
+        for name in ("k_tok", "v_tok", "q"):
+            getattr(fus, name).copy_(getattr(sep, name))
+        sep.run_decode_step()
+        fus.run_decode_step()
+        torch.cuda.synchronize()
+        assert _same_bits(sep.out, fus.out), f"out differs at step {step}"
+        assert _same_bits(sep.lse, fus.lse), f"lse differs at step {step}"
+        assert _same_bits(sep.pool, fus.pool), f"pool differs at step {step}"
+        assert torch.equal(sep.live_len, fus.live_len), f"live lengths differ at step {step}"
+    assert np.array_equal(fus.live_len.cpu().numpy(), t.kv_len + T)
+    assert int(sep.full.item()) == 0 and int(fus.full.item()) == 0
+
+
+def test_append_in_decode_without_room_matches_append_launch():
+    """Heads whose table is full take no token in either form: the flag is set, nothing is stored, and the
+    attention runs over the full table; the other heads append (matrix-core and generic kernels)."""
+    _gpu()
+    for geom, dtype in ((Geometry(1, 4, 16, 128, 16, 2), "bf16"), (Geometry(1, 4, 8, 64, 16, 2), "f32")):
+        B = 2
+        wl = custom(77, geom, B, dtype, [512, 512], budget=np.array([[1.0, 0.5, 0.25, 0.125]]), jitter=0.0)
+        t = Tables(wl)
+        host = torch.from_numpy(host_pool(wl, t.pool_pages)).to(TORCH_DTYPE[dtype])
+        pair = []
+        for fused in (False, True):
+            s = DecodeSession(wl, tables=t, mode=tg.TG_PLAN_AOT_FILL, n_bins=16, fill="host",
+                              pool=host.clone().cuda(), open_end=True)
+            s.enable_append(fused=fused)
+            pair.append(s)
+        sep, fus = pair
+        rng = np.random.default_rng(6)
+        for step in range(3):
+            ks, vs = _step_inputs(rng, sep, dtype)
+            for name in ("k_tok", "v_tok", "q"):
+                getattr(fus, name).copy_(getattr(sep, name))
+            before = _f64(sep.pool)
+            live0 = sep.live_len.cpu().numpy()
+            sep.run_decode_step()
+            fus.run_decode_step()
+            torch.cuda.synchronize()
+            ref, live, full = oracle.append_token(ks[0], vs[0], before, 0, geom=geom, live_len=live0,
+                                                  offsets=t.pt_offsets, pages=t.pt_pages, group_of=t.group_of,
+                                                  slot_of=t.slot_of)
+            assert sorted(full) == [(0, 0), (0, 2), (1, 0), (1, 2)]
+            assert np.array_equal(fus.live_len.cpu().numpy(), live)
+            assert np.array_equal(_f64(fus.pool), ref)
+            assert _same_bits(sep.out, fus.out) and _same_bits(sep.lse, fus.lse), f"{geom} step {step}"
+        assert int(sep.full.item()) == 1 and int(fus.full.item()) == 1

@@ -502,6 +502,27 @@ def test_append_launch_validation_on_host():
         assert e.value.code == tg.TG_ERR_INVALID_ARG, kw
 
 
+def test_decode_append_arguments_checked_on_host():
+    """tg_decode's in-launch append needs both token arrays and the live lengths; the call is refused on
+    the host, before any launch (the device pointers below are never dereferenced)."""
+    g = Geometry(1, 2, 4, 128, 16, 2)
+    fake = 1 << 20
+
+    def args(**kw):
+        a = tg.make_decode_args(g, 1, tg.TG_BF16, None, None, None, None, None, 4, 1, None, None, 0, None)
+        for f in ("q", "kv_pool", "pt_pages", "items", "bin_offsets", "out"):
+            setattr(a, f, fake)
+        for k, v in kw.items():
+            setattr(a, k, v)
+        return a
+
+    for kw in (dict(append_k=fake), dict(append_v=fake), dict(append_k=fake, append_v=fake),
+               dict(append_k=fake, live_len=fake)):
+        with pytest.raises(tg.TangramError) as e:
+            tg.tg_decode(args(**kw))
+        assert e.value.code == tg.TG_ERR_INVALID_ARG, kw
+
+
 def test_read_probe_slab_sizes_checked_on_host():
     """tg_read_probe runs only the 2, 4 and 8 KiB slab kernels: every other slab size is refused before
     anything is enqueued, and an accepted size goes on to the remaining argument checks (here a zero
