@@ -792,27 +792,43 @@ __global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, 
           f32x4 A[8];
 #pragma unroll
           for (int mm = 0; mm < 8; ++mm) A[mm] = f32x4{0.f, 0.f, 0.f, 0.f};
-          for (int i = 0; i < s; ++i) {
-            const int64_t pidx = (int64_t)base + i;
-            const float li = __hip_atomic_load(p.part_lse + pidx * G + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            const uint64_t* prow = reinterpret_cast<const uint64_t*>(p.part_o + (pidx * G + col) * D + 4 * rb);
-            f32x4 oi[8];
+          // up to kSplitBatch partials are requested before the first is
+          // used: one round trip for a unit of that many splits (indices past
+          // the last re-read it, and selects discard their steps)
+          constexpr int kSplitBatch = 4;
+          for (int i0 = 0; i0 < s; i0 += kSplitBatch) {
+            float lv[kSplitBatch];
+            f32x4 ov[kSplitBatch][8];
 #pragma unroll
-            for (int mm = 0; mm < 8; ++mm) {
-              const uint64_t lo = __hip_atomic_load(prow + mm * 8, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-              const uint64_t hi = __hip_atomic_load(prow + mm * 8 + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-              oi[mm] = f32x4{__uint_as_float((uint32_t)lo), __uint_as_float((uint32_t)(lo >> 32)),
-                             __uint_as_float((uint32_t)hi), __uint_as_float((uint32_t)(hi >> 32))};
+            for (int jj = 0; jj < kSplitBatch; ++jj) {
+              const int64_t pidx = (int64_t)base + min(i0 + jj, s - 1);
+              lv[jj] = __hip_atomic_load(p.part_lse + pidx * G + col, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+              const uint64_t* prow = reinterpret_cast<const uint64_t*>(p.part_o + (pidx * G + col) * D + 4 * rb);
+#pragma unroll
+              for (int mm = 0; mm < 8; ++mm) {
+                const uint64_t lo = __hip_atomic_load(prow + mm * 8, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                const uint64_t hi = __hip_atomic_load(prow + mm * 8 + 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                ov[jj][mm] = f32x4{__uint_as_float((uint32_t)lo), __uint_as_float((uint32_t)(lo >> 32)),
+                                   __uint_as_float((uint32_t)hi), __uint_as_float((uint32_t)(hi >> 32))};
+              }
             }
             // the same running-max recurrence, in the same order, as tg_merge_kernel
-            const float mn = fmaxf(mr, li);
-            const float a = __expf(mr - mn), w = __expf(li - mn);
-            L = fmaf(L, a, w);
 #pragma unroll
-            for (int mm = 0; mm < 8; ++mm)
+            for (int jj = 0; jj < kSplitBatch; ++jj) {
+              const bool use = i0 + jj < s;
+              const float mn = fmaxf(mr, lv[jj]);
+              const float a = __expf(mr - mn), w = __expf(lv[jj] - mn);
+              const float Ln = fmaf(L, a, w);
 #pragma unroll
-              for (int q = 0; q < 4; ++q) A[mm][q] = fmaf(A[mm][q], a, w * oi[mm][q]);
-            mr = mn;
+              for (int mm = 0; mm < 8; ++mm)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                  const float An = fmaf(A[mm][q], a, w * ov[jj][mm][q]);
+                  A[mm][q] = use ? An : A[mm][q];
+                }
+              L = use ? Ln : L;
+              mr = use ? mn : mr;
+            }
           }
           const int qh = h * G + col;
           uint2* orow =
@@ -848,24 +864,41 @@ __global__ void __launch_bounds__(kBlock) tg_merge_kernel(const int32_t* __restr
                                                          int32_t num_kv_heads, int32_t gqa) {
   const int u = blockIdx.x;
   const int s = unit_splits[u];
+  const int base = unit_base[u];
+  // both reads in flight together, before the exit test (the compiler would
+  // otherwise sink the second behind it: two round trips instead of one)
+  asm volatile("" ::"s"(s), "s"(base));
   const int o = blockIdx.y * kBlock + threadIdx.x;
   if (s <= 1 || o >= gqa * D) return;
-  const int base = unit_base[u];
   const int b = u / num_kv_heads, h = u % num_kv_heads;
   const int64_t row0 = (int64_t)b * num_kv_heads * gqa + (int64_t)h * gqa;
   const int g = o / D, e = o % D;
   const float* pl = part_lse + (int64_t)base * gqa + g;
   const float* po = part_o + ((int64_t)base * gqa + g) * D + e;
   float m = -INFINITY, L = 0.f, A = 0.f;
-#pragma unroll 8
-  for (int i = 0; i < s; ++i) {
-    const float li = pl[(int64_t)i * gqa];
-    const float oi = po[(int64_t)i * gqa * D];
-    const float mn = fmaxf(m, li);
-    const float a = __expf(m - mn), w = __expf(li - mn);
-    L = fmaf(L, a, w);
-    A = fmaf(A, a, w * oi);
-    m = mn;
+  // kBatch splits' loads go out before the first is used, so a unit of up to
+  // kBatch splits pays one memory round trip, not one per split.  Indices past
+  // the last split re-read it; their steps are computed and then discarded by
+  // selects (a branch would let the compiler sink the loads behind it).
+  constexpr int kBatch = 4;
+  for (int i0 = 0; i0 < s; i0 += kBatch) {
+    float lv[kBatch], ov[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int64_t i = min(i0 + j, s - 1);
+      lv[j] = pl[i * gqa];
+      ov[j] = po[i * gqa * D];
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const bool use = i0 + j < s;
+      const float mn = fmaxf(m, lv[j]);
+      const float a = __expf(m - mn), w = __expf(lv[j] - mn);
+      const float Ln = fmaf(L, a, w), An = fmaf(A, a, w * ov[j]);
+      L = use ? Ln : L;
+      A = use ? An : A;
+      m = use ? mn : m;
+    }
   }
   store_out<T>(static_cast<T*>(out) + (row0 + g) * D + e, A / L);
   if (lse && e == 0) lse[row0 + g] = m + logf(L);
