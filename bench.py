@@ -664,7 +664,10 @@ def main():
     ap.add_argument("--n-bins", type=int, default=0)
     ap.add_argument("--split-target", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--no-graph", action="store_true", help="time eager launches instead of a HIP graph replay")
+    ap.add_argument("--launch", default="auto", choices=["auto", "graph", "eager"],
+                    help="how the timed steps are launched: a HIP graph replay or eager calls; auto = the graph for "
+                         "multi-layer steps, eager calls for single-layer ones (each of those follows a MALL flush, "
+                         "during which the host enqueues the step, and a graph replay adds dispatch latency)")
     ap.add_argument("--fused-merge", action="store_true",
                     help="merge split units inside the decode launch (merge_counters) instead of a second launch")
     ap.add_argument("--no-calibrate", action="store_true",
@@ -750,8 +753,9 @@ def main():
                 s.run_step(stream)
             stream.synchronize()
         log(f"[bench] warmup {args.warmup} steps done")
-        # whole-step timing: the 64 layers' launches captured once in a HIP graph (or eager)
-        graph = None if args.no_graph else s.capture_step(stream)
+        # whole-step timing: the layers' launches captured once in a HIP graph, or eager calls
+        use_graph = args.launch == "graph" or (args.launch == "auto" and g.num_layers > 1)
+        graph = s.capture_step(stream) if use_graph else None
         if graph is not None:
             graph.replay()
             stream.synchronize()
@@ -825,7 +829,7 @@ def main():
                    "kv_heads": g.num_kv_heads, "head_dim": g.head_dim, "page_size": g.page_size,
                    "heads_per_group": g.heads_per_group, "plan": args.mode, "n_bins": s.n_bins,
                    "split_target": s.split_target, "kv_bytes_per_step": kv_bytes_step,
-                   "free_order": args.free_order, "launch": "eager" if args.no_graph else "hip graph",
+                   "free_order": args.free_order, "launch": "hip graph" if use_graph else "eager",
                    "merge": "in the decode launch" if args.fused_merge else "second launch",
                    "bin_weights": None if xcd_speed is None else "per-layer per-XCD speed from one stamped "
                                   "step (mean over layers " + str(np.round(xcd_speed.mean(0), 3).tolist()) + ")",
