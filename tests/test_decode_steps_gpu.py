@@ -161,6 +161,7 @@ def _same_bits(a, b):
     (Geometry(1, 4, 8, 64, 16, 2), "f32", "fill", False),      # generic kernel, fp32, d 64
     (Geometry(1, 4, 16, 64, 16, 1), "bf16", "aot", False),     # generic kernel, bf16, d 64
     (Geometry(1, 2, 4, 128, 16, 2), "f32", "fill", False),     # generic kernel, fp32, d 128
+    (Geometry(1, 4, 4, 128, 16, 2), "bf16", "fill", False),    # matrix-core kernel, one query head per KV head
 ])
 def test_append_in_decode_is_bitwise_append_then_decode(geom, dtype, mode, merge):
     """Every step: out, lse, the whole pool and the live lengths equal bit for bit between tg_append +
@@ -220,3 +221,78 @@ def test_append_in_decode_without_room_matches_append_launch():
             assert np.array_equal(_f64(fus.pool), ref)
             assert _same_bits(sep.out, fus.out) and _same_bits(sep.lse, fus.lse), f"{geom} step {step}"
         assert int(sep.full.item()) == 1 and int(fus.full.item()) == 1
+
+
+def test_append_in_noalloc_decode_is_bitwise_append_then_decode():
+    """tg_decode_noalloc takes the same append arguments: bitwise equal to tg_append + tg_decode at every step."""
+    _gpu()
+    g = Geometry(2, 8, 32, 128, 16, 2)
+    B, T = 4, 9
+    wl, t, (sep, fus) = _twin_sessions(g, B, "bf16", (1, 500), tg.TG_PLAN_AOT_FILL, 919, T, 48, False)
+    rng = np.random.default_rng(17)
+    for step in range(1, T + 1):
+        _step_inputs(rng, sep, "bf16")
+        for name in ("k_tok", "v_tok", "q"):
+            getattr(fus, name).copy_(getattr(sep, name))
+        sep.run_decode_step()
+        for l in fus.layers:
+            tg.tg_decode_noalloc(fus.append_decode_args[l])
+        torch.cuda.synchronize()
+        assert _same_bits(sep.out, fus.out) and _same_bits(sep.lse, fus.lse), f"step {step}"
+        assert _same_bits(sep.pool, fus.pool) and torch.equal(sep.live_len, fus.live_len), f"step {step}"
+
+
+@pytest.mark.parametrize("geom,dtype", [(Geometry(1, 4, 16, 128, 16, 2), "bf16"), (Geometry(1, 4, 8, 64, 16, 2), "f32")])
+def test_append_in_decode_below_the_open_item_stores_nothing(geom, dtype):
+    """A live length below the open item's first entry (lengths that shrank below those the plan was built for)
+    is outside the append's contract: the unit takes no token, the flag is set, and its attention is the one
+    the same call gives without the append."""
+    _gpu()
+    B = 3
+    wl = custom(55, geom, B, dtype, (300, 900))
+    t = Tables(wl, headroom=np.full(B, 8, dtype=np.int32))
+    host = torch.from_numpy(host_pool(wl, t.pool_pages)).to(TORCH_DTYPE[dtype])
+    pair = []
+    for fused in (False, True):
+        s = DecodeSession(wl, tables=t, mode=tg.TG_PLAN_AOT_FILL, n_bins=16, fill="host", pool=host.clone().cuda(),
+                          open_end=True)
+        s.enable_append(fused=fused)
+        pair.append(s)
+    plain, fus = pair
+    rng = np.random.default_rng(8)
+    _step_inputs(rng, plain, dtype)
+    for name in ("k_tok", "v_tok", "q"):
+        getattr(fus, name).copy_(getattr(plain, name))
+    # a unit whose open item does not start at entry 0: its live length becomes the item's first entry - 1
+    items = fus.plans[0]["items"]
+    split_open = [it for it in items if it["tok_end"] < 0 and it["tok_begin"] > 0]
+    assert split_open, "the plan has no split unit"
+    ub, uh, tb = int(split_open[0]["b"]), int(split_open[0]["kv_head"]), int(split_open[0]["tok_begin"])
+    live = plain.live_len.cpu().numpy()
+    live[ub, 0, uh] = tb - 1
+    plain.live_len.copy_(torch.from_numpy(live).cuda())
+    fus.live_len.copy_(torch.from_numpy(live).cuda())
+    before = _f64(fus.pool)
+    tg.tg_decode(plain.dplans[0].args)       # no append at all
+    tg.tg_decode(fus.append_decode_args[0])  # the append: every other unit takes its token
+    torch.cuda.synchronize()
+    assert int(fus.full.item()) == 1
+    got_live = fus.live_len.cpu().numpy()
+    expect = live.copy()
+    expect[:, 0, :] += 1
+    expect[ub, 0, uh] = tb - 1
+    assert np.array_equal(got_live, expect)
+    # the unit's attention: the same bits as without the append
+    G = geom.num_q_heads // geom.num_kv_heads
+    a = plain.out[0, ub, uh * G:(uh + 1) * G]
+    b = fus.out[0, ub, uh * G:(uh + 1) * G]
+    assert _same_bits(a.contiguous(), b.contiguous())
+    # nothing was stored for the unit: its reserved rows past its old length are unchanged
+    ref, _, full = oracle.append_token(_f64(fus.k_tok[0]), _f64(fus.v_tok[0]), before, 0, geom=geom, live_len=live,
+                                       offsets=t.pt_offsets, pages=t.pt_pages, group_of=t.group_of, slot_of=t.slot_of)
+    # the oracle appends for the unit at entry tb - 1; the launch must not have: undo that row in the reference
+    pg, slot, row = oracle.token_location(ub, 0, uh, tb - 1, num_layers=geom.num_layers, num_groups=geom.num_groups,
+                                   page_size=geom.page_size, offsets=t.pt_offsets, pages=t.pt_pages,
+                                   group_of=t.group_of, slot_of=t.slot_of)
+    ref[pg, :, slot, row] = before[pg, :, slot, row]
+    assert np.array_equal(_f64(fus.pool), ref)
