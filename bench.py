@@ -72,7 +72,7 @@ def host_cores():
 def compress_kernel_name(chunk_len):
     from paper_2606_06302_amd import tangram as tg
     if chunk_len <= tg.TG_COMPRESS_ONE_LAUNCH_MAX_CHUNK:
-        return "tg_compress (one launch: each item selects its unit and copies its ranks)"
+        return "tg_compress (one launch: each item's wave selects its unit from registers and copies its ranks)"
     return "tg_compress (select + copy launches)"
 
 

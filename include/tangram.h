@@ -501,8 +501,8 @@ int32_t tg_compress_plan(const tg_geometry* geom, int32_t batch, int32_t layer, 
  * workgroup per (b, h), ranks the chunk's entries and writes the indices of
  * Top(keep_count[b][h]) to kept[]; the copy launch takes one workgroup per
  * item and copies the K and V rows of ranks [rank_begin, rank_end) into their
- * pages.  Shorter chunks take one launch in which every item's workgroup
- * ranks its unit itself and copies its own ranks.  The results are the same.
+ * pages.  Shorter chunks take one launch in which every item's wave ranks
+ * its unit itself and copies its own ranks.  The results are the same.
  * DEVICE pointers:
  *   k_new, v_new [B][C][H][d] dtype: the chunk's K and V before compression
  *   scores  [B][H][C] float32: importance of every chunk entry (from the

@@ -2,9 +2,10 @@
 // per-head Top(count) selection over a chunk's importance scores and the
 // scatter of the kept K and V rows into the head's reserved ragged pages.
 //
-// Chunks of up to kFusedMaxChunk tokens take one launch: every work item's
-// workgroup ranks its unit's chunk in LDS and copies its own ranks.  Longer
-// chunks take two launches on the caller's stream:
+// Chunks of up to kFusedMaxChunk tokens take one launch, one wave per work
+// item: the wave ranks its unit's chunk from registers and copies its own
+// ranks (tg_compress_wave_kernel).  Longer chunks take two launches on the
+// caller's stream:
 //   select - one workgroup of 256 threads per (request, KV head) unit:
 //     1. the unit's n scores become order-preserving 32-bit keys in LDS
 //        (larger score = larger key; -0 maps to +0; NaN maps to 0, below all);
@@ -51,6 +52,7 @@ struct CopyParams {
   const tg_compress_item* items;
   const int32_t* kept;
   int32_t H, C, Hp, P;
+  int32_t p_shift;                   // log2(P) when P is a power of two, else -1
   int32_t row_u4;                    // 16-byte vectors per K or V row: 8, 16 or 32
 };
 
@@ -104,11 +106,9 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
 }
 
 // Top(count) of one unit's chunk scores: the kept chunk indices in ascending
-// order go to kept[] (global, when write_out) and, when kept_lds is not NULL,
-// to kept_lds[0 .. count) as well.  Called by a whole workgroup of kThreads
-// threads; keys is LDS room for C keys.  Returns count.
-__device__ __forceinline__ int select_unit(const SelectParams& p, int64_t unit, uint32_t* keys, int32_t* kept_lds,
-                                           bool write_out = true) {
+// order go to kept[].  Called by a whole workgroup of kThreads threads; keys
+// is LDS room for C keys.
+__device__ __forceinline__ void select_unit(const SelectParams& p, int64_t unit, uint32_t* keys) {
   // per-wave digit histograms, two buffers: a pass reads one while the
   // waves build the next pass's in the other, each wave clearing its own
   __shared__ __align__(16) uint32_t hist[2][kWaves][kBins];
@@ -127,7 +127,7 @@ __device__ __forceinline__ int select_unit(const SelectParams& p, int64_t unit, 
   }
   const int n = min(max(((const TG_CONST int32_t*)p.chunk_tokens)[b], 0), p.C);
   const int count = min(max(((const TG_CONST int32_t*)p.keep_count)[unit], 0), n);
-  if (count == 0) return 0;                      // the whole workgroup leaves together
+  if (count == 0) return;                        // the whole workgroup leaves together
   const bool keep_all = count >= n;
 
   if (!keep_all) *reinterpret_cast<u4*>(&hist[0][wave][4 * lane]) = u4(0u);
@@ -259,21 +259,16 @@ __device__ __forceinline__ int select_unit(const SelectParams& p, int64_t unit, 
       const uint64_t eq_mask = __ballot(eq);
       const bool keep = valid && (keep_all || kk[u] > thr || (eq && run_eq + lanes_below(eq_mask) < need));
       const uint64_t keep_mask = __ballot(keep);
-      if (keep) {
-        const int r = run_kept + lanes_below(keep_mask);
-        if (write_out) out[r] = t;
-        if (kept_lds) kept_lds[r] = t;
-      }
+      if (keep) out[run_kept + lanes_below(keep_mask)] = t;
       run_eq += __popcll(eq_mask);
       run_kept += __popcll(keep_mask);
     }
   }
-  return count;
 }
 
 __global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectParams p) {
   extern __shared__ uint32_t keys[];             // [C] keys of the unit's scores
-  select_unit(p, blockIdx.x, keys, nullptr);
+  select_unit(p, blockIdx.x, keys);
 }
 
 // Copies the K and V rows of ranks [r0, r0 + rows) of one unit: rank j's
@@ -281,10 +276,9 @@ __global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectPara
 // whole workgroup, kUnroll rows in flight per thread.
 template <int kUnroll, typename TokFn>
 __device__ __forceinline__ void copy_rows(const CopyParams& p, const tg_compress_item& it, int r0, int rows,
-                                          TokFn tok) {
-  const int tid = threadIdx.x;
+                                          TokFn tok, int tid = threadIdx.x, int nthreads = kThreads) {
   const int lpr = p.row_u4;
-  const int rpp = kThreads / lpr;               // rows per pass of the workgroup
+  const int rpp = nthreads / lpr;               // rows per pass of the thread group
   const int sub = tid % lpr, rsel = tid / lpr;
   const int64_t tok_stride = (int64_t)p.H * lpr;
   const int64_t src0 = ((int64_t)it.b * p.C * p.H + it.kv_head) * lpr + sub;
@@ -302,14 +296,16 @@ __device__ __forceinline__ void copy_rows(const CopyParams& p, const tg_compress
       const int64_t src = src0 + t * tok_stride;
       kk[u] = p.k_new[src];
       vv[u] = p.v_new[src];
-      page[u] = p.pt_pages[it.pt_base + (it.cursor + r0 + j) / p.P];
+      const int pos = it.cursor + r0 + j;
+      page[u] = p.pt_pages[it.pt_base + (p.p_shift >= 0 ? pos >> p.p_shift : pos / p.P)];
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int j = base + u * rpp + rsel;
       if (j < rows) {
         const int pos = it.cursor + r0 + j;
-        const int64_t dst = (((int64_t)page[u] * 2 * p.Hp + it.slot) * p.P + pos % p.P) * lpr + sub;
+        const int row = p.p_shift >= 0 ? pos & (p.P - 1) : pos % p.P;
+        const int64_t dst = (((int64_t)page[u] * 2 * p.Hp + it.slot) * p.P + row) * lpr + sub;
         p.pool[dst] = kk[u];
         p.pool[dst + v_plane] = vv[u];
       }
@@ -325,26 +321,110 @@ __global__ __launch_bounds__(kThreads) void tg_compress_copy_kernel(CopyParams p
   copy_rows<kUnroll>(p, it, r0, r1 - r0, [&](int j) { return src_tok[j]; });
 }
 
-// Short chunks in one launch: every work item's workgroup ranks its unit's
-// chunk itself (into LDS; the unit's first item also writes kept[]) and
-// copies its own ranks.  A unit's selection runs once per item, which at short
-// chunks costs less than the second launch and the round trip of the kept
-// indices through global memory that the two-launch form pays.
-__global__ __launch_bounds__(kThreads) void tg_compress_fused_kernel(SelectParams sp, CopyParams p) {
-  extern __shared__ uint32_t lds[];             // [C] keys, then [C] kept chunk indices
-  const tg_compress_item it = load_item((const TG_CONST tg_compress_item*)p.items + blockIdx.x);
-  int32_t* kept_lds = reinterpret_cast<int32_t*>(lds + p.C);
+// Short chunks in one launch, one single-wave workgroup per work item and no
+// barrier: the wave holds its unit's whole chunk of keys in registers (lane
+// l, slot i: token 64*i + l, so the score loads are coalesced and token order
+// is slot-major), finds the count-th largest key with the same
+// most-significant-digit radix select as select_unit (the digit histogram in
+// the wave's LDS, whose operations a wave executes in order), ranks the kept
+// entries by ballots in token order, and copies its own ranks.  The unit's
+// first item also writes kept[].  KPL = keys per lane.  Single-wave
+// workgroups spread the items over every CU (measured at chunk 512: 7.9 us,
+// against 8.1, 9.3 and 12.1 us with 4, 8 and 16 items per workgroup).
+template <int KPL>
+__global__ __launch_bounds__(64) void tg_compress_wave_kernel(SelectParams sp, CopyParams p, int32_t n_items) {
+  constexpr int kSpill = kFusedMaxChunk;        // per-lane dummy entries for branch-free stores
+  __shared__ __align__(16) uint32_t hist[kBins];
+  __shared__ int32_t kept_lds[kFusedMaxChunk + 64];
+  const int lane = threadIdx.x;
+  const int item = blockIdx.x;
+  if (item >= n_items) return;
+  const tg_compress_item it = load_item((const TG_CONST tg_compress_item*)p.items + item);
   const int64_t unit = (int64_t)it.b * p.H + it.kv_head;
-  const int count = select_unit(sp, unit, lds, kept_lds, false);
-  __syncthreads();
+  const int C = sp.C;
+  // every score load goes out before the counts arrive: entries below C exist whatever chunk_tokens says
+  const uint32_t* sc = sp.scores + unit * C;
+  uint32_t key[KPL];
+#pragma unroll
+  for (int i = 0; i < KPL; ++i) {
+    const int t = 64 * i + lane;
+    key[i] = t < C ? sc[t] : 0u;
+  }
+  const int n = min(max(((const TG_CONST int32_t*)sp.chunk_tokens)[it.b], 0), C);
+  const int count = min(max(((const TG_CONST int32_t*)sp.keep_count)[unit], 0), n);
+  if (count == 0) return;
+  const bool keep_all = count >= n;
+#pragma unroll
+  for (int i = 0; i < KPL; ++i) key[i] = order_key(key[i]);
+
+  // after the select, the kept keys are those whose prefix (mask) is above
+  // thr, and `need` of those whose prefix equals thr (the lowest-index ones);
+  // whole: every key with prefix thr is kept
+  uint32_t thr = 0, mask = 0;
+  int need = count;
+  bool whole = true;
+  if (!keep_all) {
+    for (int shift = 24;; shift -= 8) {
+      *reinterpret_cast<u4*>(&hist[4 * lane]) = u4(0u);
+#pragma unroll
+      for (int i = 0; i < KPL; ++i)
+        if (64 * i + lane < n && (key[i] & mask) == thr) atomicAdd(&hist[(key[i] >> shift) & 0xffu], 1u);
+      // lane i owns digits 255-4i .. 252-4i, in descending order
+      const u4 hv = *reinterpret_cast<const u4*>(&hist[252 - 4 * lane]);
+      const int c[4] = {(int)hv.w, (int)hv.z, (int)hv.y, (int)hv.x};
+      const int s = c[0] + c[1] + c[2] + c[3];
+      int run = wave_inclusive_sum(s) - s;   // matching keys with a larger digit
+      int f_digit = -1, f_need = 0, f_whole = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (run < need && run + c[j] >= need) {
+          f_digit = 255 - 4 * lane - j;
+          f_need = need - run;
+          f_whole = run + c[j] == need;
+        }
+        run += c[j];
+      }
+      const uint64_t holder = __ballot(f_digit >= 0);
+      const int src = holder ? (int)__builtin_ctzll(holder) : 0;
+      const int digit = __builtin_amdgcn_readlane(f_digit, src);
+      need = __builtin_amdgcn_readlane(f_need, src);
+      whole = __builtin_amdgcn_readlane(f_whole, src) != 0;
+      thr |= (uint32_t)digit << shift;
+      mask |= 0xffu << shift;
+      if (whole || shift == 0) break;
+    }
+  }
+
+  // ranks in token order (slot-major); a lane that keeps nothing in a slot
+  // stores to its own dummy entry instead of branching
+  int32_t* kl = kept_lds;
+  int run_eq = 0, run_kept = 0;
+#pragma unroll
+  for (int i = 0; i < KPL; ++i) {
+    const int t = 64 * i + lane;
+    const bool valid = t < n;
+    const uint32_t kk = key[i] & mask;
+    bool keep;
+    if (keep_all) {
+      keep = valid;
+    } else if (whole) {
+      keep = valid && kk >= thr;
+    } else {   // only the lowest-index `need` keys equal to thr are kept
+      const bool eq = valid && kk == thr;
+      const uint64_t eq_mask = __ballot(eq);
+      keep = valid && (kk > thr || (eq && run_eq + lanes_below(eq_mask) < need));
+      run_eq += __popcll(eq_mask);
+    }
+    const uint64_t keep_mask = __ballot(keep);
+    kl[keep ? run_kept + lanes_below(keep_mask) : kSpill + lane] = t;
+    run_kept += __popcll(keep_mask);
+  }
   const int r0 = max(it.rank_begin, 0);
   const int r1 = min(min(it.rank_end, min(count, min(it.count, p.C))), r0 + TG_COMPRESS_MAX_ROWS);
-  copy_rows<kUnroll>(p, it, r0, r1 - r0, [&](int j) { return kept_lds[r0 + j]; });
-  // the unit's first item publishes the kept indices last: stored before the
-  // barrier above, they would make every wave wait for them there
+  copy_rows<8>(p, it, r0, r1 - r0, [&](int j) { return kl[r0 + j]; }, lane, 64);
   if (it.rank_begin == 0) {
     int32_t* out = sp.kept + unit * p.C;
-    for (int r = threadIdx.x; r < count; r += kThreads) out[r] = kept_lds[r];
+    for (int r = lane; r < count; r += 64) out[r] = kl[r];
   }
 }
 
@@ -378,6 +458,7 @@ extern "C" int32_t tg_compress(const tg_compress_args* a, void* hip_stream) {
   c.C = a->chunk_len;
   c.Hp = g.heads_per_group;
   c.P = g.page_size;
+  c.p_shift = (g.page_size & (g.page_size - 1)) == 0 ? __builtin_ctz((unsigned)g.page_size) : -1;
   c.row_u4 = g.head_dim * (a->dtype == TG_F32 ? 4 : 2) / 16;
   s.scores = reinterpret_cast<const uint32_t*>(a->scores);
   s.chunk_tokens = a->chunk_tokens;
@@ -387,8 +468,13 @@ extern "C" int32_t tg_compress(const tg_compress_args* a, void* hip_stream) {
   s.C = a->chunk_len;
   static_assert(kBins == kThreads, "one histogram bin per thread");
   if (a->chunk_len <= kFusedMaxChunk) {
-    const size_t lds2 = 2 * (size_t)a->chunk_len * sizeof(uint32_t);   // keys + kept indices
-    hipLaunchKernelGGL(tg_compress_fused_kernel, dim3(a->num_items), dim3(kThreads), lds2, stream, s, c);
+    const int kpl = (a->chunk_len + 63) / 64;
+    const dim3 grid((unsigned)a->num_items), block(64);
+    if (kpl <= 1) hipLaunchKernelGGL(tg_compress_wave_kernel<1>, grid, block, 0, stream, s, c, a->num_items);
+    else if (kpl <= 2) hipLaunchKernelGGL(tg_compress_wave_kernel<2>, grid, block, 0, stream, s, c, a->num_items);
+    else if (kpl <= 4) hipLaunchKernelGGL(tg_compress_wave_kernel<4>, grid, block, 0, stream, s, c, a->num_items);
+    else if (kpl <= 8) hipLaunchKernelGGL(tg_compress_wave_kernel<8>, grid, block, 0, stream, s, c, a->num_items);
+    else hipLaunchKernelGGL(tg_compress_wave_kernel<16>, grid, block, 0, stream, s, c, a->num_items);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress launch failed: %s", hipGetErrorString(e));
     return TG_OK;

@@ -73,6 +73,8 @@ CASES = [
     (Geometry(1, 8, 8, 128, 16, 4), 2, "f32", 300, 256, "overflow", 0, None),
     (Geometry(2, 4, 16, 128, 16, 2), 3, "bf16", 2000, 64, "reserved", 1, None),
     (Geometry(1, 4, 4, 64, 5, 2), 2, "bf16", 100, 7, "overflow", 0, None),
+    (Geometry(1, 4, 8, 128, 16, 2), 2, "bf16", 200, 32, "reserved", 0, None),
+    (Geometry(1, 2, 4, 128, 16, 1), 2, "f32", 1024, 256, "overflow", 0, None),
 ]
 
 
