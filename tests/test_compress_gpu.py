@@ -96,6 +96,26 @@ def test_compress_small_vs_oracle(geom, B, dtype, C, R, sel, layer, budget):
     assert kept > 0
 
 
+@pytest.mark.parametrize("C", [64, 65, 128, 129, 256, 257, 1023, 1024, 1025])
+def test_compress_chunk_lengths_at_kernel_boundaries(C):
+    """Chunk lengths on both sides of the one-launch kernel's keys-per-lane steps (64, 128, 256 tokens) and of
+    the one-launch limit (1024): the whole pool and the kept lists bit-exact against the oracle, with ties,
+    signed zeros, infinities and NaN among the scores."""
+    _gpu()
+    g = Geometry(1, 4, 16, 128, 16, 2)
+    B = 3
+    rng = np.random.default_rng(4000 + C)
+    ctx = rng.integers(C, 3 * C + 20, size=B).astype(np.int32)
+    wl = custom(4000 + C, g, B, "bf16", ctx, chunk_len=C)
+    toks = np.array([C, int(rng.integers(1, C + 1)), max(1, C - 1)], dtype=np.int32)
+    starts = np.array([int(rng.integers(0, c - n + 1)) for c, n in zip(ctx, toks)], dtype=np.int32)
+    say(f"compress boundary C={C} toks={toks.tolist()}")
+    tables = Tables(wl)
+    pool = _pool_for(wl, tables)
+    _, kept = _run_and_check(wl, tables, pool, starts, toks, np.minimum(1.0, wl.ratio * 1.3), 32, 0, rng)
+    assert kept > 0
+
+
 def test_compress_three_chunks_then_decode():
     """A context compressed chunk by chunk fills its reservation exactly; decode attention over the
     resulting cache matches the oracle (prefill compression feeding the decode kernel)."""
