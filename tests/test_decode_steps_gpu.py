@@ -6,7 +6,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_helpers import check_close, say
+from gpu_helpers import check_close, say, sweep_cases
 from workloads import Geometry, custom, host_pool
 
 pytestmark = pytest.mark.gpu
@@ -221,6 +221,43 @@ def test_append_in_decode_without_room_matches_append_launch():
             assert np.array_equal(_f64(fus.pool), ref)
             assert _same_bits(sep.out, fus.out) and _same_bits(sep.lse, fus.lse), f"{geom} step {step}"
         assert int(sep.full.item()) == 1 and int(fus.full.item()) == 1
+
+
+def test_append_in_decode_random_sweep():
+    """Seeded sweep: 6 random (dtype, head_dim, KV heads, heads per group, gqa, batch, layers, context range, plan
+    mode, bins, merge) cases, each run for a few steps with the append as its own launch and inside the decode
+    launch: outputs, lse, the whole pool and the live lengths equal bit for bit after every step."""
+    _gpu()
+    rng = np.random.default_rng(777)
+    for case in range(sweep_cases(6)):
+        dtype = ["f32", "bf16"][int(rng.integers(2))]
+        d = [64, 128][int(rng.integers(2))]
+        H = [1, 2, 4, 8][int(rng.integers(4))]
+        hps = [x for x in (1, 2, 4, 8) if H % x == 0]
+        Hp = hps[int(rng.integers(len(hps)))]
+        gqa = int(rng.integers(1, 17))
+        B, L, T = int(rng.integers(1, 5)), int(rng.integers(1, 3)), int(rng.integers(2, 10))
+        lo = int(rng.integers(1, 300))
+        hi = lo + int(rng.integers(1, 1500))
+        mode = [tg.TG_PLAN_AOT_FILL, tg.TG_PLAN_AOT][int(rng.integers(2))]
+        n_bins, merge = int(rng.integers(1, 200)), bool(rng.integers(2))
+        g = Geometry(L, H, H * gqa, d, 16, Hp)
+        say(f"append sweep case {case}: {dtype} d{d} H{H} Hp{Hp} gqa{gqa} B{B} L{L} ctx ({lo}, {hi}) steps {T} "
+            f"mode {mode} bins {n_bins} merge {merge}")
+        wl, t, (sep, fus) = _twin_sessions(g, B, dtype, (lo, hi), mode, 6000 + case, T, n_bins, merge)
+        srng = np.random.default_rng(case)
+        for step in range(1, T + 1):
+            _step_inputs(srng, sep, dtype)
+            for name in ("k_tok", "v_tok", "q"):
+                getattr(fus, name).copy_(getattr(sep, name))
+            sep.run_decode_step()
+            fus.run_decode_step()
+            torch.cuda.synchronize()
+            assert _same_bits(sep.out, fus.out), f"case {case}: out differs at step {step}"
+            assert _same_bits(sep.lse, fus.lse), f"case {case}: lse differs at step {step}"
+            assert _same_bits(sep.pool, fus.pool), f"case {case}: pool differs at step {step}"
+            assert torch.equal(sep.live_len, fus.live_len), f"case {case}: live lengths differ at step {step}"
+        assert int(fus.full.item()) == 0
 
 
 def test_append_in_noalloc_decode_is_bitwise_append_then_decode():
