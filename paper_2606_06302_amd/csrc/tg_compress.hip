@@ -6,14 +6,15 @@
 // item: the wave ranks its unit's chunk from registers and copies its own
 // ranks (tg_compress_wave_kernel).  Longer chunks take two launches on the
 // caller's stream:
-//   select - one workgroup of 256 threads per (request, KV head) unit:
+//   select - one workgroup per (request, KV head) unit, 512 threads up to
+//     4096 chunk entries and 1024 above (8 to 16 keys per thread):
 //     1. the unit's n scores become order-preserving 32-bit keys in LDS
 //        (larger score = larger key; -0 maps to +0; NaN maps to 0, below all);
 //     2. a most-significant-digit-first radix select (up to four 8-bit
 //        passes, one LDS histogram per wave) finds the count-th largest key T
 //        and how many entries equal to T are kept (the lowest-index ones); it
 //        stops early once the chosen digit's whole bucket is kept;
-//     3. each wave walks its quarter of the tokens 64 at a time; ballots of
+//     3. each wave walks its share of the tokens 64 at a time; ballots of
 //        the "kept" and "equal to T" predicates and lane-prefix bit counts
 //        give every kept entry its rank in token order, written to kept[].
 //   copy - one workgroup per work item (at most TG_COMPRESS_MAX_ROWS ranks of
@@ -26,9 +27,8 @@
 
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWaves = kThreads / 64;
-constexpr int kBins = 256;           // one radix digit of 8 bits; == kThreads
+constexpr int kThreads = 256;           // copy launch
+constexpr int kBins = 256;              // one radix digit of 8 bits
 constexpr int kUnroll = 4;           // rows in flight per thread in the copy launch
 constexpr int kBatch = 8;            // score loads / LDS key reads in flight per thread
 constexpr int kGroups = 4;           // 64-token groups per batch of the ranking walk
@@ -106,9 +106,11 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
 }
 
 // Top(count) of one unit's chunk scores: the kept chunk indices in ascending
-// order go to kept[].  Called by a whole workgroup of kThreads threads; keys
+// order go to kept[].  Called by a whole workgroup of kSelThreads threads; keys
 // is LDS room for C keys.
+template <int kSelThreads>
 __device__ __forceinline__ void select_unit(const SelectParams& p, int64_t unit, uint32_t* keys) {
+  constexpr int kWaves = kSelThreads / 64;
   // per-wave digit histograms, two buffers: a pass reads one while the
   // waves build the next pass's in the other, each wave clearing its own
   __shared__ __align__(16) uint32_t hist[2][kWaves][kBins];
@@ -122,7 +124,7 @@ __device__ __forceinline__ void select_unit(const SelectParams& p, int64_t unit,
   uint32_t v[kBatch];
 #pragma unroll
   for (int u = 0; u < kBatch; ++u) {
-    const int t = tid + u * kThreads;
+    const int t = tid + u * kSelThreads;
     v[u] = t < p.C ? sc[t] : 0u;
   }
   const int n = min(max(((const TG_CONST int32_t*)p.chunk_tokens)[b], 0), p.C);
@@ -133,17 +135,17 @@ __device__ __forceinline__ void select_unit(const SelectParams& p, int64_t unit,
   if (!keep_all) *reinterpret_cast<u4*>(&hist[0][wave][4 * lane]) = u4(0u);
   // keys into LDS, kBatch loads in flight per thread; the histogram of the
   // top digit is taken on the way
-  for (int t0 = tid; t0 < n; t0 += kBatch * kThreads) {
+  for (int t0 = tid; t0 < n; t0 += kBatch * kSelThreads) {
     if (t0 != tid) {
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
-        const int t = t0 + u * kThreads;
+        const int t = t0 + u * kSelThreads;
         v[u] = t < n ? sc[t] : 0u;
       }
     }
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
-      const int t = t0 + u * kThreads;
+      const int t = t0 + u * kSelThreads;
       if (t < n) {
         const uint32_t key = order_key(v[u]);
         keys[t] = key;
@@ -198,11 +200,11 @@ __device__ __forceinline__ void select_unit(const SelectParams& p, int64_t unit,
       // the next digit's histogram over the keys that share the prefix
       buf ^= 1;
       *reinterpret_cast<u4*>(&hist[buf][wave][4 * lane]) = u4(0u);
-      for (int t0 = tid; t0 < n; t0 += kBatch * kThreads) {
+      for (int t0 = tid; t0 < n; t0 += kBatch * kSelThreads) {
         uint32_t kk[kBatch];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-          const int t = t0 + u * kThreads;
+          const int t = t0 + u * kSelThreads;
           kk[u] = t < n ? keys[t] : ~thr;    // ~thr never matches thr under mask (mask != 0 here)
         }
 #pragma unroll
@@ -215,7 +217,7 @@ __device__ __forceinline__ void select_unit(const SelectParams& p, int64_t unit,
 
   // ranks in token order: wave w owns tokens [w*span, (w+1)*span), walked in
   // groups of 64, kGroups groups per batch of LDS reads
-  const int span = ((n + kThreads - 1) / kThreads) * 64;
+  const int span = ((n + kSelThreads - 1) / kSelThreads) * 64;
   const int t_begin = wave * span, t_end = min(n, t_begin + span);
   int gt_w = 0, eq_w = 0;
   for (int base = t_begin; base < t_end; base += 64 * kGroups) {
@@ -266,9 +268,11 @@ __device__ __forceinline__ void select_unit(const SelectParams& p, int64_t unit,
   }
 }
 
-__global__ __launch_bounds__(kThreads) void tg_compress_select_kernel(SelectParams p) {
+// kSelThreads: 512 up to 4096 chunk entries, 1024 above (8 to 16 keys per thread)
+template <int kSelThreads>
+__global__ __launch_bounds__(kSelThreads) void tg_compress_select_kernel(SelectParams p) {
   extern __shared__ uint32_t keys[];             // [C] keys of the unit's scores
-  select_unit(p, blockIdx.x, keys);
+  select_unit<kSelThreads>(p, blockIdx.x, keys);
 }
 
 // Copies the K and V rows of ranks [r0, r0 + rows) of one unit: rank j's
@@ -466,7 +470,6 @@ extern "C" int32_t tg_compress(const tg_compress_args* a, void* hip_stream) {
   s.kept = a->kept;
   s.H = g.num_kv_heads;
   s.C = a->chunk_len;
-  static_assert(kBins == kThreads, "one histogram bin per thread");
   if (a->chunk_len <= kFusedMaxChunk) {
     const int kpl = (a->chunk_len + 63) / 64;
     const dim3 grid((unsigned)a->num_items), block(64);
@@ -480,12 +483,17 @@ extern "C" int32_t tg_compress(const tg_compress_args* a, void* hip_stream) {
     return TG_OK;
   }
   const size_t lds = (size_t)a->chunk_len * sizeof(uint32_t);
+  const bool wide = a->chunk_len > 4096;
+  const void* select = wide ? reinterpret_cast<const void*>(tg_compress_select_kernel<1024>)
+                            : reinterpret_cast<const void*>(tg_compress_select_kernel<512>);
   if (lds > 32768) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(tg_compress_select_kernel),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    hipError_t e = hipFuncSetAttribute(select, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress LDS attribute: %s", hipGetErrorString(e));
   }
-  hipLaunchKernelGGL(tg_compress_select_kernel, dim3(a->batch * g.num_kv_heads), dim3(kThreads), lds, stream, s);
+  if (wide)
+    hipLaunchKernelGGL(tg_compress_select_kernel<1024>, dim3(a->batch * g.num_kv_heads), dim3(1024), lds, stream, s);
+  else
+    hipLaunchKernelGGL(tg_compress_select_kernel<512>, dim3(a->batch * g.num_kv_heads), dim3(512), lds, stream, s);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "compress select launch failed: %s", hipGetErrorString(e));
   hipLaunchKernelGGL(tg_compress_copy_kernel, dim3(a->num_items), dim3(kThreads), 0, stream, c);

@@ -96,11 +96,12 @@ def test_compress_small_vs_oracle(geom, B, dtype, C, R, sel, layer, budget):
     assert kept > 0
 
 
-@pytest.mark.parametrize("C", [64, 65, 128, 129, 256, 257, 1023, 1024, 1025])
+@pytest.mark.parametrize("C", [64, 65, 128, 129, 256, 257, 1023, 1024, 1025, 4096, 4097])
 def test_compress_chunk_lengths_at_kernel_boundaries(C):
-    """Chunk lengths on both sides of the one-launch kernel's keys-per-lane steps (64, 128, 256 tokens) and of
-    the one-launch limit (1024): the whole pool and the kept lists bit-exact against the oracle, with ties,
-    signed zeros, infinities and NaN among the scores."""
+    """Chunk lengths on both sides of the one-launch kernel's keys-per-lane steps (64, 128, 256 tokens), of
+    the one-launch limit (1024) and of the select launch's switch from 512 to 1024 threads (4096): the whole
+    pool and the kept lists bit-exact against the oracle, with ties, signed zeros, infinities and NaN among
+    the scores."""
     _gpu()
     g = Geometry(1, 4, 16, 128, 16, 2)
     B = 3
