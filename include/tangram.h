@@ -27,6 +27,10 @@
  *   - Arguments are validated on the host before anything is written or
  *     enqueued.  On error nothing is written past what the error's
  *     description says, and no page is consumed.
+ *   - Device calls move Q, K, V, tokens, outputs, partials and pool rows with
+ *     8- and 16-byte vector accesses: those buffers (and the decode
+ *     workspace) must be 16-byte aligned, as hipMalloc's are; a misaligned
+ *     one is refused with TG_ERR_INVALID_ARG before anything is enqueued.
  *   - Host integer calls are pure, deterministic and thread-safe (tg_reserve
  *     checks and copies large page lists on up to 16 helper threads, or
  *     TG_HOST_THREADS; results do not depend on the thread count).  The only

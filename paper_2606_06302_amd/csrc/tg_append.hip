@@ -72,6 +72,8 @@ extern "C" int32_t tg_append(const tg_append_args* a, void* hip_stream) {
   if (!a->k_tok || !a->v_tok || !a->kv_pool || !a->pt_pages || !a->pt_offsets || !a->group_of || !a->slot_of ||
       !a->live_len)
     return tg::fail(TG_ERR_INVALID_ARG, "NULL device pointer");
+  if (!tg::aligned16({a->k_tok, a->v_tok, a->kv_pool}))
+    return tg::fail(TG_ERR_INVALID_ARG, "device buffers must be 16-byte aligned");
   AppendParams p;
   p.k_tok = static_cast<const u4*>(a->k_tok);
   p.v_tok = static_cast<const u4*>(a->v_tok);

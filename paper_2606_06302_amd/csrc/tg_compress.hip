@@ -449,6 +449,8 @@ extern "C" int32_t tg_compress(const tg_compress_args* a, void* hip_stream) {
   if (!a->k_new || !a->v_new || !a->scores || !a->kv_pool || !a->pt_pages || !a->items || !a->chunk_tokens ||
       !a->keep_count || !a->kept)
     return tg::fail(TG_ERR_INVALID_ARG, "NULL device pointer");
+  if (!tg::aligned16({a->k_new, a->v_new, a->kv_pool}))
+    return tg::fail(TG_ERR_INVALID_ARG, "device buffers must be 16-byte aligned");
   hipStream_t stream = static_cast<hipStream_t>(hip_stream);
   SelectParams s;
   CopyParams c;

@@ -100,6 +100,19 @@ __device__ __forceinline__ void store_out<float>(float* dst, float v) { *dst = v
 template <>
 __device__ __forceinline__ void store_out<uint16_t>(uint16_t* dst, float v) { *dst = f32_to_bf16(v); }
 
+// four consecutive outputs, one 16- or 8-byte store (dst 16- or 8-byte aligned)
+template <typename T>
+__device__ __forceinline__ void store_out4(T* dst, float v0, float v1, float v2, float v3);
+template <>
+__device__ __forceinline__ void store_out4<float>(float* dst, float v0, float v1, float v2, float v3) {
+  *reinterpret_cast<float4*>(dst) = make_float4(v0, v1, v2, v3);
+}
+template <>
+__device__ __forceinline__ void store_out4<uint16_t>(uint16_t* dst, float v0, float v1, float v2, float v3) {
+  *reinterpret_cast<uint2*>(dst) = make_uint2(uint32_t(f32_to_bf16(v0)) | (uint32_t(f32_to_bf16(v1)) << 16),
+                                              uint32_t(f32_to_bf16(v2)) | (uint32_t(f32_to_bf16(v3)) << 16));
+}
+
 struct DecodeParams {
   const void* q;
   const u4* pool;            // 16-byte view of the page pool
@@ -853,9 +866,10 @@ __global__ void __launch_bounds__(kBlock) tg_decode_mfma_kernel(DecodeParams p, 
 // ---------------------------------------------------------------------------
 // Log-sum-exp merge of the split partials of every unit (b, h) with more than
 // one split: lse* = log sum_i e^{lse_i}, O = sum_i e^{lse_i - lse*} o_i.
-// Grid (units, ceil(gqa*D / 256)): each thread owns one output element and
-// makes a single pass with a running max, so the loads of consecutive splits
-// are independent and issue back to back.
+// Grid (units, ceil(gqa*D / 1024)): each thread owns four consecutive output
+// elements (16-byte partial loads) and makes a single pass with a running
+// max, so the loads of consecutive splits are independent and issue back to
+// back.
 template <typename T, int D>
 __global__ void __launch_bounds__(kBlock) tg_merge_kernel(const int32_t* __restrict__ unit_splits,
                                                          const int32_t* __restrict__ unit_base,
@@ -868,39 +882,45 @@ __global__ void __launch_bounds__(kBlock) tg_merge_kernel(const int32_t* __restr
   // both reads in flight together, before the exit test (the compiler would
   // otherwise sink the second behind it: two round trips instead of one)
   asm volatile("" ::"s"(s), "s"(base));
-  const int o = blockIdx.y * kBlock + threadIdx.x;
+  const int o = (blockIdx.y * kBlock + threadIdx.x) * 4;
   if (s <= 1 || o >= gqa * D) return;
   const int b = u / num_kv_heads, h = u % num_kv_heads;
   const int64_t row0 = (int64_t)b * num_kv_heads * gqa + (int64_t)h * gqa;
-  const int g = o / D, e = o % D;
+  const int g = o / D, e = o % D;   // D is a multiple of 4: the four outputs share g
   const float* pl = part_lse + (int64_t)base * gqa + g;
-  const float* po = part_o + ((int64_t)base * gqa + g) * D + e;
-  float m = -INFINITY, L = 0.f, A = 0.f;
+  const f32x4* po = reinterpret_cast<const f32x4*>(part_o + ((int64_t)base * gqa + g) * D + e);
+  float m = -INFINITY, L = 0.f;
+  f32x4 A = {0.f, 0.f, 0.f, 0.f};
   // kBatch splits' loads go out before the first is used, so a unit of up to
   // kBatch splits pays one memory round trip, not one per split.  Indices past
   // the last split re-read it; their steps are computed and then discarded by
   // selects (a branch would let the compiler sink the loads behind it).
   constexpr int kBatch = 4;
   for (int i0 = 0; i0 < s; i0 += kBatch) {
-    float lv[kBatch], ov[kBatch];
+    float lv[kBatch];
+    f32x4 ov[kBatch];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       const int64_t i = min(i0 + j, s - 1);
       lv[j] = pl[i * gqa];
-      ov[j] = po[i * gqa * D];
+      ov[j] = po[i * gqa * (D / 4)];
     }
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
       const bool use = i0 + j < s;
       const float mn = fmaxf(m, lv[j]);
       const float a = __expf(m - mn), w = __expf(lv[j] - mn);
-      const float Ln = fmaf(L, a, w), An = fmaf(A, a, w * ov[j]);
+      const float Ln = fmaf(L, a, w);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float An = fmaf(A[q], a, w * ov[j][q]);
+        A[q] = use ? An : A[q];
+      }
       L = use ? Ln : L;
-      A = use ? An : A;
       m = use ? mn : m;
     }
   }
-  store_out<T>(static_cast<T*>(out) + (row0 + g) * D + e, A / L);
+  store_out4<T>(static_cast<T*>(out) + (row0 + g) * D + e, A[0] / L, A[1] / L, A[2] / L, A[3] / L);
   if (lse && e == 0) lse[row0 + g] = m + logf(L);
 }
 
@@ -1004,6 +1024,8 @@ int32_t decode_impl(const tg_decode_args* a, void* ws_ptr, size_t ws_bytes, void
   const size_t need = tg_decode_workspace_bytes(&g, a->batch, a->num_partials);
   if (a->num_partials > 0 && (!ws_ptr || ws_bytes < need))
     return tg::fail(TG_ERR_BUFFER_TOO_SMALL, "workspace holds %zu bytes, need %zu", ws_bytes, need);
+  if (!tg::aligned16({a->q, a->kv_pool, a->out, a->append_k, a->append_v, a->num_partials > 0 ? ws_ptr : nullptr}))
+    return tg::fail(TG_ERR_INVALID_ARG, "device buffers must be 16-byte aligned");
   const int gqa = g.num_q_heads / g.num_kv_heads;
   const int esz = a->dtype == TG_F32 ? 4 : 2;
   const size_t o_bytes = align256((size_t)a->num_partials * gqa * g.head_dim * 4);
@@ -1055,7 +1077,7 @@ int32_t decode_impl(const tg_decode_args* a, void* ws_ptr, size_t ws_bytes, void
   if (e != hipSuccess) return tg::fail(TG_ERR_HIP, "decode launch failed: %s", hipGetErrorString(e));
   if (a->num_partials > 0 && !fused_merge) {
     MergeFn mf = pick_merge(a->dtype, g.head_dim);
-    hipLaunchKernelGGL(mf, dim3(a->batch * g.num_kv_heads, (gqa * g.head_dim + kBlock - 1) / kBlock), dim3(kBlock), 0,
+    hipLaunchKernelGGL(mf, dim3(a->batch * g.num_kv_heads, (gqa * g.head_dim / 4 + kBlock - 1) / kBlock), dim3(kBlock), 0,
                        st, a->unit_splits,
                        a->unit_partial_base, p.part_o, p.part_lse, a->out, a->lse, g.num_kv_heads, gqa);
     e = hipGetLastError();

@@ -440,6 +440,8 @@ int32_t tg_prefill(const tg_prefill_args* a, void* hip_stream) {
   if (!a->q || !a->k_new || !a->v_new || !a->kv_pool || !a->pt_pages || !a->pt_offsets || !a->kv_len ||
       !a->group_of || !a->slot_of || !a->out)
     return tg::fail(TG_ERR_INVALID_ARG, "NULL device pointer");
+  if (!tg::aligned16({a->q, a->k_new, a->v_new, a->kv_pool, a->out}))
+    return tg::fail(TG_ERR_INVALID_ARG, "device buffers must be 16-byte aligned");
   PrefillParams p;
   p.q = static_cast<const uint16_t*>(a->q);
   p.k_new = static_cast<const u4*>(a->k_new);

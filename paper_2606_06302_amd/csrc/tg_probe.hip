@@ -80,6 +80,7 @@ extern "C" int32_t tg_read_probe(const tg_geometry* geom, int32_t dtype, const v
     return tg::fail(TG_ERR_UNSUPPORTED, "slab of %lld bytes: need 2, 4 or 8 KiB", (long long)slab_bytes);
   if (n < 0 || n_workers < 1) return tg::fail(TG_ERR_INVALID_ARG, "n < 0 or n_workers < 1");
   if (n > 0 && (!kv_pool || !page_ids || !slots)) return tg::fail(TG_ERR_INVALID_ARG, "NULL device pointer");
+  if (!tg::aligned16({kv_pool})) return tg::fail(TG_ERR_INVALID_ARG, "device buffers must be 16-byte aligned");
   if (!out) return tg::fail(TG_ERR_INVALID_ARG, "out is NULL");
   ProbeParams p;
   p.pool = static_cast<const u4*>(kv_pool);

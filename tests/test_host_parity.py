@@ -523,6 +523,42 @@ def test_decode_append_arguments_checked_on_host():
         assert e.value.code == tg.TG_ERR_INVALID_ARG, kw
 
 
+def test_misaligned_device_buffers_refused_on_host():
+    """The device calls move Q, K, V, tokens, outputs and pool rows with 16-byte accesses: a buffer that is
+    not 16-byte aligned is refused with TG_ERR_INVALID_ARG before anything is enqueued (the fake device
+    pointers below are never dereferenced)."""
+    g = Geometry(1, 2, 4, 128, 16, 2)
+    fake, off = 1 << 20, (1 << 20) + 8
+
+    def refused(fn, args, field):
+        setattr(args, field, off)
+        rc = fn(ctypes.byref(args), None)
+        assert rc == tg.TG_ERR_INVALID_ARG and b"16-byte aligned" in tg._lib.tg_last_error(), field
+        setattr(args, field, fake)
+
+    d = tg.make_decode_args(g, 1, tg.TG_BF16, None, None, None, None, None, 4, 1, None, None, 0, None)
+    for f in ("q", "kv_pool", "pt_pages", "items", "bin_offsets", "out"):
+        setattr(d, f, fake)
+    for f in ("q", "kv_pool", "out"):
+        refused(tg._lib.tg_decode, d, f)
+    d.append_k, d.append_v, d.live_len = fake, fake, fake
+    for f in ("append_k", "append_v"):
+        refused(tg._lib.tg_decode, d, f)
+
+    pre = tg.tg_prefill_args(tg._geom(g), 1, 1, 0, tg.TG_BF16, *([fake] * 10))
+    for f in ("q", "k_new", "v_new", "kv_pool", "out"):
+        refused(tg._lib.tg_prefill, pre, f)
+
+    cmp = tg.tg_compress_args(tg._geom(g), 1, 8, tg.TG_BF16, fake, fake, fake, fake, fake, fake, 1, fake, fake,
+                              fake)
+    for f in ("k_new", "v_new", "kv_pool"):
+        refused(tg._lib.tg_compress, cmp, f)
+
+    app = tg.tg_append_args(tg._geom(g), 1, 0, tg.TG_BF16, *([fake] * 9))
+    for f in ("k_tok", "v_tok", "kv_pool"):
+        refused(tg._lib.tg_append, app, f)
+
+
 def test_read_probe_slab_sizes_checked_on_host():
     """tg_read_probe runs only the 2, 4 and 8 KiB slab kernels: every other slab size is refused before
     anything is enqueued, and an accepted size goes on to the remaining argument checks (here a zero
